@@ -1,0 +1,296 @@
+// Per-pixel 4-layer stack (a stack of 1x1 convolutions) of the latent
+// denoiser, fused into one kernel on fp32 MFMA (v_mfma_f32_32x32x2f32).
+//
+// Each wave owns a tile of 32 pixels of one sample and runs all four layers
+// on it with the activations held in registers.  Layers are computed
+// transposed, out^T = W h^T: the MFMA's M dimension is the output feature
+// and its N dimension the pixel, so the 32x32 accumulator of output block nb
+// holds, in lane l and register r, feature 32 nb + 8 (r/4) + 4 (l/32) + r%4
+// of pixel l%32.  The B operand of the next layer needs, in lane l, one
+// input feature of pixel l%32 per lane half -- exactly what a single
+// accumulator register already holds.  So register r of block b is used
+// unchanged as the B operand of k-step (b, r), and the weights are packed on
+// the host with the same permutation of the reduction index: k-step (b, r)
+// pairs input feature 32 b + 8 (r/4) + 4 h + r%4 with lane half h.  No
+// activation ever leaves the registers.
+//
+// v_mfma_f32_32x32x2f32 (wave64): A[i][k] in lane i + 32 k, B[k][j] in lane
+// j + 32 k, D[i][j] in lane j + 32 ((i/4) % 2), register (i%4) + 4 (i/8).
+//
+// Weights stream through LDS in slabs shared by the block's 4 waves, double
+// buffered: the next slab is copied global -> LDS by the gfx950 LDS-DMA path
+// (global_load_lds_dwordx4, no registers involved) while the current one
+// feeds the MFMAs.  Slab order: layer 1 (all of it), layer 2 one input block
+// at a time, layer 3 likewise, layer 4 (all of it, output rows padded to 32).
+// Inside a mid-layer slab for input block b, fragment (g, nb) of lane l holds
+// float4 {W[32 nb + l%32][32 b + 8 g + 4 (l/32) + q] : q = 0..3}, so one
+// ds_read_b128 feeds four MFMAs.
+#include "pd_internal.h"
+
+namespace pd {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f16v __attribute__((ext_vector_type(16)));
+
+template <int NB, int C>
+struct ConvLayout {
+    static constexpr int KS1 = C / 2;                 // layer-1 k-steps
+    static constexpr int SL1 = (NB * 64 * KS1 + 255) / 256 * 256;  // layer-1 slab, 1 KB multiple
+    static constexpr int SLM = 16 * NB * 64;          // floats in every other slab
+    static constexpr int NSLAB = 2 + 2 * NB;
+    static constexpr int TOTAL = SL1 + (2 * NB + 1) * SLM;
+    static constexpr __host__ __device__ int off(int i) { return i == 0 ? 0 : SL1 + (i - 1) * SLM; }
+    static constexpr __host__ __device__ int size(int i) { return i == 0 ? SL1 : SLM; }
+};
+
+__device__ __forceinline__ float silu(float v) {
+    return v * __builtin_amdgcn_rcpf(1.0f + __expf(-v));
+}
+
+template <int NB, int C>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
+    using L = ConvLayout<NB, C>;
+    __shared__ f4 lds[2][L::SLM / 4];
+
+    const int groups = src.active ? *src.active : src.max_groups;
+    const int64_t rows = (int64_t)groups * src.group;
+    const int64_t ntiles = rows * tiles_per_row;
+    if ((int64_t)blockIdx.x * 4 >= ntiles) return;          // uniform over the block
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int64_t tile = (int64_t)blockIdx.x * 4 + wave;
+    const bool active = tile < ntiles;
+    const int64_t tt = active ? tile : ntiles - 1;          // idle waves redo the last tile
+    const int64_t row = tt / tiles_per_row;
+    const int pt = (int)(tt % tiles_per_row);
+    const int g = (int)(row / src.group), bb = (int)(row % src.group);
+    const int64_t P = a.P;
+    const int64_t sl = src.slot ? src.slot[g] : g;
+    const float* x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
+    const int n = src.n[g];
+    const int64_t px = (int64_t)pt * 32 + (lane & 31);
+    const bool pxok = px < P;
+
+    // slab i -> LDS buffer `buf`: 1 KB per wave instruction, 16 B per lane
+    auto dma = [&](int i, int buf) {
+        const int nch = L::size(i) / 256;
+        // base and lane offset are made opaque at every call so the addresses
+        // are formed here as SGPR base + 32-bit lane offset (the saddr form)
+        // instead of being hoisted out of the branch loop into 64-bit VGPRs
+        const char* gb = reinterpret_cast<const char*>(a.frags);
+        uint32_t lo = (uint32_t)lane * 16u;
+        asm volatile("" : "+s"(gb), "+v"(lo));
+        float* ls = reinterpret_cast<float*>(lds[buf]);
+        for (int c = wave; c < nch; c += 4) {
+            const uint32_t ob = (uint32_t)(L::off(i) + c * 256) * 4u + lo;
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(gb + (size_t)ob),
+                (__attribute__((address_space(3))) void*)(ls + c * 256), 16, 0, 0);
+        }
+    };
+    auto land = [&]() {          // this wave's copies are in LDS, then all waves sync
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    };
+    // bias (or shift) for the 4 features of register group q4 of block nb
+    auto vec4 = [&](const float* v, int nb, int q4) -> f4 {
+        return *reinterpret_cast<const f4*>(v + 32 * nb + 8 * q4 + 4 * half);
+    };
+
+    // layer-1 input: B[k][pixel] for k = 2 s + half
+    float xin[L::KS1];
+#pragma unroll
+    for (int s = 0; s < L::KS1; ++s) xin[s] = pxok ? x[(2 * s + half) * P + px] : 0.f;
+
+    const int nbranch = a.shift_c ? 2 : 1;
+    float eu[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int br = 0; br < nbranch; ++br) {
+        const float* shift = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * a.width;
+        f16v acc[NB], H[NB];
+
+        // ---- layer 1: K = C (VALU-cheap, but kept on MFMA for the layout)
+        dma(0, 0);
+        land();
+        dma(1, 1);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            acc[nb] = f16v{};
+            const float* f1 = reinterpret_cast<const float*>(lds[0]) + (nb * 64 + lane) * L::KS1;
+#pragma unroll
+            for (int s = 0; s < L::KS1; ++s)
+                acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(f1[s], xin[s], acc[nb], 0, 0, 0);
+        }
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const f4 sh = vec4(shift, nb, q4);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) H[nb][4 * q4 + q] = silu(acc[nb][4 * q4 + q] + sh[q]);
+            }
+        land();
+
+        // ---- layers 2 and 3: one slab per input block
+#pragma unroll
+        for (int layer = 0; layer < 2; ++layer) {
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) acc[nb] = f16v{};
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const int slab = 1 + layer * NB + b;
+                const int buf = slab & 1;
+                dma(slab + 1, buf ^ 1);
+#pragma unroll
+                for (int g4 = 0; g4 < 4; ++g4)
+#pragma unroll
+                    for (int nb = 0; nb < NB; nb += 2) {
+                        // two output blocks at a time: two independent MFMA chains
+                        const f4 w0 = lds[buf][(g4 * NB + nb) * 64 + lane];
+                        const f4 w1 = nb + 1 < NB ? lds[buf][(g4 * NB + nb + 1) * 64 + lane] : f4{};
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                                w0[q], H[b][4 * g4 + q], acc[nb], 0, 0, 0);
+                            if (nb + 1 < NB)
+                                acc[nb + 1] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                                    w1[q], H[b][4 * g4 + q], acc[nb + 1], 0, 0, 0);
+                        }
+                    }
+                land();
+            }
+            const float* bias = layer == 0 ? a.b2 : a.b3;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const f4 bv = vec4(bias, nb, q4);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        H[nb][4 * q4 + q] = silu(acc[nb][4 * q4 + q] + bv[q]);
+                }
+        }
+
+        // ---- layer 4: C outputs (rows of a 32-row block), 4 chains of MFMAs
+        {
+            constexpr int slab = 1 + 2 * NB;
+            constexpr int buf = slab & 1;
+            f16v o4[4] = {f16v{}, f16v{}, f16v{}, f16v{}};
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int g4 = 0; g4 < 4; ++g4) {
+                    const f4 w = lds[buf][(b * 4 + g4) * 64 + lane];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        o4[g4] = __builtin_amdgcn_mfma_f32_32x32x2f32(w[q], H[b][4 * g4 + q],
+                                                                      o4[g4], 0, 0, 0);
+                }
+            __syncthreads();   // the next branch overwrites both buffers
+            const f16v o = (o4[0] + o4[1]) + (o4[2] + o4[3]);
+            // output channel c = 4 half + r (r < 4) of pixel lane%32
+            float* out = eps + row * (int64_t)C * P;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int c = 4 * half + r;
+                if (c < C) {
+                    const float v = o[r] + a.b4[c];
+                    if (br == 0) {
+                        eu[r] = v;
+                        if (nbranch == 1 && active && pxok) out[c * P + px] = v;
+                    } else if (active && pxok) {
+                        out[c * P + px] = eu[r] + a.guidance * (v - eu[r]);
+                    }
+                }
+            }
+        }
+    }
+}
+
+template <int NB, int C>
+void launch_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
+    const int tiles_per_row = (int)((a.P + 31) / 32);
+    const int64_t ntiles = (int64_t)src.max_groups * src.group * tiles_per_row;
+    if (ntiles == 0) return;
+    const int64_t blocks = (ntiles + 3) / 4;
+    hipLaunchKernelGGL((k_conv_f32<NB, C>), dim3((unsigned)blocks), dim3(256), 0, s, a, src, eps,
+                       tiles_per_row);
+    PD_HIP(hipGetLastError());
+}
+
+template <int NB, int C>
+void pack_t(const float* W1, const float* W2, const float* W3, const float* W4,
+            std::vector<uint8_t>& out) {
+    using L = ConvLayout<NB, C>;
+    constexpr int W = 32 * NB;
+    out.assign((size_t)L::TOTAL * sizeof(float), 0);
+    float* f = reinterpret_cast<float*>(out.data());
+    for (int nb = 0; nb < NB; ++nb)
+        for (int l = 0; l < 64; ++l)
+            for (int s = 0; s < L::KS1; ++s)
+                f[L::off(0) + (nb * 64 + l) * L::KS1 + s] = W1[(32 * nb + l % 32) * C + 2 * s + l / 32];
+    for (int layer = 0; layer < 2; ++layer) {
+        const float* Wm = layer == 0 ? W2 : W3;
+        for (int b = 0; b < NB; ++b) {
+            float* sl = f + L::off(1 + layer * NB + b);
+            for (int g4 = 0; g4 < 4; ++g4)
+                for (int nb = 0; nb < NB; ++nb)
+                    for (int l = 0; l < 64; ++l)
+                        for (int q = 0; q < 4; ++q)
+                            sl[((g4 * NB + nb) * 64 + l) * 4 + q] =
+                                Wm[(32 * nb + l % 32) * W + 32 * b + 8 * g4 + 4 * (l / 32) + q];
+        }
+    }
+    float* sl = f + L::off(1 + 2 * NB);
+    for (int b = 0; b < NB; ++b)
+        for (int g4 = 0; g4 < 4; ++g4)
+            for (int l = 0; l < 64; ++l)
+                for (int q = 0; q < 4; ++q)
+                    sl[((b * 4 + g4) * 64 + l) * 4 + q] =
+                        (l % 32 < C) ? W4[(l % 32) * W + 32 * b + 8 * g4 + 4 * (l / 32) + q] : 0.f;
+}
+
+#define PD_CONV_SHAPES(X) X(1, 4) X(2, 4) X(4, 4) X(10, 4)
+
+}  // namespace
+
+bool conv_supported(int C, int width, bool bf16) {
+    if (bf16) return false;
+#define X(nb, c) if (C == c && width == 32 * nb) return true;
+    PD_CONV_SHAPES(X)
+#undef X
+    return false;
+}
+
+size_t conv_frag_bytes(int C, int width, bool bf16) {
+#define X(nb, c) if (!bf16 && C == c && width == 32 * nb) return (size_t)ConvLayout<nb, c>::TOTAL * 4;
+    PD_CONV_SHAPES(X)
+#undef X
+    return 0;
+}
+
+void conv_pack_weights(int C, int width, bool bf16, const float* W1, const float* W2,
+                       const float* W3, const float* W4, std::vector<uint8_t>& out) {
+#define X(nb, c)                                          \
+    if (!bf16 && C == c && width == 32 * nb) {            \
+        pack_t<nb, c>(W1, W2, W3, W4, out);               \
+        return;                                           \
+    }
+    PD_CONV_SHAPES(X)
+#undef X
+    fail(PD_ERR_UNSUPPORTED, "conv1x1: unsupported channel count / width / dtype");
+}
+
+void launch_conv1x1(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
+#define X(nb, c)                                                   \
+    if (!a.bf16 && a.C == c && a.width == 32 * nb) {               \
+        launch_t<nb, c>(a, src, eps, s);                           \
+        return;                                                    \
+    }
+    PD_CONV_SHAPES(X)
+#undef X
+    fail(PD_ERR_UNSUPPORTED, "conv1x1: unsupported channel count / width / dtype");
+}
+
+}  // namespace pd

@@ -1,0 +1,115 @@
+// Internal declarations shared by the host runtime and the HIP kernels of
+// the gfx950 ParaDiGMS library.  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "paradigms.h"
+
+namespace pd {
+
+// ---------------------------------------------------------------- errors
+struct Error {
+    pd_status code;
+    std::string msg;
+};
+[[noreturn]] void fail(pd_status code, const std::string& msg);
+void hip_check(hipError_t e, const char* what);
+#define PD_HIP(call) ::pd::hip_check((call), #call)
+
+// ---------------------------------------------------------------- rows
+// Where the rows of one denoiser batch live.  Rows come in groups of `group`
+// consecutive rows (the samples of a batch at one trajectory point); group g
+// is read from base + slot[g] * slot_stride (slot == nullptr: slot[g] = g) and
+// row (g, b) from there + b * D.  n[g] is the network timestep of group g.
+// The number of groups to process is *active (device) or max_groups.
+struct RowSrc {
+    const float* base;
+    const int32_t* slot;
+    int64_t slot_stride;
+    int32_t group;
+    int32_t max_groups;
+    const int32_t* n;
+    const int32_t* active;
+};
+
+// Loop state of one Picard run, in device memory.
+struct LoopState {
+    int32_t t;       // window start
+    int32_t k;       // iterations done
+    int32_t f;       // frontier: highest trajectory index holding a computed point
+    int32_t p_eff;   // size of the current window; 0 once t >= T or after an error
+    int32_t status;  // PD_OK or PD_ERR_NUMERIC
+    int32_t pad;
+    int64_t evals;   // sum of window sizes
+};
+
+// ---------------------------------------------------------------- kernels
+// rng.hip
+void launch_normals(uint64_t seed, uint32_t rng_stream, int64_t count, const float* scale,
+                    int64_t per_scale, float* out, hipStream_t s);
+
+// gmm.hip: exact epsilon of an isotropic 2-D Gaussian mixture.
+struct GmmParams {
+    const float* means;   // [K][2]
+    const float* a;       // [T_train] sqrt(abar_n)
+    const float* inv2s2;  // [T_train] 1 / (2 s_n^2)
+    const float* coef;    // [T_train] sqrt(1 - abar_n) / s_n^2
+    int32_t K;
+};
+void launch_gmm_eps(const GmmParams& g, const RowSrc& src, float* eps, hipStream_t s);
+
+// mlp.hip: y = act(x W^T + bias [+ shift[n_row]]) with fp32 MFMA.
+enum Act { ACT_NONE = 0, ACT_GELU = 1 };
+struct LinearArgs {
+    const float* W;       // [N][K]
+    const float* bias;    // [N] (ignored when shift != nullptr)
+    const float* shift;   // [T_train][N] per-timestep shift, or nullptr
+    int32_t K, N;
+    int32_t act;
+};
+// rows from `src` (gathered, first layer) or from a dense [M][K] buffer.
+void launch_linear_gather(const LinearArgs& a, const RowSrc& src, int64_t D, float* y,
+                          hipStream_t s);
+void launch_linear_dense(const LinearArgs& a, const float* x, const RowSrc& rows, float* y,
+                         hipStream_t s);
+
+// conv.hip: per-pixel 4-layer stack with fp32 or bf16 MFMA.
+struct ConvArgs {
+    const void* frags;      // packed weight fragments (layout in conv.hip)
+    const float* shift_u;   // [T_train][W] b1 + e_n
+    const float* shift_c;   // [T_train][W] b1 + e_n + Wc c, or nullptr
+    const float* b2;
+    const float* b3;
+    const float* b4;
+    float guidance;
+    int32_t C;              // channels
+    int32_t width;          // hidden width W
+    int64_t P;              // pixels per sample
+    int32_t bf16;
+};
+size_t conv_frag_bytes(int C, int width, bool bf16);
+void conv_pack_weights(int C, int width, bool bf16, const float* W1, const float* W2,
+                       const float* W3, const float* W4, std::vector<uint8_t>& out);
+bool conv_supported(int C, int width, bool bf16);
+void launch_conv1x1(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s);
+
+// picard.hip
+void launch_picard_init(LoopState* st, int32_t* slot, int32_t* nrow, const int32_t* model_t,
+                        int T, int p, hipStream_t s);
+int picard_partial_blocks(int64_t D);
+void launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
+                        const float* A, const float* B, int p, int batch, int64_t D,
+                        float* partials, hipStream_t s);
+void launch_picard_finalize(LoopState* st, const float* partials, int p, int batch, int64_t D,
+                            int T, const float* tol_var, float tau2, int tol_offset,
+                            const int32_t* model_t, int32_t* trace, int32_t* slot,
+                            int32_t* nrow, hipStream_t s);
+void launch_seq_step(float* x, const float* eps, const float* z, float A, float B, int64_t n,
+                     hipStream_t s);
+
+}  // namespace pd

@@ -1,0 +1,82 @@
+// Up-front noise of Algorithm 1 (prior point and the noise of every step):
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11) with Box-Muller in double
+// precision.  One thread turns one 128-bit counter block into four normals.
+#include "pd_internal.h"
+
+namespace pd {
+namespace {
+
+constexpr uint32_t kPhiloxM0 = 0xD2511F53u;
+constexpr uint32_t kPhiloxM1 = 0xCD9E8D57u;
+constexpr uint32_t kPhiloxW0 = 0x9E3779B9u;
+constexpr uint32_t kPhiloxW1 = 0xBB67AE85u;
+
+__device__ __forceinline__ void philox4x32_10(uint32_t& c0, uint32_t& c1, uint32_t& c2,
+                                              uint32_t& c3, uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) {
+            k0 += kPhiloxW0;
+            k1 += kPhiloxW1;
+        }
+        const uint32_t lo0 = kPhiloxM0 * c0, hi0 = __umulhi(kPhiloxM0, c0);
+        const uint32_t lo1 = kPhiloxM1 * c2, hi1 = __umulhi(kPhiloxM1, c2);
+        const uint32_t n0 = hi1 ^ c1 ^ k0;
+        const uint32_t n2 = hi0 ^ c3 ^ k1;
+        c0 = n0;
+        c1 = lo1;
+        c2 = n2;
+        c3 = lo0;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_normals(uint64_t seed, uint32_t rng_stream,
+                                                 int64_t count, const float* __restrict__ scale,
+                                                 int64_t per_scale, float* __restrict__ out) {
+    const int64_t nq = (count + 3) / 4;
+    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+    const double kTwoPi = 6.283185307179586;   // 2 * pi in double
+    const double kInv32 = 2.3283064365386963e-10;   // 2^-32
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < nq; q += step) {
+        uint32_t c0 = (uint32_t)q, c1 = (uint32_t)((uint64_t)q >> 32), c2 = rng_stream, c3 = 0;
+        philox4x32_10(c0, c1, c2, c3, (uint32_t)seed, (uint32_t)(seed >> 32));
+        const double u0 = ((double)c0 + 0.5) * kInv32;
+        const double u1 = ((double)c1 + 0.5) * kInv32;
+        const double u2 = ((double)c2 + 0.5) * kInv32;
+        const double u3 = ((double)c3 + 0.5) * kInv32;
+        const double r01 = sqrt(-2.0 * log(u0));
+        const double r23 = sqrt(-2.0 * log(u2));
+        double s1, co1, s3, co3;
+        sincos(kTwoPi * u1, &s1, &co1);
+        sincos(kTwoPi * u3, &s3, &co3);
+        float v[4] = {(float)(r01 * co1), (float)(r01 * s1), (float)(r23 * co3), (float)(r23 * s3)};
+        const int64_t base = 4 * q;
+        if (scale != nullptr) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (base + e < count) v[e] = scale[(base + e) / per_scale] * v[e];
+        }
+        if (base + 3 < count && (count & 3) == 0) {
+            *reinterpret_cast<float4*>(out + base) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (base + e < count) out[base + e] = v[e];
+        }
+    }
+}
+
+}  // namespace
+
+void launch_normals(uint64_t seed, uint32_t rng_stream, int64_t count, const float* scale,
+                    int64_t per_scale, float* out, hipStream_t s) {
+    if (count <= 0) return;
+    const int64_t nq = (count + 3) / 4;
+    int64_t blocks = (nq + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(k_normals, dim3((unsigned)blocks), dim3(256), 0, s, seed, rng_stream,
+                       count, scale, per_scale, out);
+    PD_HIP(hipGetLastError());
+}
+
+}  // namespace pd

@@ -1,0 +1,622 @@
+// Host runtime of the gfx950 ParaDiGMS library: the C ABI of paradigms.h,
+// argument validation, schedule tables, denoiser weights on the device, the
+// sampling workspace and the two sampler loops.
+#include <cmath>
+#include <cstring>
+#include <exception>
+#include <memory>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "pd_internal.h"
+
+namespace pd {
+
+[[noreturn]] void fail(pd_status code, const std::string& msg) { throw Error{code, msg}; }
+
+void hip_check(hipError_t e, const char* what) {
+    if (e == hipSuccess) return;
+    const pd_status code = (e == hipErrorOutOfMemory) ? PD_ERR_OOM : PD_ERR_DEVICE;
+    fail(code, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+namespace {
+
+thread_local std::string g_last_error;
+
+template <class F>
+pd_status guard(F&& f) {
+    try {
+        f();
+        g_last_error.clear();
+        return PD_OK;
+    } catch (const Error& e) {
+        g_last_error = e.msg;
+        return e.code;
+    } catch (const std::bad_alloc&) {
+        g_last_error = "host allocation failed";
+        return PD_ERR_OOM;
+    } catch (const std::exception& e) {
+        g_last_error = e.what();
+        return PD_ERR_DEVICE;
+    } catch (...) {
+        g_last_error = "unknown error";
+        return PD_ERR_DEVICE;
+    }
+}
+
+void require(bool ok, const std::string& msg) {
+    if (!ok) fail(PD_ERR_INVALID_ARG, msg);
+}
+
+// Device buffer owned by a handle.
+struct DevBuf {
+    void* p = nullptr;
+    size_t bytes = 0;
+    DevBuf() = default;
+    DevBuf(const DevBuf&) = delete;
+    DevBuf& operator=(const DevBuf&) = delete;
+    ~DevBuf() {
+        if (p) (void)hipFree(p);
+    }
+    void alloc(size_t n) {
+        if (p) (void)hipFree(p);
+        p = nullptr;
+        bytes = n;
+        if (n == 0) return;
+        PD_HIP(hipMalloc(&p, n));
+    }
+    template <class T>
+    void upload(const T* src, size_t count) {
+        alloc(count * sizeof(T));
+        if (count) PD_HIP(hipMemcpy(p, src, count * sizeof(T), hipMemcpyHostToDevice));
+    }
+    template <class T>
+    T* as() const {
+        return static_cast<T*>(p);
+    }
+};
+
+int current_device() {
+    int n = 0;
+    const hipError_t e = hipGetDeviceCount(&n);
+    if (e != hipSuccess || n <= 0) fail(PD_ERR_DEVICE, "no HIP device is available");
+    int dev = 0;
+    PD_HIP(hipGetDevice(&dev));
+    hipDeviceProp_t prop;
+    PD_HIP(hipGetDeviceProperties(&prop, dev));
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        fail(PD_ERR_DEVICE, std::string("this library is built for gfx950, device is ") +
+                                prop.gcnArchName);
+    return dev;
+}
+
+std::vector<double> timestep_embedding(int n, int width) {
+    const int half = width / 2;
+    std::vector<double> e(width);
+    for (int k = 0; k < half; ++k) {
+        const double freq = std::exp(-std::log(10000.0) * (double)k / (double)half);
+        const double arg = (double)n * freq;
+        e[k] = std::sin(arg);
+        e[half + k] = std::cos(arg);
+    }
+    return e;
+}
+
+int64_t product(const int64_t* shape, int32_t ndim) {
+    int64_t D = 1;
+    for (int i = 0; i < ndim; ++i) D *= shape[i];
+    return D;
+}
+
+}  // namespace
+}  // namespace pd
+
+using namespace pd;
+
+// ============================================================== schedule
+struct pd_schedule {
+    pd_schedule_desc desc;
+    int T = 0, T_train = 0;
+    std::vector<float> A, B, noise_std, tol_var;
+    std::vector<int32_t> model_t;
+    std::vector<double> alphabar;
+    bool has_noise = false;
+};
+
+static void build_tables(pd_schedule& s) {
+    const pd_schedule_desc& d = s.desc;
+    const int Tt = d.T_train, T = d.T;
+    std::vector<double> beta(Tt), ab(Tt);
+    const double step = Tt > 1 ? (d.beta_end - d.beta_start) / (double)(Tt - 1) : 0.0;
+    double acc = 1.0;
+    for (int n = 0; n < Tt; ++n) {
+        beta[n] = d.beta_start + (double)n * step;
+        acc = acc * (1.0 - beta[n]);
+        ab[n] = acc;
+    }
+    s.T = T;
+    s.T_train = Tt;
+    s.alphabar = ab;
+    s.A.resize(T);
+    s.B.resize(T);
+    s.noise_std.resize(T);
+    s.tol_var.resize(T);
+    s.model_t.resize(T);
+    s.has_noise = false;
+    for (int i = 0; i < T; ++i) {
+        double A, B, var, tol;
+        int n;
+        if (d.kind == PD_DDPM) {
+            n = T - 1 - i;
+            const double a = 1.0 - beta[n];
+            const double ab_prev = n >= 1 ? ab[n - 1] : 1.0;
+            A = 1.0 / std::sqrt(a) - 1.0;
+            B = -beta[n] / (std::sqrt(a) * std::sqrt(1.0 - ab[n]));
+            var = beta[n] * (1.0 - ab_prev) / (1.0 - ab[n]);
+            tol = var;
+        } else {
+            const int c = Tt / T;
+            n = (T - 1 - i) * c;
+            const int npv = n - c;
+            const double ap = npv >= 0 ? ab[npv] : 1.0;
+            const double an = ab[n];
+            const double v1 = (1.0 - ap) / (1.0 - an) * (1.0 - an / ap);
+            const double s2 = d.eta * d.eta * v1;
+            A = std::sqrt(ap / an) - 1.0;
+            B = std::sqrt(1.0 - ap - s2) - std::sqrt(ap * (1.0 - an) / an);
+            var = s2;
+            tol = v1;
+        }
+        s.model_t[i] = n;
+        s.A[i] = (float)A;
+        s.B[i] = (float)B;
+        s.noise_std[i] = (float)std::sqrt(var);
+        s.tol_var[i] = (float)tol;
+        if (var > 0.0) s.has_noise = true;
+    }
+}
+
+extern "C" pd_status pd_init_schedule(const pd_schedule_desc* desc, pd_schedule** out) {
+    return guard([&] {
+        require(desc != nullptr && out != nullptr, "desc and out must not be NULL");
+        *out = nullptr;
+        const pd_schedule_desc& d = *desc;
+        require(d.kind == PD_DDPM || d.kind == PD_DDIM, "kind must be PD_DDPM or PD_DDIM");
+        require(d.T_train >= 2, "T_train must be >= 2");
+        require(d.T >= 1 && d.T <= d.T_train, "T must be in [1, T_train]");
+        require(d.kind != PD_DDPM || d.T == d.T_train, "DDPM needs T == T_train");
+        require(d.kind != PD_DDIM || d.T_train % d.T == 0, "DDIM needs T_train % T == 0");
+        require(std::isfinite(d.beta_start) && std::isfinite(d.beta_end) && d.beta_start > 0.0 &&
+                    d.beta_end < 1.0 && d.beta_start <= d.beta_end,
+                "need 0 < beta_start <= beta_end < 1");
+        require(d.kind != PD_DDIM || (d.eta >= 0.0 && d.eta <= 1.0), "eta must be in [0, 1]");
+        require(d.tol_index_offset == 0 || d.tol_index_offset == -1,
+                "tol_index_offset must be 0 or -1");
+        auto s = std::make_unique<pd_schedule>();
+        s->desc = d;
+        if (d.kind == PD_DDPM) s->desc.eta = 1.0;
+        build_tables(*s);
+        *out = s.release();
+    });
+}
+
+extern "C" void pd_destroy_schedule(pd_schedule* s) { delete s; }
+
+extern "C" pd_status pd_schedule_tables(const pd_schedule* s, int32_t* T, float* A, float* B,
+                                        float* noise_std, float* tol_var, int32_t* model_t) {
+    return guard([&] {
+        require(s != nullptr, "schedule must not be NULL");
+        if (T) *T = s->T;
+        const size_t n = (size_t)s->T;
+        if (A) std::memcpy(A, s->A.data(), n * sizeof(float));
+        if (B) std::memcpy(B, s->B.data(), n * sizeof(float));
+        if (noise_std) std::memcpy(noise_std, s->noise_std.data(), n * sizeof(float));
+        if (tol_var) std::memcpy(tol_var, s->tol_var.data(), n * sizeof(float));
+        if (model_t) std::memcpy(model_t, s->model_t.data(), n * sizeof(int32_t));
+    });
+}
+
+extern "C" const char* pd_last_error(void) { return g_last_error.c_str(); }
+extern "C" const char* pd_version(void) { return "paradigms-gfx950 0.1"; }
+
+// ============================================================== denoiser
+struct pd_denoiser {
+    pd_model_desc desc{};
+    std::vector<int64_t> shape;
+    int64_t D = 0, P = 0;
+    int C = 0, T_train = 0, device = 0;
+    // gmm2d
+    DevBuf means, g_a, g_inv2s2, g_coef;
+    // mlp
+    DevBuf W[4], bias[4], shift1;
+    // conv1x1
+    DevBuf frags, shift_u, shift_c;
+
+    bool guided() const { return desc.cond_dim > 0; }
+
+    size_t scratch_floats(int64_t rows) const {
+        return desc.kind == PD_MODEL_MLP ? (size_t)(2 * rows * desc.width) : 0;
+    }
+
+    void forward(const RowSrc& src, float* eps, float* scratch, hipStream_t s) const {
+        switch (desc.kind) {
+            case PD_MODEL_GMM2D: {
+                GmmParams g{means.as<float>(), g_a.as<float>(), g_inv2s2.as<float>(),
+                            g_coef.as<float>(), desc.n_components};
+                launch_gmm_eps(g, src, eps, s);
+                break;
+            }
+            case PD_MODEL_MLP: {
+                const int Wd = desc.width;
+                const int64_t rows = (int64_t)src.max_groups * src.group;
+                float* h1 = scratch;
+                float* h2 = scratch + rows * Wd;
+                LinearArgs l1{W[0].as<float>(), nullptr, shift1.as<float>(), (int)D, Wd, ACT_GELU};
+                LinearArgs l2{W[1].as<float>(), bias[1].as<float>(), nullptr, Wd, Wd, ACT_GELU};
+                LinearArgs l3{W[2].as<float>(), bias[2].as<float>(), nullptr, Wd, Wd, ACT_GELU};
+                LinearArgs l4{W[3].as<float>(), bias[3].as<float>(), nullptr, Wd, (int)D, ACT_NONE};
+                launch_linear_gather(l1, src, D, h1, s);
+                launch_linear_dense(l2, h1, src, h2, s);
+                launch_linear_dense(l3, h2, src, h1, s);
+                launch_linear_dense(l4, h1, src, eps, s);
+                break;
+            }
+            case PD_MODEL_CONV1X1: {
+                ConvArgs a{frags.p,           shift_u.as<float>(),
+                           guided() ? shift_c.as<float>() : nullptr,
+                           bias[1].as<float>(), bias[2].as<float>(), bias[3].as<float>(),
+                           desc.guidance,     C,
+                           desc.width,        P,
+                           desc.dtype == PD_BF16 ? 1 : 0};
+                launch_conv1x1(a, src, eps, s);
+                break;
+            }
+            default:
+                fail(PD_ERR_UNSUPPORTED, "unknown model kind");
+        }
+    }
+};
+
+static void create_denoiser(const pd_model_desc& m, const int64_t* shape, int32_t ndim,
+                            const float* const* w, int32_t nw, const pd_schedule& train,
+                            pd_denoiser& d) {
+    d.desc = m;
+    d.shape.assign(shape, shape + ndim);
+    d.D = product(shape, ndim);
+    d.T_train = train.T_train;
+    const int Tt = train.T_train;
+    if (m.kind == PD_MODEL_GMM2D) {
+        require(ndim == 1 && shape[0] == 2, "gmm2d samples have shape {2}");
+        require(m.n_components >= 1 && m.n_components <= 64, "gmm2d needs 1..64 components");
+        require(m.cond_dim == 0 && m.dtype == PD_F32, "gmm2d is unconditional float32");
+        require(nw == 2, "gmm2d takes 2 weight arrays (means, sigma0)");
+        d.device = current_device();
+        const double s0 = (double)w[1][0];
+        std::vector<float> a(Tt), inv2s2(Tt), coef(Tt);
+        for (int n = 0; n < Tt; ++n) {
+            const double ab = train.alphabar[n];
+            const double s2 = ab * (s0 * s0) + 1.0 - ab;
+            a[n] = (float)std::sqrt(ab);
+            inv2s2[n] = (float)(1.0 / (2.0 * s2));
+            coef[n] = (float)(std::sqrt(1.0 - ab) / s2);
+        }
+        d.means.upload(w[0], (size_t)2 * m.n_components);
+        d.g_a.upload(a.data(), a.size());
+        d.g_inv2s2.upload(inv2s2.data(), inv2s2.size());
+        d.g_coef.upload(coef.data(), coef.size());
+        return;
+    }
+    require(m.kind == PD_MODEL_MLP || m.kind == PD_MODEL_CONV1X1, "unknown model kind");
+    require(m.width >= 2 && m.width % 2 == 0, "width must be even and >= 2");
+    require(m.cond_dim >= 0, "cond_dim must be >= 0");
+    require(m.dtype == PD_F32 || m.dtype == PD_BF16, "dtype must be PD_F32 or PD_BF16");
+    const int Wd = m.width;
+    int Din;
+    if (m.kind == PD_MODEL_MLP) {
+        require(m.cond_dim == 0, "guidance is implemented for conv1x1 only");
+        require(m.dtype == PD_F32, "the mlp denoiser is float32");
+        require(d.D % 4 == 0 && Wd % 4 == 0, "mlp sizes must be multiples of 4");
+        Din = (int)d.D;
+    } else {
+        require(ndim == 3, "conv1x1 samples have shape {C, H, W}");
+        d.C = (int)shape[0];
+        d.P = shape[1] * shape[2];
+        require(d.C >= 1 && d.P >= 1, "empty conv1x1 sample shape");
+        if (!conv_supported(d.C, Wd, m.dtype == PD_BF16))
+            fail(PD_ERR_UNSUPPORTED, "conv1x1: this channel count / width / dtype is not built");
+        Din = d.C;
+    }
+    const int nexp = 8 + (m.cond_dim > 0 ? 2 : 0);
+    require(nw == nexp, "wrong number of weight arrays");
+    for (int i = 0; i < nw; ++i) require(w[i] != nullptr, "weight array is NULL");
+    if (m.cond_dim > 0) require(std::isfinite(m.guidance), "guidance must be finite");
+    d.device = current_device();
+
+    // first-layer shift b1 + e_n for every network timestep (float adds)
+    std::vector<float> sh((size_t)Tt * Wd);
+    for (int n = 0; n < Tt; ++n) {
+        const std::vector<double> e = timestep_embedding(n, Wd);
+        for (int k = 0; k < Wd; ++k) sh[(size_t)n * Wd + k] = w[1][k] + (float)e[k];
+    }
+    const float* W1 = w[0];
+    const float* W2 = w[2];
+    const float* W3 = w[4];
+    const float* W4 = w[6];
+    d.bias[1].upload(w[3], Wd);
+    d.bias[2].upload(w[5], Wd);
+    d.bias[3].upload(w[7], (size_t)Din);
+    if (m.kind == PD_MODEL_MLP) {
+        d.W[0].upload(W1, (size_t)Wd * Din);
+        d.W[1].upload(W2, (size_t)Wd * Wd);
+        d.W[2].upload(W3, (size_t)Wd * Wd);
+        d.W[3].upload(W4, (size_t)Din * Wd);
+        d.shift1.upload(sh.data(), sh.size());
+        return;
+    }
+    std::vector<uint8_t> packed;
+    conv_pack_weights(d.C, Wd, m.dtype == PD_BF16, W1, W2, W3, W4, packed);
+    d.frags.upload(packed.data(), packed.size());
+    d.shift_u.upload(sh.data(), sh.size());
+    if (m.cond_dim > 0) {
+        const float* Wc = w[8];
+        const float* c = w[9];
+        std::vector<float> wc(Wd);
+        for (int k = 0; k < Wd; ++k) {
+            double acc = 0.0;
+            for (int j = 0; j < m.cond_dim; ++j) acc += (double)Wc[(size_t)k * m.cond_dim + j] * c[j];
+            wc[k] = (float)acc;
+        }
+        std::vector<float> shc(sh.size());
+        for (int n = 0; n < Tt; ++n)
+            for (int k = 0; k < Wd; ++k) shc[(size_t)n * Wd + k] = sh[(size_t)n * Wd + k] + wc[k];
+        d.shift_c.upload(shc.data(), shc.size());
+    }
+}
+
+extern "C" pd_status pd_denoiser_create(const pd_model_desc* desc, const int64_t* sample_shape,
+                                        int32_t ndim, const float* const* weights,
+                                        int32_t n_weights, const pd_schedule* train,
+                                        pd_denoiser** out) {
+    return guard([&] {
+        require(desc && sample_shape && weights && train && out, "NULL argument");
+        *out = nullptr;
+        require(ndim >= 1 && ndim <= 8, "ndim must be in [1, 8]");
+        for (int i = 0; i < ndim; ++i) require(sample_shape[i] >= 1, "sample_shape entries must be >= 1");
+        require(n_weights >= 1, "no weights");
+        auto d = std::make_unique<pd_denoiser>();
+        create_denoiser(*desc, sample_shape, ndim, weights, n_weights, *train, *d);
+        *out = d.release();
+    });
+}
+
+extern "C" void pd_denoiser_destroy(pd_denoiser* d) { delete d; }
+
+extern "C" pd_status pd_denoiser_forward(const pd_denoiser* d, const float* x,
+                                         const int32_t* model_t, int64_t M, float* eps,
+                                         void* stream) {
+    return guard([&] {
+        require(d != nullptr, "denoiser must not be NULL");
+        require(M >= 0 && M <= (int64_t)1 << 30, "M out of range");
+        if (M == 0) return;
+        require(x && model_t && eps, "NULL device pointer");
+        const hipStream_t s = static_cast<hipStream_t>(stream);
+        const RowSrc src{x, nullptr, d->D, 1, (int32_t)M, model_t, nullptr};
+        const size_t sc = d->scratch_floats(M);
+        float* scratch = nullptr;
+        if (sc) PD_HIP(hipMallocAsync(reinterpret_cast<void**>(&scratch), sc * sizeof(float), s));
+        try {
+            d->forward(src, eps, scratch, s);
+        } catch (...) {
+            if (scratch) (void)hipFreeAsync(scratch, s);
+            throw;
+        }
+        if (scratch) PD_HIP(hipFreeAsync(scratch, s));
+    });
+}
+
+// ============================================================== noise
+extern "C" pd_status pd_normals(uint64_t seed, uint32_t rng_stream, int64_t count, float* out,
+                                void* stream) {
+    return guard([&] {
+        require(count >= 0, "count must be >= 0");
+        if (count == 0) return;
+        require(out != nullptr, "out must not be NULL");
+        launch_normals(seed, rng_stream, count, nullptr, 1, out, static_cast<hipStream_t>(stream));
+    });
+}
+
+// ============================================================== workspace
+struct pd_workspace {
+    int device = 0;
+    const pd_schedule* s = nullptr;
+    const pd_denoiser* d = nullptr;
+    int p = 0, batch = 0, T = 0;
+    int64_t D = 0;
+    DevBuf ring, eps, noise, A, B, zstd, tolv, model_t, state, trace, slot, nrow, partials, scratch;
+    LoopState* h_state = nullptr;
+    ~pd_workspace() {
+        if (h_state) (void)hipHostFree(h_state);
+    }
+};
+
+static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, int batch,
+                             pd_workspace& w) {
+    w.device = current_device();
+    require(w.device == d.device, "the denoiser lives on another device");
+    require(s.T_train == d.T_train, "schedule and denoiser disagree on T_train");
+    w.s = &s;
+    w.d = &d;
+    w.p = p;
+    w.batch = batch;
+    w.T = s.T;
+    w.D = d.D;
+    const int64_t BD = (int64_t)batch * d.D;
+    w.ring.alloc(sizeof(float) * (size_t)(p + 1) * BD);
+    w.eps.alloc(sizeof(float) * (size_t)p * BD);
+    if (s.has_noise) w.noise.alloc(sizeof(float) * (size_t)s.T * BD);
+    w.A.upload(s.A.data(), s.T);
+    w.B.upload(s.B.data(), s.T);
+    w.zstd.upload(s.noise_std.data(), s.T);
+    w.tolv.upload(s.tol_var.data(), s.T);
+    w.model_t.upload(s.model_t.data(), s.T);
+    w.state.alloc(sizeof(LoopState));
+    w.trace.alloc(sizeof(int32_t) * (size_t)s.T);
+    w.slot.alloc(sizeof(int32_t) * (size_t)p);
+    w.nrow.alloc(sizeof(int32_t) * (size_t)p);
+    w.partials.alloc(sizeof(float) * (size_t)picard_partial_blocks(d.D) * p * batch);
+    const size_t sc = d.scratch_floats((int64_t)p * batch);
+    if (sc) w.scratch.alloc(sc * sizeof(float));
+    PD_HIP(hipHostMalloc(reinterpret_cast<void**>(&w.h_state), sizeof(LoopState), hipHostMallocDefault));
+}
+
+extern "C" pd_status pd_workspace_create(const pd_schedule* s, const pd_denoiser* d, int32_t p,
+                                         int32_t batch, pd_workspace** out) {
+    return guard([&] {
+        require(s && d && out, "NULL argument");
+        *out = nullptr;
+        require(p >= 1, "p must be >= 1");
+        require(batch >= 1, "batch must be >= 1");
+        const int pc = p < s->T ? p : s->T;
+        auto w = std::make_unique<pd_workspace>();
+        create_workspace(*s, *d, pc, batch, *w);
+        *out = w.release();
+    });
+}
+
+extern "C" void pd_workspace_destroy(pd_workspace* w) { delete w; }
+
+// ============================================================== samplers
+static void check_sample_args(const pd_schedule* s, const pd_denoiser* d, int32_t batch,
+                              const int64_t* shape, int32_t ndim, const float* x_out) {
+    require(s && d, "schedule and denoiser must not be NULL");
+    require(batch >= 1, "batch must be >= 1");
+    require(shape != nullptr && ndim == (int32_t)d->shape.size(),
+            "sample_shape does not match the denoiser");
+    for (int i = 0; i < ndim; ++i)
+        require(shape[i] == d->shape[i], "sample_shape does not match the denoiser");
+    require(s->T_train == d->T_train, "schedule and denoiser disagree on T_train");
+    require(x_out != nullptr, "x_out must not be NULL");
+}
+
+static pd_workspace* use_workspace(pd_workspace* ws, std::unique_ptr<pd_workspace>& own,
+                                   const pd_schedule* s, const pd_denoiser* d, int p, int batch) {
+    if (ws) {
+        require(ws->s == s && ws->d == d && ws->batch == batch,
+                "workspace was made for another schedule, denoiser or batch");
+        require(ws->p >= p, "workspace window is smaller than p");
+        int dev = 0;
+        PD_HIP(hipGetDevice(&dev));
+        require(dev == ws->device, "workspace lives on another device");
+        return ws;
+    }
+    own = std::make_unique<pd_workspace>();
+    create_workspace(*s, *d, p, batch, *own);
+    return own.get();
+}
+
+static void draw_noise(pd_workspace& w, uint64_t seed, hipStream_t st) {
+    const int64_t BD = (int64_t)w.batch * w.D;
+    launch_normals(seed, 0, BD, nullptr, 1, w.ring.as<float>(), st);   // x_0 into slot 0
+    if (w.noise.p)
+        launch_normals(seed, 1, (int64_t)w.T * BD, w.zstd.as<float>(), BD, w.noise.as<float>(), st);
+}
+
+static void fill_stats(pd_sample_stats* stats, int iters, int64_t evals, int batch, bool guided,
+                       const int32_t* dtrace) {
+    if (!stats) return;
+    stats->iters = iters;
+    stats->evals_per_sample = evals;
+    stats->network_rows = evals * batch * (guided ? 2 : 1);
+    if (stats->stride_trace && stats->trace_cap > 0 && dtrace) {
+        const int n = iters < stats->trace_cap ? iters : stats->trace_cap;
+        if (n > 0)
+            PD_HIP(hipMemcpy(stats->stride_trace, dtrace, sizeof(int32_t) * n, hipMemcpyDeviceToHost));
+    }
+}
+
+extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoiser* d,
+                                          uint64_t noise_seed, int32_t batch,
+                                          const int64_t* sample_shape, int32_t ndim, float* x_out,
+                                          pd_sample_stats* stats, pd_workspace* ws, void* stream) {
+    return guard([&] {
+        check_sample_args(s, d, batch, sample_shape, ndim, x_out);
+        if (stats) require(stats->trace_cap >= 0, "trace_cap must be >= 0");
+        const hipStream_t st = static_cast<hipStream_t>(stream);
+        std::unique_ptr<pd_workspace> own;
+        pd_workspace& w = *use_workspace(ws, own, s, d, 1, batch);
+        const int64_t BD = (int64_t)batch * d->D;
+        float* x = w.ring.as<float>();
+        draw_noise(w, noise_seed, st);
+        for (int i = 0; i < s->T; ++i) {
+            const RowSrc src{x, nullptr, BD, batch, 1, w.model_t.as<int32_t>() + i, nullptr};
+            d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
+            const float* z = w.noise.p ? w.noise.as<float>() + (int64_t)i * BD : nullptr;
+            launch_seq_step(x, w.eps.as<float>(), z, s->A[i], s->B[i], BD, st);
+        }
+        PD_HIP(hipMemcpyAsync(x_out, x, sizeof(float) * BD, hipMemcpyDeviceToDevice, st));
+        PD_HIP(hipStreamSynchronize(st));
+        if (stats) {
+            fill_stats(stats, s->T, s->T, batch, d->guided(), nullptr);
+            const int n = s->T < stats->trace_cap ? s->T : stats->trace_cap;
+            for (int i = 0; i < n && stats->stride_trace; ++i) stats->stride_trace[i] = 1;
+        }
+    });
+}
+
+extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d, int32_t p,
+                                      float tau, uint64_t noise_seed, int32_t batch,
+                                      const int64_t* sample_shape, int32_t ndim, float* x_out,
+                                      pd_sample_stats* stats, pd_workspace* ws, void* stream) {
+    return guard([&] {
+        require(p >= 1, "p must be >= 1");
+        require(!std::isnan(tau) && tau >= 0.f, "tau must be >= 0 (inf allowed)");
+        check_sample_args(s, d, batch, sample_shape, ndim, x_out);
+        if (stats) require(stats->trace_cap >= 0, "trace_cap must be >= 0");
+        const int T = s->T;
+        const int pc = p < T ? p : T;
+        if (pc > 128) fail(PD_ERR_UNSUPPORTED, "windows larger than 128 points are not built");
+        const hipStream_t st = static_cast<hipStream_t>(stream);
+        std::unique_ptr<pd_workspace> own;
+        pd_workspace& w = *use_workspace(ws, own, s, d, pc, batch);
+        const int64_t BD = (int64_t)batch * d->D;
+        const float tau2 = tau * tau;
+        LoopState* dst = w.state.as<LoopState>();
+
+        draw_noise(w, noise_seed, st);
+        launch_picard_init(dst, w.slot.as<int32_t>(), w.nrow.as<int32_t>(),
+                           w.model_t.as<int32_t>(), T, pc, st);
+        const RowSrc src{w.ring.as<float>(), w.slot.as<int32_t>(), BD,     batch,
+                         pc,                 w.nrow.as<int32_t>(), &dst->p_eff};
+        int t_host = 0, issued = 0;
+        for (;;) {
+            // every iteration advances t by at most pc, so at least this many
+            // more are needed: enqueue them without looking at the device
+            const int need = (T - t_host + pc - 1) / pc;
+            for (int it = 0; it < need; ++it) {
+                d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
+                launch_picard_scan(dst, w.ring.as<float>(), w.eps.as<float>(), w.noise.as<float>(),
+                                   w.A.as<float>(), w.B.as<float>(), pc, batch, d->D,
+                                   w.partials.as<float>(), st);
+                launch_picard_finalize(dst, w.partials.as<float>(), pc, batch, d->D, T,
+                                       w.tolv.as<float>(), tau2, s->desc.tol_index_offset,
+                                       w.model_t.as<int32_t>(), w.trace.as<int32_t>(),
+                                       w.slot.as<int32_t>(), w.nrow.as<int32_t>(), st);
+            }
+            issued += need;
+            PD_HIP(hipMemcpyAsync(w.h_state, dst, sizeof(LoopState), hipMemcpyDeviceToHost, st));
+            PD_HIP(hipStreamSynchronize(st));
+            if (w.h_state->status != PD_OK) fail(PD_ERR_NUMERIC, "non-finite point or error in the window");
+            t_host = w.h_state->t;
+            if (t_host >= T) break;
+            if (issued > T) fail(PD_ERR_DEVICE, "Picard loop did not terminate within T iterations");
+        }
+        const int iters = w.h_state->k;
+        const int64_t evals = w.h_state->evals;
+        const float* xT = w.ring.as<float>() + (int64_t)(T % (pc + 1)) * BD;
+        PD_HIP(hipMemcpyAsync(x_out, xT, sizeof(float) * BD, hipMemcpyDeviceToDevice, st));
+        PD_HIP(hipStreamSynchronize(st));
+        fill_stats(stats, iters, evals, batch, d->guided(), w.trace.as<int32_t>());
+    });
+}

@@ -1,0 +1,127 @@
+"""CPU-side checks of the C ABI: the library loads, exports what the header
+declares, validates arguments without touching a device, reports a missing
+GPU, and builds schedule tables bitwise equal to the oracle's."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2305_16317_amd as pd
+from oracle import schedule as osched
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "paradigms.h")
+
+
+def _declared():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(pd_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_built_and_loads():
+    assert os.path.exists(pd.lib_path()), "run python -m paper_2305_16317_amd.build first"
+    L = pd.load()
+    assert L.pd_version().decode().startswith("paradigms-gfx950")
+
+
+def test_every_declared_symbol_is_exported():
+    L = pd.load()
+    decl = _declared()
+    assert set(decl) == set(pd.EXPORTED_SYMBOLS)
+    for name in decl:
+        assert hasattr(L, name), name
+
+
+def test_library_is_gfx950_only():
+    data = open(pd.lib_path(), "rb").read()
+    assert b"gfx950" in data
+    assert b"gfx942" not in data and b"gfx90a" not in data
+
+
+def _status(fn, *args):
+    code = fn(*args)
+    return code, pd.load().pd_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(kind=7), "kind"),
+    (dict(T_train=1, T=1), "T_train"),
+    (dict(T=0), "T must"),
+    (dict(T=50), "DDPM needs"),
+    (dict(kind=pd.PD_DDIM, T=300), "T_train % T"),
+    (dict(beta_start=0.0), "beta"),
+    (dict(beta_end=1.0), "beta"),
+    (dict(beta_start=0.03), "beta"),
+    (dict(beta_start=float("nan")), "beta"),
+    (dict(kind=pd.PD_DDIM, T=200, eta=1.5), "eta"),
+    (dict(tol_index_offset=2), "tol_index_offset"),
+])
+def test_schedule_validation(kw, msg):
+    args = dict(kind=pd.PD_DDPM, T_train=1000, T=1000, beta_start=1e-4, beta_end=0.02,
+                eta=0.0, tol_index_offset=0)
+    args.update(kw)
+    with pytest.raises(pd.PdError) as e:
+        pd.pd_init_schedule(**args)
+    assert e.value.code == pd.PD_ERR_INVALID_ARG and msg in str(e.value)
+
+
+@pytest.mark.parametrize("spec", [("ddpm", 1000, 1000, 0.0), ("ddpm", 100, 100, 0.0),
+                                  ("ddim", 1000, 200, 0.0), ("ddim", 1000, 50, 0.7),
+                                  ("ddpm", 2, 2, 0.0)])
+def test_schedule_tables_bitwise_equal_oracle(spec):
+    kind, Tt, T, eta = spec
+    s = pd.pd_init_schedule(pd.PD_DDPM if kind == "ddpm" else pd.PD_DDIM, Tt, T, eta=eta)
+    tb = s.tables()
+    ref = osched.ddpm(T) if kind == "ddpm" else osched.ddim(Tt, T, eta)
+    A, B, zs, tv = ref.as_dtype(np.float32)
+    for name, ours, theirs in (("A", tb["A"], A), ("B", tb["B"], B),
+                               ("noise_std", tb["noise_std"], zs), ("tol_var", tb["tol_var"], tv)):
+        assert np.array_equal(ours.view(np.uint32), theirs.view(np.uint32)), name
+    assert np.array_equal(tb["model_t"], ref.model_t)
+
+
+def test_null_and_range_arguments_rejected_without_device():
+    L = pd.load()
+    out = ctypes.c_void_p()
+    assert _status(L.pd_init_schedule, None, ctypes.byref(out))[0] == pd.PD_ERR_INVALID_ARG
+    assert _status(L.pd_normals, 0, 0, -1, None, None)[0] == pd.PD_ERR_INVALID_ARG
+    assert _status(L.pd_normals, 0, 0, 5, None, None)[0] == pd.PD_ERR_INVALID_ARG
+    assert _status(L.pd_normals, 0, 0, 0, None, None)[0] == pd.PD_OK        # empty is a no-op
+    assert _status(L.pd_denoiser_forward, None, None, None, 4, None, None)[0] == pd.PD_ERR_INVALID_ARG
+    s = pd.pd_init_schedule(pd.PD_DDPM, 10, 10)
+    shp = (ctypes.c_int64 * 1)(2)
+    st = pd._Stats()
+    for p, tau, msg in ((0, 0.1, "p must"), (4, -1.0, "tau"), (4, float("nan"), "tau")):
+        code, m = _status(L.pd_sample_picard, s.handle, None, p, tau, 0, 1, shp, 1, None,
+                          ctypes.byref(st), None, None)
+        assert code == pd.PD_ERR_INVALID_ARG and msg in m
+    code, m = _status(L.pd_sample_picard, s.handle, None, 4, 0.1, 0, 1, shp, 1, None,
+                      ctypes.byref(st), None, None)
+    assert code == pd.PD_ERR_INVALID_ARG and "NULL" in m
+    code, m = _status(L.pd_sample_sequential, None, None, 0, 1, shp, 1, None, None, None, None)
+    assert code == pd.PD_ERR_INVALID_ARG
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-GPU path")
+def test_missing_gpu_reported_as_device_error():
+    s = pd.pd_init_schedule(pd.PD_DDPM, 10, 10)
+    w = {"means": np.zeros((8, 2), np.float32), "sigma0": np.ones(1, np.float32)}
+    with pytest.raises(pd.PdError) as e:
+        pd.pd_denoiser_create(pd.PD_MODEL_GMM2D, (2,), w, s)
+    assert e.value.code == pd.PD_ERR_DEVICE
+
+
+def test_denoiser_argument_validation_precedes_device():
+    s = pd.pd_init_schedule(pd.PD_DDPM, 10, 10)
+    w = {"means": np.zeros((8, 2), np.float32), "sigma0": np.ones(1, np.float32)}
+    with pytest.raises(pd.PdError) as e:
+        pd.pd_denoiser_create(pd.PD_MODEL_GMM2D, (3,), w, s)       # gmm2d is 2-D
+    assert e.value.code == pd.PD_ERR_INVALID_ARG
+    conv = {k: np.zeros((4, 4), np.float32) for k in pd.WEIGHT_ORDER[pd.PD_MODEL_CONV1X1]}
+    with pytest.raises(pd.PdError) as e:
+        pd.pd_denoiser_create(pd.PD_MODEL_CONV1X1, (4, 8, 8), conv, s, width=96)
+    assert e.value.code == pd.PD_ERR_UNSUPPORTED

@@ -1,0 +1,278 @@
+"""Device path vs oracle, element by element on the same seeded inputs.
+
+Bars: bit-exact for integers (iteration counts, strides, evaluation counts);
+relative L2 <= 1e-5 for float32 results; the generated normals equal the
+oracle's up to a handful of one-ulp roundings (Box-Muller runs in double on
+both sides with different libm implementations, then rounds once to float).
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2305_16317_amd as pd
+import workloads as W
+from oracle import Problem, denoisers, philox, schedule
+
+pytestmark = pytest.mark.gpu
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+REL_F32 = 1e-5
+
+
+def _dev(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    return t.to(device="cuda", dtype=dtype) if dtype else t.cuda()
+
+
+def _rel(a, b):
+    a = np.asarray(a, np.float64); b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    pd.load()
+
+
+# ------------------------------------------------------------------ normals
+@pytest.mark.parametrize("seed,stream,count", [(0, 0, 1), (0, 0, 7), (3, 1, 4096),
+                                               (1 << 33, 1, 1_000_003), (12345, 0, 36_864)])
+def test_normals_match_oracle(seed, stream, count):
+    out = torch.empty(count, device="cuda")
+    pd.pd_normals(seed, stream, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    ref = philox.normals(seed, stream, count)
+    diff = got.view(np.int32).astype(np.int64) - ref.view(np.int32).astype(np.int64)
+    assert np.abs(diff).max() <= 1
+    assert np.count_nonzero(diff) <= max(2, count // 1_000_000 + 2)
+
+
+# ------------------------------------------------------------------ denoisers
+def _forward(wl, weights, x, n):
+    sched, den = pd.from_workload(wl, weights)
+    M = x.shape[0]
+    eps = torch.empty((M, wl.model.D), device="cuda")
+    pd.pd_denoiser_forward(den, _dev(x.reshape(M, -1)), _dev(n, torch.int32), eps)
+    torch.cuda.synchronize()
+    return eps.cpu().numpy()
+
+
+def _oracle_eps(wl, weights, x, n, bf16=None):
+    tb = schedule.from_spec(wl.schedule)
+    f = denoisers.Denoiser(wl.model, weights, tb.alphabar, np.float32, bf16)
+    return f(x.reshape(x.shape[0], -1) if wl.model.kind != "conv1x1" else x, n).reshape(x.shape[0], -1)
+
+
+def _wl(kind, shape, width=0, T=100, cond=0, dtype="f32", seed=1):
+    sch = W.ScheduleSpec("ddpm", T, T)
+    m = W.ModelSpec(kind, tuple(shape), width=width, cond_dim=cond, guidance=7.5,
+                    dtype=dtype, weight_seed=seed, cond_seed=seed + 1)
+    return W.Workload("t", sch, m, p=8, tau=0.1)
+
+
+@pytest.mark.parametrize("M", [1, 5, 1000])
+def test_gmm_forward(M):
+    wl = W.WORKLOADS["gmm2d_ddpm100"]
+    w = W.make_weights(wl.model)
+    rng = np.random.default_rng(M)
+    x = (rng.standard_normal((M, 2)) * 3).astype(np.float32)
+    n = rng.integers(0, 100, M).astype(np.int32)
+    got = _forward(wl, w, x, n)
+    ref = _oracle_eps(wl, w, x, n)
+    assert _rel(got, ref) <= REL_F32
+    assert np.allclose(got, ref, rtol=1e-4, atol=1e-5)
+
+
+@pytest.mark.parametrize("shape,width,M", [((4, 3), 32, 3), ((4, 3), 32, 37), ((16, 10), 1024, 100),
+                                           ((16, 10), 1024, 1)])
+def test_mlp_forward(shape, width, M):
+    wl = _wl("mlp", shape, width)
+    w = W.make_weights(wl.model)
+    rng = np.random.default_rng(M)
+    x = rng.standard_normal((M, int(np.prod(shape)))).astype(np.float32)
+    n = rng.integers(0, 100, M).astype(np.int32)
+    got = _forward(wl, w, x, n)
+    ref = _oracle_eps(wl, w, x, n)
+    assert _rel(got, ref) <= REL_F32
+
+
+@pytest.mark.parametrize("shape,width,M,cond", [
+    ((4, 8, 8), 32, 3, 0),        # two full pixel tiles per row
+    ((4, 6, 7), 64, 5, 0),        # ragged last tile (42 pixels)
+    ((4, 5, 5), 128, 2, 0),
+    ((4, 16, 16), 320, 7, 0),     # production width, 8 tiles per row, idle waves
+    ((4, 96, 96), 320, 2, 0),     # production shape
+    ((4, 6, 6), 64, 3, 24),       # classifier-free guidance, w = 7.5
+])
+def test_conv1x1_forward(shape, width, M, cond):
+    wl = _wl("conv1x1", shape, width, T=1000, cond=cond)
+    w = W.make_weights(wl.model)
+    rng = np.random.default_rng(M + width)
+    x = rng.standard_normal((M,) + shape).astype(np.float32)
+    n = rng.integers(0, 1000, M).astype(np.int32)
+    got = _forward(wl, w, x, n)
+    ref = _oracle_eps(wl, w, x, n)
+    assert _rel(got, ref) <= REL_F32
+
+
+def test_forward_empty_batch_is_noop():
+    wl = _wl("conv1x1", (4, 8, 8), 32, T=10)
+    sched, den = pd.from_workload(wl, W.make_weights(wl.model))
+    e = torch.full((1, 256), 7.0, device="cuda")
+    pd.pd_denoiser_forward(den, torch.empty((0, 256), device="cuda"),
+                           torch.empty(0, dtype=torch.int32, device="cuda"), e)
+    torch.cuda.synchronize()
+    assert torch.all(e == 7.0)
+
+
+# ------------------------------------------------------------------ samplers
+def _run(wl, weights, sampler="picard", p=None, tau=None, workspace=None, seed=None):
+    sched, den = pd.from_workload(wl, weights)
+    x = torch.empty(wl.batch * wl.model.D, device="cuda")
+    seed = wl.noise_seed if seed is None else seed
+    if sampler == "picard":
+        st = pd.pd_sample_picard(sched, den, wl.p if p is None else p,
+                                 wl.tau if tau is None else tau, seed, wl.batch,
+                                 wl.model.sample_shape, x, workspace=workspace)
+    else:
+        st = pd.pd_sample_sequential(sched, den, seed, wl.batch, wl.model.sample_shape, x,
+                                     workspace=workspace)
+    torch.cuda.synchronize()
+    return x.cpu().numpy().reshape(wl.batch, -1), st
+
+
+SMALL = {
+    "gmm_full": lambda: W.WORKLOADS["gmm2d_ddpm100"],
+    "gmm_p7_b3": lambda: W.small_variant("gmm2d_ddpm100", p=7, batch=3),
+    "mlp_full": lambda: W.WORKLOADS["policy_mlp_ddpm100"],
+    "mlp_small": lambda: W.small_variant("policy_mlp_ddpm100", T=30, p=9, shape=(4, 3), width=32, batch=2),
+    "conv_ddpm": lambda: W.small_variant("latent_ddpm1000_p64", T=40, p=16, shape=(4, 16, 16), width=64),
+    "conv_ddpm_w320": lambda: W.small_variant("latent_ddpm1000_p64", T=60, p=32, shape=(4, 8, 12), width=320),
+    "conv_ddim_b3": lambda: W.small_variant("latent_ddim200_b4", T=30, p=8, shape=(4, 6, 7), width=32, batch=3),
+    "conv_p128": lambda: W.small_variant("latent_ddpm1000_p64", T=200, p=128, shape=(4, 4, 8), width=32),
+    "conv_p_clamped": lambda: W.small_variant("latent_ddpm1000_p64", T=20, p=500, shape=(4, 4, 8), width=32),
+    "conv_cfg_f32": lambda: W.Workload("cfg", W.ScheduleSpec("ddpm", 50, 50),
+                                       W.ModelSpec("conv1x1", (4, 8, 8), width=64, cond_dim=24,
+                                                   guidance=7.5), p=16, tau=0.1),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_picard_matches_oracle(name):
+    wl = SMALL[name]()
+    w = W.make_weights(wl.model)
+    got, st = _run(wl, w)
+    pr = Problem(wl, w, np.float32)
+    ref = pr.picard()
+    assert (st.iters, st.trace, st.evals_per_sample) == (ref.iters, ref.trace, ref.evals)
+    assert st.network_rows == ref.evals * wl.batch * (2 if wl.model.cond_dim else 1)
+    assert _rel(got, ref.x) <= REL_F32, _rel(got, ref.x)
+
+
+@pytest.mark.parametrize("name", ["gmm_p7_b3", "mlp_small", "conv_ddpm", "conv_ddim_b3"])
+def test_sequential_matches_oracle(name):
+    wl = SMALL[name]()
+    w = W.make_weights(wl.model)
+    got, st = _run(wl, w, "sequential")
+    ref = Problem(wl, w, np.float32).sequential()
+    assert st.iters == wl.schedule.T and st.evals_per_sample == wl.schedule.T
+    assert _rel(got, ref) <= REL_F32
+
+
+@pytest.mark.parametrize("name", ["gmm_p7_b3", "mlp_small", "conv_ddpm", "conv_ddim_b3"])
+def test_window_of_one_is_sequential_bitwise(name):
+    wl = SMALL[name]()
+    w = W.make_weights(wl.model)
+    a, st = _run(wl, w, "picard", p=1)
+    b, _ = _run(wl, w, "sequential")
+    assert st.iters == wl.schedule.T and st.trace == [1] * wl.schedule.T
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_runs_are_deterministic_and_workspace_reuse():
+    wl = SMALL["conv_ddpm"]()
+    w = W.make_weights(wl.model)
+    a, sa = _run(wl, w)
+    b, sb = _run(wl, w)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32)) and sa == sb
+    sched, den = pd.from_workload(wl, w)
+    ws = pd.pd_workspace_create(sched, den, wl.p, wl.batch)
+    for seed in (5, 0):
+        x = torch.empty(wl.model.D, device="cuda")
+        st = pd.pd_sample_picard(sched, den, wl.p, wl.tau, seed, 1, wl.model.sample_shape, x,
+                                 workspace=ws)
+        torch.cuda.synchronize()
+    assert np.array_equal(x.cpu().numpy().reshape(1, -1).view(np.uint32), a.view(np.uint32))
+    assert st == sa
+
+
+def test_infinite_tolerance_single_sweeps():
+    wl = SMALL["conv_ddpm"]()
+    w = W.make_weights(wl.model)
+    got, st = _run(wl, w, tau=float("inf"))
+    ref = Problem(wl, w, np.float32).picard(tau=float("inf"))
+    assert st.trace == ref.trace
+    assert _rel(got, ref.x) <= REL_F32
+
+
+def test_non_finite_reports_numeric_error():
+    wl = SMALL["conv_ddpm"]()
+    w = W.make_weights(wl.model)
+    w["b4"] = w["b4"].copy()
+    w["b4"][1] = np.float32(np.inf)
+    with pytest.raises(pd.PdError) as e:
+        _run(wl, w)
+    assert e.value.code == pd.PD_ERR_NUMERIC
+
+
+def test_workspace_mismatch_rejected():
+    wl = SMALL["conv_ddpm"]()
+    w = W.make_weights(wl.model)
+    sched, den = pd.from_workload(wl, w)
+    ws = pd.pd_workspace_create(sched, den, 4, 1)
+    x = torch.empty(wl.model.D, device="cuda")
+    with pytest.raises(pd.PdError) as e:
+        pd.pd_sample_picard(sched, den, 16, 0.1, 0, 1, wl.model.sample_shape, x, workspace=ws)
+    assert e.value.code == pd.PD_ERR_INVALID_ARG
+
+
+# ------------------------------------------------------------ full-size workloads
+def _golden(name):
+    path = os.path.join(HERE, "golden", f"{name}.json")
+    if not os.path.exists(path):
+        pytest.fail(f"{path} missing: run tests/golden/make_golden.py {name}")
+    return json.load(open(path))
+
+
+def _check_summary(got, g, tol):
+    flat = got.reshape(-1).astype(np.float32)
+    vals = flat[np.asarray(g["idx"])]
+    assert _rel(vals, g["values"]) <= tol, _rel(vals, g["values"])
+    n2 = float(np.sum(flat.astype(np.float64) ** 2))
+    assert abs(math.sqrt(n2) - math.sqrt(g["norm2"])) <= tol * math.sqrt(g["norm2"])
+
+
+@pytest.mark.parametrize("name", ["gmm2d_ddpm100", "policy_mlp_ddpm100", "latent_ddpm1000_p64",
+                                  "latent_ddim200_b4"])
+def test_full_size_picard_matches_oracle(name):
+    g = _golden(name)
+    wl = W.WORKLOADS[name]
+    got, st = _run(wl, W.make_weights(wl.model))
+    gp = g["picard"]
+    assert (st.iters, st.trace, st.evals_per_sample) == (gp["iters"], gp["trace"], gp["evals"])
+    _check_summary(got, gp, REL_F32)
+
+
+@pytest.mark.parametrize("name", ["gmm2d_ddpm100", "policy_mlp_ddpm100", "latent_ddpm1000_p64"])
+def test_full_size_sequential_matches_oracle(name):
+    g = _golden(name)
+    wl = W.WORKLOADS[name]
+    got, st = _run(wl, W.make_weights(wl.model), "sequential")
+    _check_summary(got, g["sequential"], REL_F32)
