@@ -1,0 +1,225 @@
+"""Benchmark of the ParaDiGMS hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--no-cpu-baseline] [--no-sequential]
+
+One step = one full ParaDiGMS sample (Algorithm 1: up-front noise, then
+Picard iterations of batched denoiser + fused scan/error + on-device slide
+until the window passes T) of the named synthetic workload, inputs resident
+on the GPU.  Step s uses noise seed s, so the iteration count K varies over
+the steps as it does over samples.  Prints one JSON line:
+
+  value        denoiser evaluations (network rows) per second, whole job
+  ms_per_step  sample latency in ms (mean over the timed steps)
+  roofline     the dominant kernel (the denoiser, fp32 MFMA): algorithmic
+               FLOPs per launch over its mean event-timed duration
+  roofline_update  the Picard update (scan + error partials), HBM-bound
+  cpu_baseline the CPU oracle (float32 NumPy) timed on a bounded sample of the
+               same workload on this host
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "sample latency (ms) + denoiser evals/s at T=1000, p=64; % HBM / MFMA peak"
+PEAK = {"f32": 157.3e12, "bf16": 2.5e15}       # dense MFMA FLOP/s, MI355X
+HBM_PEAK = 8.0e12                              # bytes/s
+
+
+def flops_per_row(model) -> float:
+    """Algorithmic matmul FLOPs of one network row (one full sample)."""
+    if model.kind == "conv1x1":
+        C, W = model.sample_shape[0], model.width
+        P = model.sample_shape[1] * model.sample_shape[2]
+        return 2.0 * P * (C * W + W * W + W * W + W * C)
+    if model.kind == "mlp":
+        D, W = model.D, model.width
+        return 2.0 * (D * W + W * W + W * W + W * D)
+    return 0.0
+
+
+def update_bytes(wl, p_eff_sum: int, has_noise: bool) -> float:
+    """Algorithmic HBM bytes of the Picard update summed over launches:
+    per window point and column, read x^k and eps (and z), write x^{k+1}."""
+    per = 4 * (3 + (1 if has_noise else 0))
+    return float(per) * wl.batch * wl.model.D * p_eff_sum
+
+
+def _source_hash() -> str:
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2305_16317_amd", "csrc"))):
+        h.update(open(os.path.join(ROOT, "paper_2305_16317_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profiles(kernel_tag: str):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, or None
+    if they are missing or were taken on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path))
+        e = d.get(kernel_tag)
+        if not e or e.get("source_hash") != _source_hash():
+            return None
+        return e["bytes_per_launch"]
+    except Exception:
+        return None
+
+
+def cpu_baseline(wl, weights, budget_s: float):
+    """Oracle Picard iterations on the host until the time budget is spent."""
+    import numpy as np
+    from oracle import Problem
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    pr = Problem(wl, weights, np.float32)
+    setup = time.perf_counter() - t0
+    done = {"rows": 0, "iters": 0}
+
+    class _Stop(Exception):
+        pass
+
+    def on_iter(k, t, pe, xo, xn, err, stride):
+        done["rows"] += pe * wl.batch * (2 if wl.model.cond_dim else 1)
+        done["iters"] += 1
+        if time.perf_counter() - t1 > budget_s:
+            raise _Stop()
+
+    t1 = time.perf_counter()
+    try:
+        pr.picard(on_iter=on_iter)
+    except _Stop:
+        pass
+    el = time.perf_counter() - t1
+    return {"value": done["rows"] / el, "unit": "denoiser evals/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": (f"first {done['iters']} Picard iterations ({done['rows']} network rows) "
+                       f"of {wl.name}, float32 NumPy oracle, {el:.1f} s "
+                       f"(+{setup:.1f} s noise setup not counted)")}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="latent_ddpm1000_p64")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sequential", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    a = ap.parse_args()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only: --gpus {a.gpus} is not supported "
+              "(the window is not split across GPUs in this build)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2305_16317_amd as pd
+    import workloads as W
+
+    wl = W.WORKLOADS[a.workload]
+    weights = W.make_weights(wl.model)
+    sched, den = pd.from_workload(wl, weights)
+    ws = pd.pd_workspace_create(sched, den, wl.p, wl.batch)
+    x = torch.empty(wl.batch * wl.model.D, device="cuda")
+    shape = wl.model.sample_shape
+    stream = torch.cuda.current_stream()
+
+    for s in range(a.warmup):
+        pd.pd_sample_picard(sched, den, wl.p, wl.tau, 1000 + s, wl.batch, shape, x, workspace=ws)
+    torch.cuda.synchronize()
+
+    stats = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(a.steps):
+        stats.append(pd.pd_sample_picard(sched, den, wl.p, wl.tau, s, wl.batch, shape, x,
+                                         workspace=ws, stream=stream, time_kernels=True))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    rows = sum(st.network_rows for st in stats)
+    evals = sum(st.evals_per_sample for st in stats)
+    value = rows / elapsed
+    ms_per_step = 1e3 * elapsed / a.steps
+    den_ms = sum(st.kernel_times["denoiser_ms"] for st in stats)
+    den_n = sum(st.kernel_times["denoiser_launches"] for st in stats)
+    upd_ms = sum(st.kernel_times["update_ms"] for st in stats)
+    upd_n = sum(st.kernel_times["update_launches"] for st in stats)
+    fin_ms = sum(st.kernel_times["finalize_ms"] for st in stats)
+    dtype = "bf16" if wl.model.dtype == "bf16" else "f32"
+    fl = flops_per_row(wl.model) * rows
+    achieved = fl / (den_ms * 1e-3) if den_ms > 0 else 0.0
+    has_noise = bool(np.any(sched.tables()["noise_std"] > 0))
+    ub = update_bytes(wl, evals, has_noise)
+    upd_rate = ub / (upd_ms * 1e-3) if upd_ms > 0 else 0.0
+    traffic = traffic_from_profiles("k_conv_f32" if dtype == "f32" else "k_conv_bf16")
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "denoiser evals/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic (seeded Xavier weights, Philox noise; no trained model or dataset)",
+        "config": {"workload": wl.name, "sampler": "ParaDDPM" if wl.schedule.kind == "ddpm" else "ParaDDIM",
+                   "T": wl.schedule.T, "p": wl.p, "tau": wl.tau, "batch": wl.batch,
+                   "sample_shape": list(shape), "denoiser_width": wl.model.width,
+                   "guidance": wl.model.guidance if wl.model.cond_dim else None,
+                   "noise_seeds": f"0..{a.steps - 1}"},
+        "latency_ms": ms_per_step,
+        "iters_K": [st.iters for st in stats],
+        "evals_per_sample": [st.evals_per_sample for st in stats],
+        "roofline": {"bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK[dtype] / 1e12,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK[dtype],
+                     "traffic": traffic, "kernel": f"k_conv_{dtype}",
+                     "flops_per_launch": fl / max(den_n, 1),
+                     "mean_launch_ms": den_ms / max(den_n, 1), "launches": den_n},
+        "roofline_update": {"bound": "hbm", "achieved": upd_rate / 1e9, "peak": HBM_PEAK / 1e9,
+                            "unit": "GB/s", "frac": upd_rate / HBM_PEAK, "traffic": None,
+                            "kernel": "k_picard_scan", "bytes_per_launch": ub / max(upd_n, 1),
+                            "mean_launch_us": 1e3 * upd_ms / max(upd_n, 1), "launches": upd_n,
+                            "finalize_mean_us": 1e3 * fin_ms / max(upd_n, 1)},
+        "time_split_ms_per_step": {"denoiser": den_ms / a.steps, "update": upd_ms / a.steps,
+                                   "finalize": fin_ms / a.steps,
+                                   "other": ms_per_step - (den_ms + upd_ms + fin_ms) / a.steps},
+    }
+    if not a.no_sequential:
+        pd.pd_sample_sequential(sched, den, 0, wl.batch, shape, x, workspace=ws)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        pd.pd_sample_sequential(sched, den, 0, wl.batch, shape, x, workspace=ws)
+        torch.cuda.synchronize()
+        seq_ms = 1e3 * (time.perf_counter() - t0)
+        out["sequential_ms"] = seq_ms
+        out["speedup_vs_sequential"] = seq_ms / ms_per_step
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, weights, a.cpu_budget)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

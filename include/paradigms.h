@@ -180,6 +180,14 @@ typedef struct pd_sample_stats {
     int64_t evals_per_sample;  /* sum of window sizes: the paper's "model evaluations" */
     int64_t network_rows;      /* evals_per_sample * batch * (2 with guidance)         */
     int32_t* stride_trace;     /* optional host array: stride of each iteration        */
+    int32_t time_kernels;      /* in: nonzero = bracket every denoiser, update and     */
+                               /*     finalize launch with HIP events on `stream`      */
+    int32_t denoiser_launches; /* out (with time_kernels): denoiser calls timed        */
+    int32_t update_launches;   /* out: Picard update (scan) or sequential step launches */
+    int32_t finalize_launches; /* out: stride/slide launches (Picard only)             */
+    double denoiser_ms;        /* out: summed event time of the denoiser calls         */
+    double update_ms;          /* out: summed event time of the update launches        */
+    double finalize_ms;        /* out: summed event time of the finalize launches      */
 } pd_sample_stats;
 
 typedef struct pd_workspace pd_workspace;

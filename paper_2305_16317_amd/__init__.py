@@ -62,7 +62,11 @@ class _ModelDesc(ctypes.Structure):
 class _Stats(ctypes.Structure):
     _fields_ = [("iters", ctypes.c_int32), ("trace_cap", ctypes.c_int32),
                 ("evals_per_sample", ctypes.c_int64), ("network_rows", ctypes.c_int64),
-                ("stride_trace", ctypes.POINTER(ctypes.c_int32))]
+                ("stride_trace", ctypes.POINTER(ctypes.c_int32)),
+                ("time_kernels", ctypes.c_int32), ("denoiser_launches", ctypes.c_int32),
+                ("update_launches", ctypes.c_int32), ("finalize_launches", ctypes.c_int32),
+                ("denoiser_ms", ctypes.c_double), ("update_ms", ctypes.c_double),
+                ("finalize_ms", ctypes.c_double)]
 
 
 _LIB: Optional[ctypes.CDLL] = None
@@ -193,6 +197,7 @@ class SampleStats:
     evals_per_sample: int
     network_rows: int
     trace: List[int]
+    kernel_times: Optional[Dict[str, float]] = dataclasses.field(default=None, compare=False)
 
 
 # ------------------------------------------------------------------ entry points
@@ -252,15 +257,21 @@ def pd_workspace_create(sched: Schedule, den: Denoiser, p: int, batch: int) -> W
     return Workspace(h)
 
 
-def _stats(trace_cap: int):
+def _stats(trace_cap: int, time_kernels: bool = False):
     buf = (ctypes.c_int32 * max(trace_cap, 1))()
-    st = _Stats(0, trace_cap, 0, 0, ctypes.cast(buf, ctypes.POINTER(ctypes.c_int32)))
+    st = _Stats(0, trace_cap, 0, 0, ctypes.cast(buf, ctypes.POINTER(ctypes.c_int32)),
+                int(time_kernels))
     return st, buf
 
 
 def _out_stats(st, buf) -> SampleStats:
     n = min(st.iters, st.trace_cap)
-    return SampleStats(st.iters, st.evals_per_sample, st.network_rows, list(buf[:n]))
+    kt = None
+    if st.time_kernels:
+        kt = {"denoiser_ms": st.denoiser_ms, "denoiser_launches": st.denoiser_launches,
+              "update_ms": st.update_ms, "update_launches": st.update_launches,
+              "finalize_ms": st.finalize_ms, "finalize_launches": st.finalize_launches}
+    return SampleStats(st.iters, st.evals_per_sample, st.network_rows, list(buf[:n]), kt)
 
 
 def _check_out(x_out: torch.Tensor, batch: int, den: Denoiser):
@@ -272,10 +283,10 @@ def _check_out(x_out: torch.Tensor, batch: int, den: Denoiser):
 def pd_sample_sequential(sched: Schedule, den: Denoiser, noise_seed: int, batch: int,
                          sample_shape: Sequence[int], x_out: torch.Tensor,
                          workspace: Optional[Workspace] = None, stream=None,
-                         trace_cap: int = 0) -> SampleStats:
+                         trace_cap: int = 0, time_kernels: bool = False) -> SampleStats:
     _check_out(x_out, batch, den)
     shp, nd = _shape(sample_shape)
-    st, buf = _stats(trace_cap)
+    st, buf = _stats(trace_cap, time_kernels)
     _check(load().pd_sample_sequential(sched.handle, den.handle, noise_seed, batch, shp, nd,
                                        _ptr(x_out), ctypes.byref(st),
                                        workspace.handle if workspace else None, _stream(stream)))
@@ -285,10 +296,10 @@ def pd_sample_sequential(sched: Schedule, den: Denoiser, noise_seed: int, batch:
 def pd_sample_picard(sched: Schedule, den: Denoiser, p: int, tau: float, noise_seed: int,
                      batch: int, sample_shape: Sequence[int], x_out: torch.Tensor,
                      workspace: Optional[Workspace] = None, stream=None,
-                     trace_cap: Optional[int] = None) -> SampleStats:
+                     trace_cap: Optional[int] = None, time_kernels: bool = False) -> SampleStats:
     _check_out(x_out, batch, den)
     shp, nd = _shape(sample_shape)
-    st, buf = _stats(sched.T if trace_cap is None else trace_cap)
+    st, buf = _stats(sched.T if trace_cap is None else trace_cap, time_kernels)
     _check(load().pd_sample_picard(sched.handle, den.handle, p, float(tau), noise_seed, batch,
                                    shp, nd, _ptr(x_out), ctypes.byref(st),
                                    workspace.handle if workspace else None, _stream(stream)))

@@ -104,6 +104,39 @@ std::vector<double> timestep_embedding(int n, int width) {
     return e;
 }
 
+// Optional per-launch timing: consecutive events recorded on the sampling
+// stream; elapsed times are summed per category after the final sync.
+struct KernelTimer {
+    bool on = false;
+    hipStream_t st = nullptr;
+    std::vector<hipEvent_t> ev;
+    std::vector<int> cat;            // category of the interval ending at ev[i]
+    double ms[3] = {0.0, 0.0, 0.0};
+    int count[3] = {0, 0, 0};
+    ~KernelTimer() {
+        for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+    }
+    void mark(int category) {        // category < 0: start of an interval
+        if (!on) return;
+        hipEvent_t e;
+        PD_HIP(hipEventCreate(&e));
+        ev.push_back(e);
+        cat.push_back(category);
+        PD_HIP(hipEventRecord(e, st));
+    }
+    void collect() {                 // call after the stream is synchronised
+        if (!on) return;
+        for (size_t i = 1; i < ev.size(); ++i) {
+            if (cat[i] < 0) continue;
+            float t = 0.f;
+            PD_HIP(hipEventElapsedTime(&t, ev[i - 1], ev[i]));
+            ms[cat[i]] += t;
+            count[cat[i]] += 1;
+        }
+    }
+};
+enum { CAT_DENOISER = 0, CAT_UPDATE = 1, CAT_FINALIZE = 2 };
+
 int64_t product(const int64_t* shape, int32_t ndim) {
     int64_t D = 1;
     for (int i = 0; i < ndim; ++i) D *= shape[i];
@@ -524,8 +557,14 @@ static void draw_noise(pd_workspace& w, uint64_t seed, hipStream_t st) {
 }
 
 static void fill_stats(pd_sample_stats* stats, int iters, int64_t evals, int batch, bool guided,
-                       const int32_t* dtrace) {
+                       const int32_t* dtrace, const KernelTimer& tm) {
     if (!stats) return;
+    stats->denoiser_launches = tm.count[CAT_DENOISER];
+    stats->update_launches = tm.count[CAT_UPDATE];
+    stats->finalize_launches = tm.count[CAT_FINALIZE];
+    stats->denoiser_ms = tm.ms[CAT_DENOISER];
+    stats->update_ms = tm.ms[CAT_UPDATE];
+    stats->finalize_ms = tm.ms[CAT_FINALIZE];
     stats->iters = iters;
     stats->evals_per_sample = evals;
     stats->network_rows = evals * batch * (guided ? 2 : 1);
@@ -548,17 +587,24 @@ extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoise
         pd_workspace& w = *use_workspace(ws, own, s, d, 1, batch);
         const int64_t BD = (int64_t)batch * d->D;
         float* x = w.ring.as<float>();
+        KernelTimer tm;
+        tm.on = stats && stats->time_kernels;
+        tm.st = st;
         draw_noise(w, noise_seed, st);
         for (int i = 0; i < s->T; ++i) {
             const RowSrc src{x, nullptr, BD, batch, 1, w.model_t.as<int32_t>() + i, nullptr};
+            tm.mark(-1);
             d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
+            tm.mark(CAT_DENOISER);
             const float* z = w.noise.p ? w.noise.as<float>() + (int64_t)i * BD : nullptr;
             launch_seq_step(x, w.eps.as<float>(), z, s->A[i], s->B[i], BD, st);
+            tm.mark(CAT_UPDATE);
         }
         PD_HIP(hipMemcpyAsync(x_out, x, sizeof(float) * BD, hipMemcpyDeviceToDevice, st));
         PD_HIP(hipStreamSynchronize(st));
+        tm.collect();
         if (stats) {
-            fill_stats(stats, s->T, s->T, batch, d->guided(), nullptr);
+            fill_stats(stats, s->T, s->T, batch, d->guided(), nullptr, tm);
             const int n = s->T < stats->trace_cap ? s->T : stats->trace_cap;
             for (int i = 0; i < n && stats->stride_trace; ++i) stats->stride_trace[i] = 1;
         }
@@ -584,6 +630,9 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         const float tau2 = tau * tau;
         LoopState* dst = w.state.as<LoopState>();
 
+        KernelTimer tm;
+        tm.on = stats && stats->time_kernels;
+        tm.st = st;
         draw_noise(w, noise_seed, st);
         launch_picard_init(dst, w.slot.as<int32_t>(), w.nrow.as<int32_t>(),
                            w.model_t.as<int32_t>(), T, pc, st);
@@ -595,14 +644,18 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
             // more are needed: enqueue them without looking at the device
             const int need = (T - t_host + pc - 1) / pc;
             for (int it = 0; it < need; ++it) {
+                tm.mark(-1);
                 d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
+                tm.mark(CAT_DENOISER);
                 launch_picard_scan(dst, w.ring.as<float>(), w.eps.as<float>(), w.noise.as<float>(),
                                    w.A.as<float>(), w.B.as<float>(), pc, batch, d->D,
                                    w.partials.as<float>(), st);
+                tm.mark(CAT_UPDATE);
                 launch_picard_finalize(dst, w.partials.as<float>(), pc, batch, d->D, T,
                                        w.tolv.as<float>(), tau2, s->desc.tol_index_offset,
                                        w.model_t.as<int32_t>(), w.trace.as<int32_t>(),
                                        w.slot.as<int32_t>(), w.nrow.as<int32_t>(), st);
+                tm.mark(CAT_FINALIZE);
             }
             issued += need;
             PD_HIP(hipMemcpyAsync(w.h_state, dst, sizeof(LoopState), hipMemcpyDeviceToHost, st));
@@ -617,6 +670,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         const float* xT = w.ring.as<float>() + (int64_t)(T % (pc + 1)) * BD;
         PD_HIP(hipMemcpyAsync(x_out, xT, sizeof(float) * BD, hipMemcpyDeviceToDevice, st));
         PD_HIP(hipStreamSynchronize(st));
-        fill_stats(stats, iters, evals, batch, d->guided(), w.trace.as<int32_t>());
+        tm.collect();
+        fill_stats(stats, iters, evals, batch, d->guided(), w.trace.as<int32_t>(), tm);
     });
 }
