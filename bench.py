@@ -122,6 +122,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sequential", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="after the run, copy this many bytes device-to-device 3 times "
+                         "(a plain copy of known size, to scale rocprofv3 byte counters)")
     a = ap.parse_args()
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only: --gpus {a.gpus} is not supported "
@@ -198,7 +201,8 @@ def main() -> int:
                      "flops_per_launch": fl / max(den_n, 1),
                      "mean_launch_ms": den_ms / max(den_n, 1), "launches": den_n},
         "roofline_update": {"bound": "hbm", "achieved": upd_rate / 1e9, "peak": HBM_PEAK / 1e9,
-                            "unit": "GB/s", "frac": upd_rate / HBM_PEAK, "traffic": None,
+                            "unit": "GB/s", "frac": upd_rate / HBM_PEAK,
+                            "traffic": traffic_from_profiles("k_picard_scan"),
                             "kernel": "k_picard_scan", "bytes_per_launch": ub / max(upd_n, 1),
                             "mean_launch_us": 1e3 * upd_ms / max(upd_n, 1), "launches": upd_n,
                             "finalize_mean_us": 1e3 * fin_ms / max(upd_n, 1)},
@@ -215,6 +219,14 @@ def main() -> int:
         seq_ms = 1e3 * (time.perf_counter() - t0)
         out["sequential_ms"] = seq_ms
         out["speedup_vs_sequential"] = seq_ms / ms_per_step
+    if a.copy_bytes > 0:
+        n = a.copy_bytes // 4
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty(n, device="cuda")
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = 4 * n
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, weights, a.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -47,14 +47,42 @@ __global__ void k_picard_init(LoopState* st, int32_t* slot, int32_t* nrow,
     }
 }
 
+// Sum each of the R values v[0..R) of a lane over the 64 lanes of the wave.
+// Butterfly with halving: at every step a lane keeps half of its values and
+// adds the partner's copy of that half, so R - 1 + log2(64/R) shuffles cover
+// all R sums (instead of 6 R).  Returns the full sum of value index `idx`
+// (a function of the lane); lanes with (lane & (64/R - 1)) == 0 hold distinct
+// indices.  Every sum is formed in a fixed order, so results are reproducible.
+template <int R>
+__device__ __forceinline__ float multi_wave_sum(float (&v)[R], int lane, int& idx) {
+    idx = 0;
+#pragma unroll
+    for (int h = R / 2, bit = 32; h >= 1; h /= 2, bit /= 2) {
+        const bool upper = (lane & bit) != 0;
+#pragma unroll
+        for (int i = 0; i < h; ++i) {
+            const float keep = upper ? v[i + h] : v[i];
+            const float send = upper ? v[i] : v[i + h];
+            v[i] = keep + __shfl_xor(send, bit, 64);
+        }
+        if (upper) idx += h;
+    }
+    float r = v[0];
+#pragma unroll
+    for (int bit = 32 / R; bit >= 1; bit /= 2) r += __shfl_xor(r, bit, 64);
+    return r;
+}
+
 // One block: 64 columns of one sample b, all window rows, split over 4 waves
-// (rows [w*ch, (w+1)*ch) per wave).  Drift and noise are summed along the
-// rows inside each wave, the wave totals are exchanged through LDS, and the
-// new points x^{k+1}_{t+j+1} = x_t + sum y + sum z are written back to the ring.
-// The squared differences against the old points are reduced over the 64
-// columns per window offset and written as per-block partial sums
-// partials[b][o][blk]; offset 0 (never tested) carries the count of
-// non-finite new points instead.
+// (rows [w*ch, (w+1)*ch) per wave, ch <= R).  Drift and noise are summed along
+// the rows inside each wave, the wave totals are exchanged through LDS, and
+// the new points x^{k+1}_{t+j+1} = x_t + sum y + sum z are written back to the
+// ring.  All loads use clamped, always-valid indices and no branches, so the
+// R rows' loads of a wave are in flight together.  The squared differences
+// against the old points are reduced over the 64 columns per window offset
+// and written as per-block partial sums partials[b][o][blk]; offset 0 (never
+// tested) carries the count of non-finite new points instead.
+template <int R, bool NOISE>
 __global__ __launch_bounds__(256) void k_picard_scan(
     const LoopState* __restrict__ st, float* ring, const float* __restrict__ eps,
     const float* __restrict__ noise, const float* __restrict__ Atab,
@@ -62,7 +90,9 @@ __global__ __launch_bounds__(256) void k_picard_scan(
     const int pe = st->p_eff;
     if (pe <= 0) return;
     const int t = st->t, f = st->f;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    // the wave index is uniform: keep it (and every row index derived from
+    // it) in scalar registers so the per-row table reads are scalar loads
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int b = blockIdx.y, blk = blockIdx.x, nblk = gridDim.x;
     const int64_t d = (int64_t)blk * kScanCols + lane;
     const bool valid = d < D;
@@ -80,20 +110,31 @@ __global__ __launch_bounds__(256) void k_picard_scan(
     // ---- every read of this block's ring columns is consumed before the
     // barrier; the writes all come after it (the ring slots overlap).
     const float anchor = ring[(int64_t)(t % P1) * slotsz + col];
-    const float xf = ring[(int64_t)(f % P1) * slotsz + col];
-    float xo[kScanMaxRows], sy[kScanMaxRows], sz[kScanMaxRows];
+    const int slot_f = f % P1;
+    float xo[R], e[R], z[R], ca[R], cb[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int j = min(j0 + r, pe - 1);            // clamped: always a window row
+        const int m = t + j;
+        const int sl = m <= f ? m % P1 : slot_f;      // points past f equal x_f
+        xo[r] = ring[(int64_t)sl * slotsz + col];
+        e[r] = eps[(int64_t)j * slotsz + col];
+        z[r] = NOISE ? noise[(int64_t)m * slotsz + col] : 0.f;
+        ca[r] = Atab[m];
+        cb[r] = Btab[m];
+    }
+    // drifts of every (clamped) row first, then the masked running sums: no
+    // load is left behind a condition
+    float y[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) y[r] = drift(ca[r], xo[r], cb[r], e[r]);
+    float sy[R], sz[R];
     float acc_y = 0.f, acc_z = 0.f;
 #pragma unroll
-    for (int r = 0; r < kScanMaxRows; ++r) {
-        xo[r] = 0.f;
-        if (r < nr) {
-            const int j = j0 + r, m = t + j;
-            xo[r] = m <= f ? ring[(int64_t)(m % P1) * slotsz + col] : xf;
-            const float e = eps[(int64_t)j * slotsz + col];
-            const float z = noise ? noise[(int64_t)m * slotsz + col] : 0.f;
-            acc_y = __fadd_rn(acc_y, drift(Atab[m], xo[r], Btab[m], e));
-            acc_z = __fadd_rn(acc_z, z);
-        }
+    for (int r = 0; r < R; ++r) {
+        const bool in = r < nr;
+        acc_y = __fadd_rn(acc_y, in ? y[r] : 0.f);
+        acc_z = __fadd_rn(acc_z, in ? z[r] : 0.f);
         sy[r] = acc_y;
         sz[r] = acc_z;
     }
@@ -109,26 +150,25 @@ __global__ __launch_bounds__(256) void k_picard_scan(
     const float next_old = (w + 1 < kScanWaves) ? s_first[w + 1][lane] : 0.f;
 
     // ---- new points, their errors, and the writes
-    float bad = 0.f;
+    float bad = 0.f, d2[R];
 #pragma unroll
-    for (int r = 0; r < kScanMaxRows; ++r) {
-        if (r < nr) {
-            const int j = j0 + r;
-            const float xn =
-                __fadd_rn(__fadd_rn(anchor, __fadd_rn(py, sy[r])), __fadd_rn(pz, sz[r]));
-            if (valid) {
-                ring[(int64_t)((t + j + 1) % P1) * slotsz + col] = xn;
-                bad += isfinite(xn) ? 0.f : 1.f;
-            }
-            const int o = j + 1;                      // window offset of point t+j+1
-            if (o < pe) {
-                const float xold = (r + 1 < nr) ? xo[r + 1] : next_old;
-                const float dl = valid ? __fsub_rn(xn, xold) : 0.f;
-                const float s = wave_sum(dl * dl);
-                if (lane == 0) partials[((int64_t)b * p + o) * nblk + blk] = s;
-            }
+    for (int r = 0; r < R; ++r) {
+        const int j = j0 + r;
+        const float xn = __fadd_rn(__fadd_rn(anchor, __fadd_rn(py, sy[r])), __fadd_rn(pz, sz[r]));
+        const bool in = r < nr;
+        if (in && valid) {
+            ring[(int64_t)((t + j + 1) % P1) * slotsz + col] = xn;
+            bad += isfinite(xn) ? 0.f : 1.f;
         }
+        // error of window offset o = j + 1: x^{k+1}_{t+j+1} against x^k_{t+j+1}
+        const float xold = (r + 1 < R && r + 1 < nr) ? xo[r + 1 < R ? r + 1 : r] : next_old;
+        const float dl = (in && valid && j + 1 < pe) ? __fsub_rn(xn, xold) : 0.f;
+        d2[r] = dl * dl;
     }
+    int idx;
+    const float s = multi_wave_sum<R>(d2, lane, idx);
+    if ((lane & (64 / R - 1)) == 0 && idx < nr && j0 + idx + 1 < pe)
+        partials[((int64_t)b * p + j0 + idx + 1) * nblk + blk] = s;
     bad = wave_sum(bad);
     if (lane == 0) s_bad[w] = bad;
     __syncthreads();
@@ -161,8 +201,16 @@ __global__ __launch_bounds__(1024) void k_picard_finalize(
     for (int pair = team; pair < pe * batch; pair += nteams) {
         const int o = pair / batch, b = pair % batch;
         const float* src = partials + ((int64_t)b * p + o) * nblk;
-        float s = 0.f;
-        for (int i = tl; i < nblk; i += kTeam) s += src[i];
+        // 8 independent loads per step keep the team's reads in flight together
+        float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        for (int i0 = 0; i0 < nblk; i0 += 8 * kTeam) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int i = i0 + u * kTeam + tl;
+                acc[u] += i < nblk ? src[i] : 0.f;
+            }
+        }
+        float s = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
 #pragma unroll
         for (int off = kTeam / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, kTeam);
         if (tl == 0) {
@@ -223,8 +271,20 @@ void launch_picard_scan(const LoopState* st, float* ring, const float* eps, cons
                         float* partials, hipStream_t s) {
     if (p > kMaxWindow) fail(PD_ERR_UNSUPPORTED, "window larger than 128 points");
     const dim3 grid((unsigned)picard_partial_blocks(D), (unsigned)batch);
-    hipLaunchKernelGGL(k_picard_scan, grid, dim3(kScanWaves * 64), 0, s, st, ring, eps, noise, A,
-                       B, p, batch, D, partials);
+    const int ch = (p + kScanWaves - 1) / kScanWaves;    // rows per wave at a full window
+#define PD_SCAN(R)                                                                           \
+    if (ch <= R) {                                                                           \
+        if (noise)                                                                           \
+            hipLaunchKernelGGL((k_picard_scan<R, true>), grid, dim3(kScanWaves * 64), 0, s, st, \
+                               ring, eps, noise, A, B, p, batch, D, partials);               \
+        else                                                                                 \
+            hipLaunchKernelGGL((k_picard_scan<R, false>), grid, dim3(kScanWaves * 64), 0, s,    \
+                               st, ring, eps, noise, A, B, p, batch, D, partials);           \
+        PD_HIP(hipGetLastError());                                                           \
+        return;                                                                              \
+    }
+    PD_SCAN(1) PD_SCAN(2) PD_SCAN(4) PD_SCAN(8) PD_SCAN(16) PD_SCAN(32)
+#undef PD_SCAN
     PD_HIP(hipGetLastError());
 }
 

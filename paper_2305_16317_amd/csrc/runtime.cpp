@@ -638,11 +638,18 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                            w.model_t.as<int32_t>(), T, pc, st);
         const RowSrc src{w.ring.as<float>(), w.slot.as<int32_t>(), BD,     batch,
                          pc,                 w.nrow.as<int32_t>(), &dst->p_eff};
-        int t_host = 0, issued = 0;
+        int t_host = 0, k_host = 0, issued = 0;
         for (;;) {
             // every iteration advances t by at most pc, so at least this many
-            // more are needed: enqueue them without looking at the device
-            const int need = (T - t_host + pc - 1) / pc;
+            // more are needed; once strides have been seen, enqueue as many as
+            // the mean stride so far predicts.  Iterations enqueued past the
+            // end find p_eff = 0 on the device and return at once.
+            int need = (T - t_host + pc - 1) / pc;
+            if (k_host > 0 && t_host > 0) {
+                const int est = (int)std::ceil((double)(T - t_host) * k_host / (double)t_host);
+                need = need > est ? need : est;
+            }
+            need = need < T - t_host ? need : T - t_host;   // stride >= 1 bounds the rest
             for (int it = 0; it < need; ++it) {
                 tm.mark(-1);
                 d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
@@ -662,8 +669,9 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
             PD_HIP(hipStreamSynchronize(st));
             if (w.h_state->status != PD_OK) fail(PD_ERR_NUMERIC, "non-finite point or error in the window");
             t_host = w.h_state->t;
+            k_host = w.h_state->k;
             if (t_host >= T) break;
-            if (issued > T) fail(PD_ERR_DEVICE, "Picard loop did not terminate within T iterations");
+            if (issued >= T) fail(PD_ERR_DEVICE, "Picard loop did not terminate within T iterations");
         }
         const int iters = w.h_state->k;
         const int64_t evals = w.h_state->evals;
