@@ -25,6 +25,8 @@
 // Inside a mid-layer slab for input block b, fragment (g, nb) of lane l holds
 // float4 {W[32 nb + l%32][32 b + 8 g + 4 (l/32) + q] : q = 0..3}, so one
 // ds_read_b128 feeds four MFMAs.
+#include <cstring>
+
 #include "pd_internal.h"
 
 namespace pd {
@@ -208,6 +210,222 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
     }
 }
 
+// ---------------------------------------------------------------- bf16
+// Same design on v_mfma_f32_32x32x16_bf16: A[i][k] holds k = 8 (l/32) + u
+// (u = 0..7) in lane i + 32 (l/32) as 8 packed bf16, B[k][j] likewise in lane
+// j + 32 (k/8), D as for the fp32 instruction.  Accumulator registers
+// 8 g2 .. 8 g2 + 7 of block b, rounded to bf16 and packed, are the B operand
+// of k-step (b, g2): lane half h then carries input features
+// 32 b + 16 g2 + 8 (u/4) + 4 h + u%4, and the packed weights use the same
+// order.  Layer 1 pads K = C to 16 with zeros, layer 4 pads its C output rows
+// to 32.  Every matmul operand is bf16 (round to nearest even); accumulation,
+// bias, shift, SiLU and the guidance combination stay in fp32.
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+
+template <int NB, int C>
+struct ConvLayoutBf16 {                          // units of 16 B (one lane's A operand)
+    static constexpr int SL1 = NB * 64;          // layer 1: one k-step per output block
+    static constexpr int SLM = 2 * NB * 64;      // layers 2, 3 per input block; layer 4 (all)
+    static constexpr int TOTAL = SL1 + (2 * NB + 1) * SLM;
+    static constexpr __host__ __device__ int off(int i) { return i == 0 ? 0 : SL1 + (i - 1) * SLM; }
+    static constexpr __host__ __device__ int size(int i) { return i == 0 ? SL1 : SLM; }
+};
+
+template <int NB, int C>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
+    using L = ConvLayoutBf16<NB, C>;
+    static_assert(C <= 8, "layer 1 holds at most 8 channels in one lane half");
+    __shared__ bf8 lds[2][L::SLM];
+
+    const int groups = src.active ? *src.active : src.max_groups;
+    const int64_t rows = (int64_t)groups * src.group;
+    const int64_t ntiles = rows * tiles_per_row;
+    if ((int64_t)blockIdx.x * 4 >= ntiles) return;          // uniform over the block
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int64_t tile = (int64_t)blockIdx.x * 4 + wave;
+    const bool active = tile < ntiles;
+    const int64_t tt = active ? tile : ntiles - 1;          // idle waves redo the last tile
+    const int64_t row = tt / tiles_per_row;
+    const int pt = (int)(tt % tiles_per_row);
+    const int g = (int)(row / src.group), bb = (int)(row % src.group);
+    const int64_t P = a.P;
+    const int64_t sl = src.slot ? src.slot[g] : g;
+    const float* x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
+    const int n = src.n[g];
+    const int64_t px = (int64_t)pt * 32 + (lane & 31);
+    const bool pxok = px < P;
+
+    auto dma = [&](int i, int buf) {
+        const int nch = L::size(i) / 64;                     // 1 KB chunks
+        const char* gb = reinterpret_cast<const char*>(a.frags);
+        uint32_t lo = (uint32_t)lane * 16u;
+        asm volatile("" : "+s"(gb), "+v"(lo));
+        bf8* ls = lds[buf];
+        for (int c = wave; c < nch; c += 4) {
+            const uint32_t ob = (uint32_t)(L::off(i) + c * 64) * 16u + lo;
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(gb + (size_t)ob),
+                (__attribute__((address_space(3))) void*)(ls + c * 64), 16, 0, 0);
+        }
+    };
+    auto land = [&]() {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    };
+    auto vec4 = [&](const float* v, int nb, int q4) -> f4 {
+        return *reinterpret_cast<const f4*>(v + 32 * nb + 8 * q4 + 4 * half);
+    };
+    // fp32 accumulator block -> shifted SiLU -> packed bf16 B operands
+    auto activate = [&](const f16v& acc, const float* v, int nb, bf8 (&hb)[2]) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+            const f4 sh = vec4(v, nb, q4);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                hb[q4 / 2][4 * (q4 % 2) + q] = (__bf16)silu(acc[4 * q4 + q] + sh[q]);
+        }
+    };
+
+    // layer-1 input: channels 0..C-1 in lane half 0, zero padding elsewhere
+    bf8 xb;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const float v = (half == 0 && u < C && pxok) ? x[u * P + px] : 0.f;
+        xb[u] = (__bf16)v;
+    }
+
+    const int nbranch = a.shift_c ? 2 : 1;
+    float eu[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int br = 0; br < nbranch; ++br) {
+        const float* shift = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * a.width;
+        f16v acc[NB];
+        bf8 H[NB][2];
+
+        dma(0, 0);
+        land();
+        dma(1, 1);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+            acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[0][nb * 64 + lane], xb, f16v{},
+                                                              0, 0, 0);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) activate(acc[nb], shift, nb, H[nb]);
+        land();
+
+#pragma unroll
+        for (int layer = 0; layer < 2; ++layer) {
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) acc[nb] = f16v{};
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const int slab = 1 + layer * NB + b;
+                const int buf = slab & 1;
+                dma(slab + 1, buf ^ 1);
+#pragma unroll
+                for (int g2 = 0; g2 < 2; ++g2)
+#pragma unroll
+                    for (int nb = 0; nb < NB; nb += 2) {
+                        const bf8 w0 = lds[buf][(g2 * NB + nb) * 64 + lane];
+                        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, H[b][g2], acc[nb],
+                                                                          0, 0, 0);
+                        if (nb + 1 < NB) {
+                            const bf8 w1 = lds[buf][(g2 * NB + nb + 1) * 64 + lane];
+                            acc[nb + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                w1, H[b][g2], acc[nb + 1], 0, 0, 0);
+                        }
+                    }
+                land();
+            }
+            const float* bias = layer == 0 ? a.b2 : a.b3;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) activate(acc[nb], bias, nb, H[nb]);
+        }
+
+        {
+            constexpr int slab = 1 + 2 * NB;
+            constexpr int buf = slab & 1;
+            f16v o2[2] = {f16v{}, f16v{}};
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int g2 = 0; g2 < 2; ++g2)
+                    o2[g2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        lds[buf][(b * 2 + g2) * 64 + lane], H[b][g2], o2[g2], 0, 0, 0);
+            __syncthreads();   // the next branch overwrites both buffers
+            const f16v o = o2[0] + o2[1];
+            float* out = eps + row * (int64_t)C * P;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int c = 4 * half + r;
+                if (c < C) {
+                    const float v = o[r] + a.b4[c];
+                    if (br == 0) {
+                        eu[r] = v;
+                        if (nbranch == 1 && active && pxok) out[c * P + px] = v;
+                    } else if (active && pxok) {
+                        out[c * P + px] = eu[r] + a.guidance * (v - eu[r]);
+                    }
+                }
+            }
+        }
+    }
+}
+
+uint16_t to_bf16(float f) {                     // round to nearest even
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40);
+    const uint32_t lsb = (u >> 16) & 1u;
+    return (uint16_t)((u + 0x7FFFu + lsb) >> 16);
+}
+
+template <int NB, int C>
+void pack_bf16_t(const float* W1, const float* W2, const float* W3, const float* W4,
+                 std::vector<uint8_t>& out) {
+    using L = ConvLayoutBf16<NB, C>;
+    constexpr int W = 32 * NB;
+    out.assign((size_t)L::TOTAL * 16, 0);
+    uint16_t* f = reinterpret_cast<uint16_t*>(out.data());     // 8 bf16 per unit
+    auto unit = [&](int u) { return f + (size_t)u * 8; };
+    for (int nb = 0; nb < NB; ++nb)
+        for (int l = 0; l < 64; ++l)
+            for (int u = 0; u < 8; ++u) {
+                const int k = 8 * (l / 32) + u;
+                unit(L::off(0) + nb * 64 + l)[u] =
+                    k < C ? to_bf16(W1[(32 * nb + l % 32) * C + k]) : (uint16_t)0;
+            }
+    auto fin = [](int b, int g2, int l, int u) { return 32 * b + 16 * g2 + 8 * (u / 4) + 4 * (l / 32) + u % 4; };
+    for (int layer = 0; layer < 2; ++layer) {
+        const float* Wm = layer == 0 ? W2 : W3;
+        for (int b = 0; b < NB; ++b)
+            for (int g2 = 0; g2 < 2; ++g2)
+                for (int nb = 0; nb < NB; ++nb)
+                    for (int l = 0; l < 64; ++l)
+                        for (int u = 0; u < 8; ++u)
+                            unit(L::off(1 + layer * NB + b) + (g2 * NB + nb) * 64 + l)[u] =
+                                to_bf16(Wm[(32 * nb + l % 32) * W + fin(b, g2, l, u)]);
+    }
+    for (int b = 0; b < NB; ++b)
+        for (int g2 = 0; g2 < 2; ++g2)
+            for (int l = 0; l < 64; ++l)
+                for (int u = 0; u < 8; ++u)
+                    unit(L::off(1 + 2 * NB) + (b * 2 + g2) * 64 + l)[u] =
+                        (l % 32 < C) ? to_bf16(W4[(l % 32) * W + fin(b, g2, l, u)]) : (uint16_t)0;
+}
+
+template <int NB, int C>
+void launch_bf16_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
+    const int tiles_per_row = (int)((a.P + 31) / 32);
+    const int64_t ntiles = (int64_t)src.max_groups * src.group * tiles_per_row;
+    if (ntiles == 0) return;
+    const int64_t blocks = (ntiles + 3) / 4;
+    hipLaunchKernelGGL((k_conv_bf16<NB, C>), dim3((unsigned)blocks), dim3(256), 0, s, a, src, eps,
+                       tiles_per_row);
+    PD_HIP(hipGetLastError());
+}
+
 template <int NB, int C>
 void launch_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
     const int tiles_per_row = (int)((a.P + 31) / 32);
@@ -256,15 +474,17 @@ void pack_t(const float* W1, const float* W2, const float* W3, const float* W4,
 }  // namespace
 
 bool conv_supported(int C, int width, bool bf16) {
-    if (bf16) return false;
 #define X(nb, c) if (C == c && width == 32 * nb) return true;
     PD_CONV_SHAPES(X)
 #undef X
+    (void)bf16;
     return false;
 }
 
 size_t conv_frag_bytes(int C, int width, bool bf16) {
-#define X(nb, c) if (!bf16 && C == c && width == 32 * nb) return (size_t)ConvLayout<nb, c>::TOTAL * 4;
+#define X(nb, c)                                                                      \
+    if (C == c && width == 32 * nb)                                                   \
+        return bf16 ? (size_t)ConvLayoutBf16<nb, c>::TOTAL * 16 : (size_t)ConvLayout<nb, c>::TOTAL * 4;
     PD_CONV_SHAPES(X)
 #undef X
     return 0;
@@ -272,25 +492,31 @@ size_t conv_frag_bytes(int C, int width, bool bf16) {
 
 void conv_pack_weights(int C, int width, bool bf16, const float* W1, const float* W2,
                        const float* W3, const float* W4, std::vector<uint8_t>& out) {
-#define X(nb, c)                                          \
-    if (!bf16 && C == c && width == 32 * nb) {            \
-        pack_t<nb, c>(W1, W2, W3, W4, out);               \
-        return;                                           \
+#define X(nb, c)                                                  \
+    if (C == c && width == 32 * nb) {                             \
+        if (bf16)                                                 \
+            pack_bf16_t<nb, c>(W1, W2, W3, W4, out);              \
+        else                                                      \
+            pack_t<nb, c>(W1, W2, W3, W4, out);                   \
+        return;                                                   \
     }
     PD_CONV_SHAPES(X)
 #undef X
-    fail(PD_ERR_UNSUPPORTED, "conv1x1: unsupported channel count / width / dtype");
+    fail(PD_ERR_UNSUPPORTED, "conv1x1: unsupported channel count / width");
 }
 
 void launch_conv1x1(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
 #define X(nb, c)                                                   \
-    if (!a.bf16 && a.C == c && a.width == 32 * nb) {               \
-        launch_t<nb, c>(a, src, eps, s);                           \
+    if (a.C == c && a.width == 32 * nb) {                          \
+        if (a.bf16)                                                \
+            launch_bf16_t<nb, c>(a, src, eps, s);                  \
+        else                                                       \
+            launch_t<nb, c>(a, src, eps, s);                       \
         return;                                                    \
     }
     PD_CONV_SHAPES(X)
 #undef X
-    fail(PD_ERR_UNSUPPORTED, "conv1x1: unsupported channel count / width / dtype");
+    fail(PD_ERR_UNSUPPORTED, "conv1x1: unsupported channel count / width");
 }
 
 }  // namespace pd

@@ -122,6 +122,29 @@ def test_conv1x1_forward(shape, width, M, cond):
     assert _rel(got, ref) <= REL_F32
 
 
+@pytest.mark.parametrize("shape,width,M,cond", [
+    ((4, 8, 8), 32, 3, 0),
+    ((4, 6, 7), 64, 5, 0),        # ragged last tile
+    ((4, 16, 16), 320, 3, 0),     # production width
+    ((4, 96, 96), 320, 2, 768),   # production shape with guidance, 768-d condition
+    ((4, 6, 6), 128, 3, 24),
+])
+def test_conv1x1_bf16_forward(shape, width, M, cond):
+    """bf16 operands, fp32 accumulation: against the oracle's bf16-operand mode
+    the only differences are summation order and the rare activation that
+    rounds to the neighbouring bf16 value; against float32 it is ~1e-3."""
+    wl = _wl("conv1x1", shape, width, T=1000, cond=cond, dtype="bf16")
+    w = W.make_weights(wl.model)
+    rng = np.random.default_rng(M + width + cond)
+    x = rng.standard_normal((M,) + shape).astype(np.float32)
+    n = rng.integers(0, 1000, M).astype(np.int32)
+    got = _forward(wl, w, x, n)
+    ref = _oracle_eps(wl, w, x, n)                     # bf16-operand oracle
+    ref32 = _oracle_eps(wl, w, x, n, bf16=False)
+    assert _rel(got, ref) <= 1e-3, _rel(got, ref)
+    assert _rel(got, ref32) <= 2e-2, _rel(got, ref32)
+
+
 def test_forward_empty_batch_is_noop():
     wl = _wl("conv1x1", (4, 8, 8), 32, T=10)
     sched, den = pd.from_workload(wl, W.make_weights(wl.model))
@@ -162,6 +185,27 @@ SMALL = {
                                        W.ModelSpec("conv1x1", (4, 8, 8), width=64, cond_dim=24,
                                                    guidance=7.5), p=16, tau=0.1),
 }
+
+BF16 = {
+    "cfg_bf16_small": lambda: W.small_variant("latent_cfg_bf16_ddpm1000_p128", T=60, p=32,
+                                              shape=(4, 8, 8), width=64),
+    "cfg_bf16_w320": lambda: W.small_variant("latent_cfg_bf16_ddpm1000_p128", T=150, p=128,
+                                             shape=(4, 8, 16), width=320),
+}
+
+
+@pytest.mark.parametrize("name", list(BF16))
+def test_picard_bf16_matches_oracle(name):
+    """bf16 denoiser: the sample is within relative L2 2e-2 of the oracle run
+    with the same bf16 operand rounding; the iteration count may differ where
+    a stride decision sits within rounding noise of the tolerance."""
+    wl = BF16[name]()
+    w = W.make_weights(wl.model)
+    got, st = _run(wl, w)
+    ref = Problem(wl, w, np.float32).picard()
+    assert st.network_rows == st.evals_per_sample * 2
+    assert _rel(got, ref.x) <= 2e-2, _rel(got, ref.x)
+    assert abs(st.iters - ref.iters) <= max(1, ref.iters // 10), (st.iters, ref.iters)
 
 
 @pytest.mark.parametrize("name", list(SMALL))
