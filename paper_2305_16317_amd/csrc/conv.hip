@@ -26,6 +26,7 @@
 // float4 {W[32 nb + l%32][32 b + 8 g + 4 (l/32) + q] : q = 0..3}, so one
 // ds_read_b128 feeds four MFMAs.
 #include <cstring>
+#include <utility>
 
 #include "pd_internal.h"
 
@@ -34,6 +35,18 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef float f16v __attribute__((ext_vector_type(16)));
+
+// Compile-time loop: f(std::integral_constant<int, i>) for i in [0, N).  Every
+// index into a register array must be a constant, or the array goes to
+// scratch memory; #pragma unroll alone is not guaranteed on bodies this big.
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 template <int NB, int C>
 struct ConvLayout {
@@ -50,37 +63,46 @@ __device__ __forceinline__ float silu(float v) {
     return v * __builtin_amdgcn_rcpf(1.0f + __expf(-v));
 }
 
+// Blocks are persistent: each loops over groups of 4 tiles (one per wave),
+// and the next pass's first weight slab is copied during the current pass's
+// last layer, so a tile starts without waiting for weights.
+//
+// Activations at a layer transition: only block 0 of the new activations is
+// computed up front; the next layer's first slab consumes block 0 alone, so
+// the SiLU of blocks 1..NB-1 is spread over that slab's MFMAs (the old
+// accumulators of those blocks stay live instead of their activations, which
+// costs no extra registers) and runs on the VALU while the matrix core works.
+template <int S, int NB>
+struct Spread {   // block k in [lo(s), hi(s)) is activated after MFMA slot s of S
+    static constexpr __device__ int lo(int s) { return 1 + (s * (NB - 1)) / S; }
+    static constexpr __device__ int hi(int s) { return 1 + ((s + 1) * (NB - 1)) / S; }
+};
+
 template <int NB, int C>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
     using L = ConvLayout<NB, C>;
+    constexpr int NBP = (NB + 1) / 2;                        // output-block pairs
+    constexpr int SLOTS = 4 * NBP;                           // MFMA slots of a mid slab
+    using SP = Spread<SLOTS, NB>;
     __shared__ f4 lds[2][L::SLM / 4];
 
     const int groups = src.active ? *src.active : src.max_groups;
-    const int64_t rows = (int64_t)groups * src.group;
-    const int64_t ntiles = rows * tiles_per_row;
-    if ((int64_t)blockIdx.x * 4 >= ntiles) return;          // uniform over the block
+    const int64_t ntiles = (int64_t)groups * src.group * tiles_per_row;
+    const int64_t ngroups = (ntiles + 3) / 4;
+    if ((int64_t)blockIdx.x >= ngroups) return;              // uniform over the block
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
-    const int64_t tile = (int64_t)blockIdx.x * 4 + wave;
-    const bool active = tile < ntiles;
-    const int64_t tt = active ? tile : ntiles - 1;          // idle waves redo the last tile
-    const int64_t row = tt / tiles_per_row;
-    const int pt = (int)(tt % tiles_per_row);
-    const int g = (int)(row / src.group), bb = (int)(row % src.group);
+    // the wave index is uniform: tile bookkeeping stays in scalar registers
+    const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t P = a.P;
-    const int64_t sl = src.slot ? src.slot[g] : g;
-    const float* x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
-    const int n = src.n[g];
-    const int64_t px = (int64_t)pt * 32 + (lane & 31);
-    const bool pxok = px < P;
 
     // slab i -> LDS buffer `buf`: 1 KB per wave instruction, 16 B per lane
     auto dma = [&](int i, int buf) {
         const int nch = L::size(i) / 256;
         // base and lane offset are made opaque at every call so the addresses
         // are formed here as SGPR base + 32-bit lane offset (the saddr form)
-        // instead of being hoisted out of the branch loop into 64-bit VGPRs
+        // instead of being hoisted out of the loops into 64-bit VGPRs
         const char* gb = reinterpret_cast<const char*>(a.frags);
         uint32_t lo = (uint32_t)lane * 16u;
         asm volatile("" : "+s"(gb), "+v"(lo));
@@ -96,117 +118,164 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     };
-    // bias (or shift) for the 4 features of register group q4 of block nb
-    auto vec4 = [&](const float* v, int nb, int q4) -> f4 {
-        return *reinterpret_cast<const f4*>(v + 32 * nb + 8 * q4 + 4 * half);
+    // SiLU(acc + v) for block nb: the 4 features of register group q4 are contiguous
+    auto act = [&](const f16v& c, const float* v0, int nb) -> f16v {
+        // opaque per call: keeps these loads next to their use instead of
+        // hoisted out of the tile loop (they do not change between tiles)
+        const float* v = v0;
+        asm volatile("" : "+s"(v));
+        f16v h;
+        static_for<4>([&](auto q4c) {
+            constexpr int q4 = decltype(q4c)::value;
+            const f4 sh = *reinterpret_cast<const f4*>(v + 32 * nb + 8 * q4 + 4 * half);
+            static_for<4>([&](auto qc) {
+                constexpr int q = decltype(qc)::value;
+                h[4 * q4 + q] = silu(c[4 * q4 + q] + sh[q]);
+            });
+        });
+        return h;
     };
+    struct Tile {
+        int64_t row, px;
+        bool active, pxok;
+        const float* x;
+        int n;
+    };
+    auto locate = [&](int64_t tg) -> Tile {
+        Tile T;
+        const int64_t tile = tg * 4 + wave;
+        T.active = tile < ntiles;
+        const int64_t tt = T.active ? tile : ntiles - 1;     // idle waves redo the last tile
+        T.row = tt / tiles_per_row;
+        const int pt = (int)(tt % tiles_per_row);
+        const int g = (int)(T.row / src.group), bb = (int)(T.row % src.group);
+        // per-wave values loaded from memory: uniform by construction
+        const int64_t sl = src.slot ? __builtin_amdgcn_readfirstlane(src.slot[g]) : g;
+        T.x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
+        T.n = __builtin_amdgcn_readfirstlane(src.n[g]);
+        T.px = (int64_t)pt * 32 + (lane & 31);
+        T.pxok = T.px < P;
+        return T;
+    };
+    const int nbranch = a.shift_c ? 2 : 1;
 
-    // layer-1 input: B[k][pixel] for k = 2 s + half
+    dma(0, 0);
+    land();
+    Tile cur = locate(blockIdx.x);
     float xin[L::KS1];
 #pragma unroll
-    for (int s = 0; s < L::KS1; ++s) xin[s] = pxok ? x[(2 * s + half) * P + px] : 0.f;
+    for (int s = 0; s < L::KS1; ++s) xin[s] = cur.pxok ? cur.x[(2 * s + half) * P + cur.px] : 0.f;
 
-    const int nbranch = a.shift_c ? 2 : 1;
-    float eu[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int br = 0; br < nbranch; ++br) {
-        const float* shift = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * a.width;
-        f16v acc[NB], H[NB];
+    for (int64_t tg = blockIdx.x; tg < ngroups; tg += gridDim.x) {
+        const bool last_group = tg + gridDim.x >= ngroups;
+        // the next group's input, fetched while this one computes
+        Tile nxt = locate(last_group ? tg : tg + gridDim.x);
+        float xnx[L::KS1];
+#pragma unroll
+        for (int s = 0; s < L::KS1; ++s) xnx[s] = nxt.pxok ? nxt.x[(2 * s + half) * P + nxt.px] : 0.f;
 
-        // ---- layer 1: K = C (VALU-cheap, but kept on MFMA for the layout)
-        dma(0, 0);
-        land();
-        dma(1, 1);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            acc[nb] = f16v{};
-            const float* f1 = reinterpret_cast<const float*>(lds[0]) + (nb * 64 + lane) * L::KS1;
-#pragma unroll
-            for (int s = 0; s < L::KS1; ++s)
-                acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(f1[s], xin[s], acc[nb], 0, 0, 0);
-        }
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const f4 sh = vec4(shift, nb, q4);
-#pragma unroll
-                for (int q = 0; q < 4; ++q) H[nb][4 * q4 + q] = silu(acc[nb][4 * q4 + q] + sh[q]);
-            }
-        land();
+        float eu[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int br = 0; br < nbranch; ++br) {
+            const float* shift = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)cur.n * a.width;
+            f16v acc[NB], H[NB];
 
-        // ---- layers 2 and 3: one slab per input block
+            // ---- layer 1 (slab 0, buffer 0): K = C
+            dma(1, 1);
+            static_for<NB>([&](auto nbc) {
+                constexpr int nb = decltype(nbc)::value;
+                acc[nb] = f16v{};
+                const float* f1 = reinterpret_cast<const float*>(lds[0]) + (nb * 64 + lane) * L::KS1;
+                static_for<L::KS1>([&](auto sc) {
+                    constexpr int s = decltype(sc)::value;
+                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(f1[s], xin[s], acc[nb], 0, 0, 0);
+                });
+            });
+
+            // ---- layers 2 and 3: one slab per input block
+            static_for<2>([&](auto lc) {
+                constexpr int layer = decltype(lc)::value;
+                const float* vin = layer == 0 ? shift : a.b2;   // shift of the activation
+                H[0] = act(acc[0], vin, 0);
+                f16v nacc[NB];
+                static_for<NB>([&](auto nbc) { nacc[decltype(nbc)::value] = f16v{}; });
+                static_for<NB>([&](auto bc) {
+                    constexpr int b = decltype(bc)::value;
+                    constexpr int slab = 1 + layer * NB + b;
+                    constexpr int buf = slab & 1;
+                    if (b == 0) land();                          // slab 1 / NB+1 has landed
+                    dma(slab + 1, buf ^ 1);
+                    static_for<4>([&](auto gc) {
+                        constexpr int g4 = decltype(gc)::value;
+                        static_for<NBP>([&](auto pc) {
+                            constexpr int nb = 2 * decltype(pc)::value;
+                            const f4 w0 = lds[buf][(g4 * NB + nb) * 64 + lane];
+                            const f4 w1 = nb + 1 < NB ? lds[buf][(g4 * NB + nb + 1) * 64 + lane] : f4{};
+                            static_for<4>([&](auto qc) {
+                                constexpr int q = decltype(qc)::value;
+                                nacc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                                    w0[q], H[b][4 * g4 + q], nacc[nb], 0, 0, 0);
+                                if constexpr (nb + 1 < NB)
+                                    nacc[nb + 1] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                                        w1[q], H[b][4 * g4 + q], nacc[nb + 1], 0, 0, 0);
+                            });
+                            if constexpr (b == 0) {              // deferred activations
+                                constexpr int slot = g4 * NBP + nb / 2;
+                                static_for<NB>([&](auto kc) {
+                                    constexpr int k = decltype(kc)::value;
+                                    if constexpr (k >= SP::lo(slot) && k < SP::hi(slot))
+                                        H[k] = act(acc[k], vin, k);
+                                });
+                            }
+                        });
+                    });
+                    if (b + 1 < NB) land();
+                });
+                static_for<NB>([&](auto nbc) { acc[decltype(nbc)::value] = nacc[decltype(nbc)::value]; });
+            });
+
+            // ---- layer 4 (slab 2NB+1, buffer 1): C outputs, 4 chains of MFMAs
+            {
+                constexpr int slab = 1 + 2 * NB;
+                constexpr int buf = slab & 1;
+                land();
+                const bool more = br + 1 < nbranch || !last_group;
+                if (more) dma(0, 0);                             // next pass's layer 1
+                H[0] = act(acc[0], a.b3, 0);
+                f16v o4[4] = {f16v{}, f16v{}, f16v{}, f16v{}};
+                static_for<NB>([&](auto bc) {
+                    constexpr int b = decltype(bc)::value;
+                    static_for<4>([&](auto gc) {
+                        constexpr int g4 = decltype(gc)::value;
+                        const f4 w = lds[buf][(b * 4 + g4) * 64 + lane];
+                        static_for<4>([&](auto qc) {
+                            constexpr int q = decltype(qc)::value;
+                            o4[g4] = __builtin_amdgcn_mfma_f32_32x32x2f32(w[q], H[b][4 * g4 + q],
+                                                                          o4[g4], 0, 0, 0);
+                        });
+                    });
+                    if constexpr (b + 1 < NB) H[b + 1] = act(acc[b + 1], a.b3, b + 1);
+                });
+                const f16v o = (o4[0] + o4[1]) + (o4[2] + o4[3]);
+                float* out = eps + cur.row * (int64_t)C * P;
 #pragma unroll
-        for (int layer = 0; layer < 2; ++layer) {
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) acc[nb] = f16v{};
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                const int slab = 1 + layer * NB + b;
-                const int buf = slab & 1;
-                dma(slab + 1, buf ^ 1);
-#pragma unroll
-                for (int g4 = 0; g4 < 4; ++g4)
-#pragma unroll
-                    for (int nb = 0; nb < NB; nb += 2) {
-                        // two output blocks at a time: two independent MFMA chains
-                        const f4 w0 = lds[buf][(g4 * NB + nb) * 64 + lane];
-                        const f4 w1 = nb + 1 < NB ? lds[buf][(g4 * NB + nb + 1) * 64 + lane] : f4{};
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                                w0[q], H[b][4 * g4 + q], acc[nb], 0, 0, 0);
-                            if (nb + 1 < NB)
-                                acc[nb + 1] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                                    w1[q], H[b][4 * g4 + q], acc[nb + 1], 0, 0, 0);
+                for (int r = 0; r < 4; ++r) {
+                    const int c = 4 * half + r;
+                    if (c < C) {
+                        const float v = o[r] + a.b4[c];
+                        if (br == 0) {
+                            eu[r] = v;
+                            if (nbranch == 1 && cur.active && cur.pxok) out[c * P + cur.px] = v;
+                        } else if (cur.active && cur.pxok) {
+                            out[c * P + cur.px] = eu[r] + a.guidance * (v - eu[r]);
                         }
                     }
-                land();
-            }
-            const float* bias = layer == 0 ? a.b2 : a.b3;
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) {
-                    const f4 bv = vec4(bias, nb, q4);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q)
-                        H[nb][4 * q4 + q] = silu(acc[nb][4 * q4 + q] + bv[q]);
                 }
-        }
-
-        // ---- layer 4: C outputs (rows of a 32-row block), 4 chains of MFMAs
-        {
-            constexpr int slab = 1 + 2 * NB;
-            constexpr int buf = slab & 1;
-            f16v o4[4] = {f16v{}, f16v{}, f16v{}, f16v{}};
-#pragma unroll
-            for (int b = 0; b < NB; ++b)
-#pragma unroll
-                for (int g4 = 0; g4 < 4; ++g4) {
-                    const f4 w = lds[buf][(b * 4 + g4) * 64 + lane];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q)
-                        o4[g4] = __builtin_amdgcn_mfma_f32_32x32x2f32(w[q], H[b][4 * g4 + q],
-                                                                      o4[g4], 0, 0, 0);
-                }
-            __syncthreads();   // the next branch overwrites both buffers
-            const f16v o = (o4[0] + o4[1]) + (o4[2] + o4[3]);
-            // output channel c = 4 half + r (r < 4) of pixel lane%32
-            float* out = eps + row * (int64_t)C * P;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int c = 4 * half + r;
-                if (c < C) {
-                    const float v = o[r] + a.b4[c];
-                    if (br == 0) {
-                        eu[r] = v;
-                        if (nbranch == 1 && active && pxok) out[c * P + px] = v;
-                    } else if (active && pxok) {
-                        out[c * P + px] = eu[r] + a.guidance * (v - eu[r]);
-                    }
-                }
+                land();                                          // slab 0 is in buffer 0 again
             }
         }
+        cur = nxt;
+#pragma unroll
+        for (int s = 0; s < L::KS1; ++s) xin[s] = xnx[s];
     }
 }
 
@@ -426,12 +495,24 @@ void launch_bf16_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t
     PD_HIP(hipGetLastError());
 }
 
+int device_cus() {
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0;
+        PD_HIP(hipGetDevice(&dev));
+        PD_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+        if (cus <= 0) cus = 256;
+    }
+    return cus;
+}
+
 template <int NB, int C>
 void launch_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
     const int tiles_per_row = (int)((a.P + 31) / 32);
     const int64_t ntiles = (int64_t)src.max_groups * src.group * tiles_per_row;
     if (ntiles == 0) return;
-    const int64_t blocks = (ntiles + 3) / 4;
+    int64_t blocks = (ntiles + 3) / 4;                       // persistent: one block per CU
+    if (blocks > device_cus()) blocks = device_cus();
     hipLaunchKernelGGL((k_conv_f32<NB, C>), dim3((unsigned)blocks), dim3(256), 0, s, a, src, eps,
                        tiles_per_row);
     PD_HIP(hipGetLastError());
