@@ -305,29 +305,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
     using L = ConvLayoutBf16<NB, C>;
     static_assert(C <= 8, "layer 1 holds at most 8 channels in one lane half");
-    __shared__ bf8 lds[2][L::SLM];
+    constexpr int NBP = (NB + 1) / 2;                        // output-block pairs
+    constexpr int SLOTS = 2 * NBP;                           // MFMA-pair slots per input block
+    // a bf16 input block is only 2 NB MFMAs, so SB blocks share one slab (and
+    // one barrier); the packed layout keeps consecutive blocks contiguous
+    constexpr int SB = (NB % 2 == 0) ? 2 : 1;
+    constexpr int NSB = NB / SB;                             // slabs per mid layer
+    __shared__ bf8 lds[2][SB * L::SLM];
 
     const int groups = src.active ? *src.active : src.max_groups;
-    const int64_t rows = (int64_t)groups * src.group;
-    const int64_t ntiles = rows * tiles_per_row;
-    if ((int64_t)blockIdx.x * 4 >= ntiles) return;          // uniform over the block
+    const int64_t ntiles = (int64_t)groups * src.group * tiles_per_row;
+    const int64_t ngroups = (ntiles + 3) / 4;
+    if ((int64_t)blockIdx.x >= ngroups) return;              // uniform over the block
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
-    const int64_t tile = (int64_t)blockIdx.x * 4 + wave;
-    const bool active = tile < ntiles;
-    const int64_t tt = active ? tile : ntiles - 1;          // idle waves redo the last tile
-    const int64_t row = tt / tiles_per_row;
-    const int pt = (int)(tt % tiles_per_row);
-    const int g = (int)(row / src.group), bb = (int)(row % src.group);
+    const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t P = a.P;
-    const int64_t sl = src.slot ? src.slot[g] : g;
-    const float* x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
-    const int n = src.n[g];
-    const int64_t px = (int64_t)pt * 32 + (lane & 31);
-    const bool pxok = px < P;
 
-    auto dma = [&](int i, int buf) {
-        const int nch = L::size(i) / 64;                     // 1 KB chunks
+    // packed slabs [i, i + n) -> LDS buffer `buf` (they are contiguous)
+    auto dma = [&](int i, int n, int buf) {
+        const int nch = (L::off(i + n - 1) + L::size(i + n - 1) - L::off(i)) / 64;   // 1 KB chunks
         const char* gb = reinterpret_cast<const char*>(a.frags);
         uint32_t lo = (uint32_t)lane * 16u;
         asm volatile("" : "+s"(gb), "+v"(lo));
@@ -343,102 +340,159 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     };
-    auto vec4 = [&](const float* v, int nb, int q4) -> f4 {
-        return *reinterpret_cast<const f4*>(v + 32 * nb + 8 * q4 + 4 * half);
+    // SiLU(acc + v) of block nb, rounded to bf16 and packed as two B operands
+    auto act = [&](const f16v& c, const float* v0, int nb, bf8 (&hb)[2]) {
+        const float* v = v0;
+        asm volatile("" : "+s"(v));
+        static_for<4>([&](auto q4c) {
+            constexpr int q4 = decltype(q4c)::value;
+            const f4 sh = *reinterpret_cast<const f4*>(v + 32 * nb + 8 * q4 + 4 * half);
+            static_for<4>([&](auto qc) {
+                constexpr int q = decltype(qc)::value;
+                hb[q4 / 2][4 * (q4 % 2) + q] = (__bf16)silu(c[4 * q4 + q] + sh[q]);
+            });
+        });
     };
-    // fp32 accumulator block -> shifted SiLU -> packed bf16 B operands
-    auto activate = [&](const f16v& acc, const float* v, int nb, bf8 (&hb)[2]) {
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-            const f4 sh = vec4(v, nb, q4);
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-                hb[q4 / 2][4 * (q4 % 2) + q] = (__bf16)silu(acc[4 * q4 + q] + sh[q]);
-        }
+    struct Tile {
+        int64_t row, px;
+        bool active, pxok;
+        const float* x;
+        int n;
     };
-
+    auto locate = [&](int64_t tg) -> Tile {
+        Tile T;
+        const int64_t tile = tg * 4 + wave;
+        T.active = tile < ntiles;
+        const int64_t tt = T.active ? tile : ntiles - 1;
+        T.row = tt / tiles_per_row;
+        const int pt = (int)(tt % tiles_per_row);
+        const int g = (int)(T.row / src.group), bb = (int)(T.row % src.group);
+        const int64_t sl = src.slot ? __builtin_amdgcn_readfirstlane(src.slot[g]) : g;
+        T.x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
+        T.n = __builtin_amdgcn_readfirstlane(src.n[g]);
+        T.px = (int64_t)pt * 32 + (lane & 31);
+        T.pxok = T.px < P;
+        return T;
+    };
     // layer-1 input: channels 0..C-1 in lane half 0, zero padding elsewhere
-    bf8 xb;
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-        const float v = (half == 0 && u < C && pxok) ? x[u * P + px] : 0.f;
-        xb[u] = (__bf16)v;
-    }
-
+    auto load_x = [&](const Tile& T) -> bf8 {
+        bf8 xb;
+        static_for<8>([&](auto uc) {
+            constexpr int u = decltype(uc)::value;
+            const float v = (half == 0 && u < C && T.pxok) ? T.x[u * P + T.px] : 0.f;
+            xb[u] = (__bf16)v;
+        });
+        return xb;
+    };
     const int nbranch = a.shift_c ? 2 : 1;
-    float eu[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int br = 0; br < nbranch; ++br) {
-        const float* shift = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * a.width;
-        f16v acc[NB];
-        bf8 H[NB][2];
 
-        dma(0, 0);
-        land();
-        dma(1, 1);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-            acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[0][nb * 64 + lane], xb, f16v{},
-                                                              0, 0, 0);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) activate(acc[nb], shift, nb, H[nb]);
-        land();
+    dma(0, 1, 0);
+    land();
+    Tile cur = locate(blockIdx.x);
+    bf8 xb = load_x(cur);
 
+    for (int64_t tg = blockIdx.x; tg < ngroups; tg += gridDim.x) {
+        const bool last_group = tg + gridDim.x >= ngroups;
+        Tile nxt = locate(last_group ? tg : tg + gridDim.x);
+        const bf8 xnx = load_x(nxt);
+
+        float eu[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int br = 0; br < nbranch; ++br) {
+            const float* shift = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)cur.n * a.width;
+            f16v acc[NB];
+            bf8 H[NB][2];
+
+            // ---- layer 1 (slab 0, buffer 0): K = C padded to 16
+            dma(1, SB, 1);
+            static_for<NB>([&](auto nbc) {
+                constexpr int nb = decltype(nbc)::value;
+                acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[0][nb * 64 + lane], xb, f16v{},
+                                                                  0, 0, 0);
+            });
+
+            // ---- layers 2 and 3: block b's MFMAs run while block b+1 is
+            // activated (its old accumulators stay live until then)
+            static_for<2>([&](auto lc) {
+                constexpr int layer = decltype(lc)::value;
+                const float* vin = layer == 0 ? shift : a.b2;
+                act(acc[0], vin, 0, H[0]);
+                f16v nacc[NB];
+                static_for<NB>([&](auto nbc) { nacc[decltype(nbc)::value] = f16v{}; });
+                static_for<NSB>([&](auto sc) {
+                    constexpr int sb = decltype(sc)::value;
+                    constexpr int gslab = layer * NSB + sb;          // mid slab counter
+                    constexpr int buf = (gslab + 1) & 1;
+                    land();                                          // this slab has landed
+                    if constexpr (gslab + 1 < 2 * NSB)
+                        dma(1 + (gslab + 1) * SB, SB, buf ^ 1);
+                    else
+                        dma(1 + 2 * NB, 1, buf ^ 1);                 // layer 4
+                    static_for<SB>([&](auto ic) {
+                        constexpr int b = sb * SB + decltype(ic)::value;
+                        constexpr int base = decltype(ic)::value * L::SLM;
+                        bf8 w0 = lds[buf][base + (0 * NB + 0) * 64 + lane];
+                        bf8 w1 = NB > 1 ? lds[buf][base + (0 * NB + 1) * 64 + lane] : bf8{};
+                        static_for<SLOTS>([&](auto tc) {
+                            constexpr int slot = decltype(tc)::value;
+                            constexpr int g2 = slot / NBP, nb = 2 * (slot % NBP);
+                            constexpr int ns = slot + 1;
+                            constexpr int ng2 = ns / NBP, nnb = 2 * (ns % NBP);
+                            bf8 n0 = bf8{}, n1 = bf8{};
+                            if constexpr (ns < SLOTS) {
+                                n0 = lds[buf][base + (ng2 * NB + nnb) * 64 + lane];
+                                if constexpr (nnb + 1 < NB) n1 = lds[buf][base + (ng2 * NB + nnb + 1) * 64 + lane];
+                            }
+                            nacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, H[b][g2], nacc[nb], 0, 0, 0);
+                            if constexpr (nb + 1 < NB)
+                                nacc[nb + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, H[b][g2],
+                                                                                       nacc[nb + 1], 0, 0, 0);
+                            if constexpr (b + 1 < NB && slot == SLOTS / 2)   // just in time
+                                act(acc[b + 1], vin, b + 1, H[b + 1]);
+                            w0 = n0;
+                            w1 = n1;
+                        });
+                    });
+                });
+                static_for<NB>([&](auto nbc) { acc[decltype(nbc)::value] = nacc[decltype(nbc)::value]; });
+            });
+
+            // ---- layer 4 (slab 2NB+1, buffer 1)
+            {
+                constexpr int buf = (2 * NSB + 1) & 1;
+                land();
+                const bool more = br + 1 < nbranch || !last_group;
+                if (more) dma(0, 1, buf ^ 1);                    // next pass's layer 1
+                act(acc[0], a.b3, 0, H[0]);
+                f16v o2[2] = {f16v{}, f16v{}};
+                static_for<NB>([&](auto bc) {
+                    constexpr int b = decltype(bc)::value;
+                    static_for<2>([&](auto gc) {
+                        constexpr int g2 = decltype(gc)::value;
+                        o2[g2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[buf][(b * 2 + g2) * 64 + lane],
+                                                                         H[b][g2], o2[g2], 0, 0, 0);
+                    });
+                    if constexpr (b + 1 < NB) act(acc[b + 1], a.b3, b + 1, H[b + 1]);
+                });
+                const f16v o = o2[0] + o2[1];
+                float* out = eps + cur.row * (int64_t)C * P;
 #pragma unroll
-        for (int layer = 0; layer < 2; ++layer) {
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) acc[nb] = f16v{};
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                const int slab = 1 + layer * NB + b;
-                const int buf = slab & 1;
-                dma(slab + 1, buf ^ 1);
-#pragma unroll
-                for (int g2 = 0; g2 < 2; ++g2)
-#pragma unroll
-                    for (int nb = 0; nb < NB; nb += 2) {
-                        const bf8 w0 = lds[buf][(g2 * NB + nb) * 64 + lane];
-                        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, H[b][g2], acc[nb],
-                                                                          0, 0, 0);
-                        if (nb + 1 < NB) {
-                            const bf8 w1 = lds[buf][(g2 * NB + nb + 1) * 64 + lane];
-                            acc[nb + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                                w1, H[b][g2], acc[nb + 1], 0, 0, 0);
+                for (int r = 0; r < 4; ++r) {
+                    const int c = 4 * half + r;
+                    if (c < C) {
+                        const float v = o[r] + a.b4[c];
+                        if (br == 0) {
+                            eu[r] = v;
+                            if (nbranch == 1 && cur.active && cur.pxok) out[c * P + cur.px] = v;
+                        } else if (cur.active && cur.pxok) {
+                            out[c * P + cur.px] = eu[r] + a.guidance * (v - eu[r]);
                         }
                     }
+                }
                 land();
             }
-            const float* bias = layer == 0 ? a.b2 : a.b3;
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) activate(acc[nb], bias, nb, H[nb]);
         }
-
-        {
-            constexpr int slab = 1 + 2 * NB;
-            constexpr int buf = slab & 1;
-            f16v o2[2] = {f16v{}, f16v{}};
-#pragma unroll
-            for (int b = 0; b < NB; ++b)
-#pragma unroll
-                for (int g2 = 0; g2 < 2; ++g2)
-                    o2[g2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        lds[buf][(b * 2 + g2) * 64 + lane], H[b][g2], o2[g2], 0, 0, 0);
-            __syncthreads();   // the next branch overwrites both buffers
-            const f16v o = o2[0] + o2[1];
-            float* out = eps + row * (int64_t)C * P;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int c = 4 * half + r;
-                if (c < C) {
-                    const float v = o[r] + a.b4[c];
-                    if (br == 0) {
-                        eu[r] = v;
-                        if (nbranch == 1 && active && pxok) out[c * P + px] = v;
-                    } else if (active && pxok) {
-                        out[c * P + px] = eu[r] + a.guidance * (v - eu[r]);
-                    }
-                }
-            }
-        }
+        cur = nxt;
+        xb = xnx;
     }
 }
 
@@ -484,12 +538,15 @@ void pack_bf16_t(const float* W1, const float* W2, const float* W3, const float*
                         (l % 32 < C) ? to_bf16(W4[(l % 32) * W + fin(b, g2, l, u)]) : (uint16_t)0;
 }
 
+int device_cus();
+
 template <int NB, int C>
 void launch_bf16_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
     const int tiles_per_row = (int)((a.P + 31) / 32);
     const int64_t ntiles = (int64_t)src.max_groups * src.group * tiles_per_row;
     if (ntiles == 0) return;
-    const int64_t blocks = (ntiles + 3) / 4;
+    int64_t blocks = (ntiles + 3) / 4;                       // persistent: one block per CU
+    if (blocks > device_cus()) blocks = device_cus();
     hipLaunchKernelGGL((k_conv_bf16<NB, C>), dim3((unsigned)blocks), dim3(256), 0, s, a, src, eps,
                        tiles_per_row);
     PD_HIP(hipGetLastError());
