@@ -44,7 +44,7 @@ struct LoopState {
     int32_t f;       // frontier: highest trajectory index holding a computed point
     int32_t p_eff;   // size of the current window; 0 once t >= T or after an error
     int32_t status;  // PD_OK or PD_ERR_NUMERIC
-    int32_t pad;
+    int32_t first_stride;  // stride of iteration 0 (the window of copies of x_0)
     int64_t evals;   // sum of window sizes
 };
 

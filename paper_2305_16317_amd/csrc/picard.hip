@@ -38,7 +38,7 @@ __global__ void k_picard_init(LoopState* st, int32_t* slot, int32_t* nrow,
         st->f = 0;
         st->p_eff = pe;
         st->status = PD_OK;
-        st->pad = 0;
+        st->first_stride = 0;
         st->evals = 0;
     }
     for (int j = threadIdx.x; j < pe; j += blockDim.x) {
@@ -231,6 +231,7 @@ __global__ __launch_bounds__(1024) void k_picard_finalize(
     const int pn = s_bad ? 0 : (p < T - tn ? p : T - tn);
     if (threadIdx.x == 0) {
         trace[k] = stride;
+        if (k == 0) st->first_stride = stride;
         st->k = k + 1;
         st->evals += pe;
         st->f = fn;

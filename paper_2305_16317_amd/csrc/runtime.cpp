@@ -641,12 +641,15 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         int t_host = 0, k_host = 0, issued = 0;
         for (;;) {
             // every iteration advances t by at most pc, so at least this many
-            // more are needed; once strides have been seen, enqueue as many as
-            // the mean stride so far predicts.  Iterations enqueued past the
-            // end find p_eff = 0 on the device and return at once.
+            // more are needed; once two strides have been seen, enqueue as many
+            // as the mean stride after the first predicts (the first window is
+            // all copies of x_0 and always slides by one).  Iterations enqueued
+            // past the end find p_eff = 0 on the device and return at once.
             int need = (T - t_host + pc - 1) / pc;
-            if (k_host > 0 && t_host > 0) {
-                const int est = (int)std::ceil((double)(T - t_host) * k_host / (double)t_host);
+            const int first_stride = w.h_state->first_stride;
+            if (k_host >= 2 && t_host > first_stride) {
+                const double mean = (double)(t_host - first_stride) / (double)(k_host - 1);
+                const int est = (int)std::ceil((double)(T - t_host) / mean);
                 need = need > est ? need : est;
             }
             need = need < T - t_host ? need : T - t_host;   // stride >= 1 bounds the rest
