@@ -62,6 +62,26 @@ struct GmmParams {
     int32_t K;
 };
 void launch_gmm_eps(const GmmParams& g, const RowSrc& src, float* eps, hipStream_t s);
+// The whole Picard (or sequential) loop of the mixture model in one workgroup.
+struct GmmLoopArgs {
+    GmmParams g;
+    const float* A;         // [T] drift coefficients
+    const float* B;
+    const float* tol_var;   // [T]
+    const int32_t* model_t; // [T]
+    const float* noise;     // [T][batch][2] or nullptr
+    const float* x0;        // [batch][2]
+    float* out;             // [batch][2]
+    LoopState* st;          // final state (t, k, evals, status)
+    int32_t* trace;         // [T] stride of every iteration
+    int32_t T, p, batch, tol_offset;
+    float tau2;
+};
+// LDS bytes the Picard loop needs at least (noise read per window from HBM);
+// the launcher stages all the noise in LDS when that fits in `max_lds`.
+size_t gmm_loop_lds_bytes(int T, int K, int p, int batch);
+void launch_gmm_picard_loop(const GmmLoopArgs& a, size_t max_lds, hipStream_t s);
+void launch_gmm_sequential_loop(const GmmLoopArgs& a, hipStream_t s);
 
 // mlp.hip: y = act(x W^T + bias [+ shift[n_row]]) with fp32 MFMA.
 enum Act { ACT_NONE = 0, ACT_GELU = 1 };

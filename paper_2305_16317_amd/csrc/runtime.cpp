@@ -269,18 +269,20 @@ struct pd_denoiser {
 
     bool guided() const { return desc.cond_dim > 0; }
 
+    GmmParams gmm() const {
+        return GmmParams{means.as<float>(), g_a.as<float>(), g_inv2s2.as<float>(), g_coef.as<float>(),
+                         desc.n_components};
+    }
+
     size_t scratch_floats(int64_t rows) const {
         return desc.kind == PD_MODEL_MLP ? (size_t)(2 * rows * desc.width) : 0;
     }
 
     void forward(const RowSrc& src, float* eps, float* scratch, hipStream_t s) const {
         switch (desc.kind) {
-            case PD_MODEL_GMM2D: {
-                GmmParams g{means.as<float>(), g_a.as<float>(), g_inv2s2.as<float>(),
-                            g_coef.as<float>(), desc.n_components};
-                launch_gmm_eps(g, src, eps, s);
+            case PD_MODEL_GMM2D:
+                launch_gmm_eps(gmm(), src, eps, s);
                 break;
-            }
             case PD_MODEL_MLP: {
                 const int Wd = desc.width;
                 const int64_t rows = (int64_t)src.max_groups * src.group;
@@ -575,6 +577,35 @@ static void fill_stats(pd_sample_stats* stats, int iters, int64_t evals, int bat
     }
 }
 
+// The mixture model's whole sampling loop fits in one workgroup's LDS.
+static constexpr size_t kFusedLoopLds = 64 * 1024;
+
+static bool use_fused_gmm_loop(const pd_denoiser& d, int T, int p, int batch) {
+    return d.desc.kind == PD_MODEL_GMM2D &&
+           gmm_loop_lds_bytes(T, d.desc.n_components, p, batch) <= kFusedLoopLds;
+}
+
+static GmmLoopArgs gmm_loop_args(const pd_schedule& s, const pd_denoiser& d, pd_workspace& w, int p,
+                                 int batch, float tau2, float* x_out) {
+    GmmLoopArgs a;
+    a.g = d.gmm();
+    a.A = w.A.as<float>();
+    a.B = w.B.as<float>();
+    a.tol_var = w.tolv.as<float>();
+    a.model_t = w.model_t.as<int32_t>();
+    a.noise = w.noise.p ? w.noise.as<float>() : nullptr;
+    a.x0 = w.ring.as<float>();
+    a.out = x_out;
+    a.st = w.state.as<LoopState>();
+    a.trace = w.trace.as<int32_t>();
+    a.T = s.T;
+    a.p = p;
+    a.batch = batch;
+    a.tol_offset = s.desc.tol_index_offset;
+    a.tau2 = tau2;
+    return a;
+}
+
 extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoiser* d,
                                           uint64_t noise_seed, int32_t batch,
                                           const int64_t* sample_shape, int32_t ndim, float* x_out,
@@ -591,6 +622,17 @@ extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoise
         tm.on = stats && stats->time_kernels;
         tm.st = st;
         draw_noise(w, noise_seed, st);
+        if (use_fused_gmm_loop(*d, s->T, 1, batch)) {
+            tm.mark(-1);
+            launch_gmm_sequential_loop(gmm_loop_args(*s, *d, w, 1, batch, 0.f, x_out), st);
+            tm.mark(CAT_UPDATE);
+            PD_HIP(hipStreamSynchronize(st));
+            tm.collect();
+            fill_stats(stats, s->T, s->T, batch, d->guided(), nullptr, tm);
+            const int n = stats ? (s->T < stats->trace_cap ? s->T : stats->trace_cap) : 0;
+            for (int i = 0; i < n && stats->stride_trace; ++i) stats->stride_trace[i] = 1;
+            return;
+        }
         for (int i = 0; i < s->T; ++i) {
             const RowSrc src{x, nullptr, BD, batch, 1, w.model_t.as<int32_t>() + i, nullptr};
             tm.mark(-1);
@@ -634,6 +676,18 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         tm.on = stats && stats->time_kernels;
         tm.st = st;
         draw_noise(w, noise_seed, st);
+        if (use_fused_gmm_loop(*d, T, pc, batch)) {
+            tm.mark(-1);
+            launch_gmm_picard_loop(gmm_loop_args(*s, *d, w, pc, batch, tau2, x_out), kFusedLoopLds,
+                                   st);
+            tm.mark(CAT_UPDATE);
+            PD_HIP(hipMemcpyAsync(w.h_state, dst, sizeof(LoopState), hipMemcpyDeviceToHost, st));
+            PD_HIP(hipStreamSynchronize(st));
+            if (w.h_state->status != PD_OK) fail(PD_ERR_NUMERIC, "non-finite point or error in the window");
+            tm.collect();
+            fill_stats(stats, w.h_state->k, w.h_state->evals, batch, d->guided(), w.trace.as<int32_t>(), tm);
+            return;
+        }
         launch_picard_init(dst, w.slot.as<int32_t>(), w.nrow.as<int32_t>(),
                            w.model_t.as<int32_t>(), T, pc, st);
         const RowSrc src{w.ring.as<float>(), w.slot.as<int32_t>(), BD,     batch,

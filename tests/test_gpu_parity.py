@@ -174,6 +174,11 @@ def _run(wl, weights, sampler="picard", p=None, tau=None, workspace=None, seed=N
 SMALL = {
     "gmm_full": lambda: W.WORKLOADS["gmm2d_ddpm100"],
     "gmm_p7_b3": lambda: W.small_variant("gmm2d_ddpm100", p=7, batch=3),
+    # too large for the single-workgroup loop: runs the general kernels
+    "gmm_b48_general": lambda: W.small_variant("gmm2d_ddpm100", p=100, batch=48),
+    # component counts past the register-held means (16) and between 8 and 16
+    "gmm_k12": lambda: W.small_variant("gmm2d_ddpm100", p=20, batch=2, n_components=12),
+    "gmm_k40": lambda: W.small_variant("gmm2d_ddpm100", p=33, batch=5, n_components=40),
     "mlp_full": lambda: W.WORKLOADS["policy_mlp_ddpm100"],
     "mlp_small": lambda: W.small_variant("policy_mlp_ddpm100", T=30, p=9, shape=(4, 3), width=32, batch=2),
     "conv_ddpm": lambda: W.small_variant("latent_ddpm1000_p64", T=40, p=16, shape=(4, 16, 16), width=64),
@@ -220,7 +225,8 @@ def test_picard_matches_oracle(name):
     assert _rel(got, ref.x) <= REL_F32, _rel(got, ref.x)
 
 
-@pytest.mark.parametrize("name", ["gmm_p7_b3", "mlp_small", "conv_ddpm", "conv_ddim_b3"])
+@pytest.mark.parametrize("name", ["gmm_p7_b3", "gmm_k12", "gmm_k40", "mlp_small", "conv_ddpm",
+                                  "conv_ddim_b3"])
 def test_sequential_matches_oracle(name):
     wl = SMALL[name]()
     w = W.make_weights(wl.model)
@@ -230,7 +236,7 @@ def test_sequential_matches_oracle(name):
     assert _rel(got, ref) <= REL_F32
 
 
-@pytest.mark.parametrize("name", ["gmm_p7_b3", "mlp_small", "conv_ddpm", "conv_ddim_b3"])
+@pytest.mark.parametrize("name", ["gmm_p7_b3", "gmm_k40", "mlp_small", "conv_ddpm", "conv_ddim_b3"])
 def test_window_of_one_is_sequential_bitwise(name):
     wl = SMALL[name]()
     w = W.make_weights(wl.model)

@@ -100,7 +100,8 @@ WORKLOADS: Dict[str, Workload] = {
 
 def small_variant(name: str, *, T: int | None = None, p: int | None = None,
                   shape: Tuple[int, ...] | None = None, width: int | None = None,
-                  batch: int | None = None, tau: float | None = None) -> Workload:
+                  batch: int | None = None, tau: float | None = None,
+                  n_components: int | None = None) -> Workload:
     """A reduced copy of a named workload (for tests the oracle finishes fast)."""
     w = WORKLOADS[name]
     s = w.schedule
@@ -112,6 +113,8 @@ def small_variant(name: str, *, T: int | None = None, p: int | None = None,
         m = dataclasses.replace(m, sample_shape=tuple(shape))
     if width is not None:
         m = dataclasses.replace(m, width=width)
+    if n_components is not None:
+        m = dataclasses.replace(m, n_components=n_components)
     return dataclasses.replace(
         w, name=w.name + "_small", schedule=s, model=m,
         p=w.p if p is None else p, tau=w.tau if tau is None else tau,
