@@ -13,20 +13,38 @@
 namespace pd {
 namespace {
 
-constexpr int kScanWaves = 4;             // waves per scan block, split along the window
-constexpr int kScanCols = 64;             // columns (sample elements) per scan block
-constexpr int kScanMaxRows = 32;          // rows per wave: windows up to 4 * 32 = 128 points
+constexpr int kScanWaves = 16;            // waves per scan block, split along the window
+constexpr int kScanMaxRows = 8;           // rows per wave: windows up to 16 * 8 = 128 points
 constexpr int kMaxWindow = kScanWaves * kScanMaxRows;
+
+// Columns per lane of the scan: four (one 16-byte access per row) when the
+// sample size allows it, else one.
+inline int scan_vec(int64_t D) { return D % 4 == 0 ? 4 : 1; }
+
+template <int VEC>
+struct Cols;
+template <>
+struct Cols<1> {
+    typedef float type;
+};
+template <>
+struct Cols<4> {
+    typedef float type __attribute__((ext_vector_type(4)));
+};
+template <int VEC>
+__device__ __forceinline__ float& col_at(typename Cols<VEC>::type& v, int c) {
+    if constexpr (VEC == 1) return v;
+    else return reinterpret_cast<float*>(&v)[c];
+}
+template <int VEC>
+__device__ __forceinline__ float col_at(const typename Cols<VEC>::type& v, int c) {
+    if constexpr (VEC == 1) return v;
+    else return v[c];
+}
 
 __device__ __forceinline__ float drift(float A, float x, float B, float e) {
     // y = A x + B eps, two products and one sum, each rounded (no contraction)
     return __fadd_rn(__fmul_rn(A, x), __fmul_rn(B, e));
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
 }
 
 __global__ void k_picard_init(LoopState* st, int32_t* slot, int32_t* nrow,
@@ -47,135 +65,142 @@ __global__ void k_picard_init(LoopState* st, int32_t* slot, int32_t* nrow,
     }
 }
 
-// Sum each of the R values v[0..R) of a lane over the 64 lanes of the wave.
-// Butterfly with halving: at every step a lane keeps half of its values and
-// adds the partner's copy of that half, so R - 1 + log2(64/R) shuffles cover
-// all R sums (instead of 6 R).  Returns the full sum of value index `idx`
-// (a function of the lane); lanes with (lane & (64/R - 1)) == 0 hold distinct
-// indices.  Every sum is formed in a fixed order, so results are reproducible.
-template <int R>
-__device__ __forceinline__ float multi_wave_sum(float (&v)[R], int lane, int& idx) {
-    idx = 0;
-#pragma unroll
-    for (int h = R / 2, bit = 32; h >= 1; h /= 2, bit /= 2) {
-        const bool upper = (lane & bit) != 0;
-#pragma unroll
-        for (int i = 0; i < h; ++i) {
-            const float keep = upper ? v[i + h] : v[i];
-            const float send = upper ? v[i] : v[i + h];
-            v[i] = keep + __shfl_xor(send, bit, 64);
-        }
-        if (upper) idx += h;
-    }
-    float r = v[0];
-#pragma unroll
-    for (int bit = 32 / R; bit >= 1; bit /= 2) r += __shfl_xor(r, bit, 64);
-    return r;
-}
-
-// One block: 64 columns of one sample b, all window rows, split over 4 waves
-// (rows [w*ch, (w+1)*ch) per wave, ch <= R).  Drift and noise are summed along
-// the rows inside each wave, the wave totals are exchanged through LDS, and
-// the new points x^{k+1}_{t+j+1} = x_t + sum y + sum z are written back to the
-// ring.  All loads use clamped, always-valid indices and no branches, so the
-// R rows' loads of a wave are in flight together.  The squared differences
-// against the old points are reduced over the 64 columns per window offset
-// and written as per-block partial sums partials[b][o][blk]; offset 0 (never
-// tested) carries the count of non-finite new points instead.
-template <int R, bool NOISE>
-__global__ __launch_bounds__(256) void k_picard_scan(
+// One block: 64 * VEC consecutive columns of one sample b, all window rows,
+// split over 16 waves (rows [w*ch, (w+1)*ch) per wave, ch <= R).  Drift and
+// noise are summed along the rows inside each wave, the wave totals are
+// exchanged through LDS, and the new points x^{k+1}_{t+j+1} = x_t + sum y +
+// sum z are written back to the ring.  All loads use clamped, always-valid
+// indices and no branches, so a wave's rows are in flight together; the drift
+// coefficients of a wave's rows come in one vector load and are broadcast
+// with readlane.  The squared differences against the old points are summed
+// per lane over its columns, transposed through LDS and reduced per window
+// offset into per-block partial sums partials[b][o][blk]; offset 0 (never
+// tested) carries the count of non-finite points in the window's last row
+// (a non-finite point in any other row makes its error non-finite).
+template <int R, int VEC, bool NOISE>
+__global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     const LoopState* __restrict__ st, float* ring, const float* __restrict__ eps,
     const float* __restrict__ noise, const float* __restrict__ Atab,
     const float* __restrict__ Btab, int p, int batch, int64_t D, float* __restrict__ partials) {
+    typedef typename Cols<VEC>::type V;
+    constexpr int NW = kScanWaves;
     const int pe = st->p_eff;
     if (pe <= 0) return;
     const int t = st->t, f = st->f;
     // the wave index is uniform: keep it (and every row index derived from
-    // it) in scalar registers so the per-row table reads are scalar loads
+    // it) in scalar registers
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int b = blockIdx.y, blk = blockIdx.x, nblk = gridDim.x;
-    const int64_t d = (int64_t)blk * kScanCols + lane;
+    const int64_t d = ((int64_t)blk * 64 + lane) * VEC;   // D is a multiple of VEC
     const bool valid = d < D;
     const int64_t slotsz = (int64_t)batch * D;
     const int64_t col = (int64_t)b * D + (valid ? d : 0);
     const int P1 = p + 1;
-    const int ch = (pe + kScanWaves - 1) / kScanWaves;
+    const int ch = (pe + NW - 1) / NW;
     const int j0 = min(w * ch, pe), j1 = min(j0 + ch, pe);
     const int nr = j1 - j0;
 
-    __shared__ float s_tot[2][kScanWaves][kScanCols];
-    __shared__ float s_first[kScanWaves][kScanCols];
-    __shared__ float s_bad[kScanWaves];
+    // wave totals and first old points, then (after a barrier) the
+    // per-row squared differences of every lane
+    __shared__ union {
+        struct {
+            V tot[2][NW][64];
+            V first[NW][64];
+        } x;
+        float d2[NW * R][65];
+    } sh;
 
     // ---- every read of this block's ring columns is consumed before the
-    // barrier; the writes all come after it (the ring slots overlap).
-    const float anchor = ring[(int64_t)(t % P1) * slotsz + col];
+    // first barrier; the writes all come after it (the ring slots overlap).
+    const V anchor = *reinterpret_cast<const V*>(ring + (int64_t)(t % P1) * slotsz + col);
     const int slot_f = f % P1;
-    float xo[R], e[R], z[R], ca[R], cb[R];
+    const int jt = min(j0 + (lane < R ? lane : R - 1), pe - 1);   // lane r: row j0 + r
+    const float ta = Atab[t + jt], tb = Btab[t + jt];
+    V xo[R], y[R], z[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int j = min(j0 + r, pe - 1);            // clamped: always a window row
         const int m = t + j;
         const int sl = m <= f ? m % P1 : slot_f;      // points past f equal x_f
-        xo[r] = ring[(int64_t)sl * slotsz + col];
-        e[r] = eps[(int64_t)j * slotsz + col];
-        z[r] = NOISE ? noise[(int64_t)m * slotsz + col] : 0.f;
-        ca[r] = Atab[m];
-        cb[r] = Btab[m];
+        xo[r] = *reinterpret_cast<const V*>(ring + (int64_t)sl * slotsz + col);
+        y[r] = *reinterpret_cast<const V*>(eps + (int64_t)j * slotsz + col);
+        if constexpr (NOISE) z[r] = *reinterpret_cast<const V*>(noise + (int64_t)m * slotsz + col);
+        else z[r] = V(0.f);
     }
-    // drifts of every (clamped) row first, then the masked running sums: no
-    // load is left behind a condition
-    float y[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) y[r] = drift(ca[r], xo[r], cb[r], e[r]);
-    float sy[R], sz[R];
-    float acc_y = 0.f, acc_z = 0.f;
+    // drifts replace eps in y; rows past the wave's range count as zero
+    V acc_y = V(0.f), acc_z = V(0.f);
 #pragma unroll
     for (int r = 0; r < R; ++r) {
+        const float ca = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ta), r));
+        const float cb = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, tb), r));
         const bool in = r < nr;
-        acc_y = __fadd_rn(acc_y, in ? y[r] : 0.f);
-        acc_z = __fadd_rn(acc_z, in ? z[r] : 0.f);
-        sy[r] = acc_y;
-        sz[r] = acc_z;
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+            const float v = drift(ca, col_at<VEC>(xo[r], c), cb, col_at<VEC>(y[r], c));
+            col_at<VEC>(y[r], c) = in ? v : 0.f;
+            if (!in) col_at<VEC>(z[r], c) = 0.f;
+            col_at<VEC>(acc_y, c) = __fadd_rn(col_at<VEC>(acc_y, c), col_at<VEC>(y[r], c));
+            col_at<VEC>(acc_z, c) = __fadd_rn(col_at<VEC>(acc_z, c), col_at<VEC>(z[r], c));
+        }
     }
-    s_tot[0][w][lane] = acc_y;
-    s_tot[1][w][lane] = acc_z;
-    s_first[w][lane] = xo[0];       // x^k_{t+j0}: the next wave's old point past its range
+    sh.x.tot[0][w][lane] = acc_y;
+    sh.x.tot[1][w][lane] = acc_z;
+    sh.x.first[w][lane] = xo[0];   // x^k_{t+j0}: the previous wave's old point past its range
     __syncthreads();
-    float py = 0.f, pz = 0.f;
+    V py = V(0.f), pz = V(0.f);
     for (int v = 0; v < w; ++v) {
-        py = __fadd_rn(py, s_tot[0][v][lane]);
-        pz = __fadd_rn(pz, s_tot[1][v][lane]);
+        const V a = sh.x.tot[0][v][lane], c2 = sh.x.tot[1][v][lane];
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+            col_at<VEC>(py, c) = __fadd_rn(col_at<VEC>(py, c), col_at<VEC>(a, c));
+            col_at<VEC>(pz, c) = __fadd_rn(col_at<VEC>(pz, c), col_at<VEC>(c2, c));
+        }
     }
-    const float next_old = (w + 1 < kScanWaves) ? s_first[w + 1][lane] : 0.f;
+    const V next_old = (w + 1 < NW) ? sh.x.first[w + 1][lane] : V(0.f);
+    __syncthreads();
 
-    // ---- new points, their errors, and the writes
-    float bad = 0.f, d2[R];
+    // ---- new points, their squared differences, and the writes
+    V sy = V(0.f), sz = V(0.f);
 #pragma unroll
     for (int r = 0; r < R; ++r) {
         const int j = j0 + r;
-        const float xn = __fadd_rn(__fadd_rn(anchor, __fadd_rn(py, sy[r])), __fadd_rn(pz, sz[r]));
         const bool in = r < nr;
-        if (in && valid) {
-            ring[(int64_t)((t + j + 1) % P1) * slotsz + col] = xn;
-            bad += isfinite(xn) ? 0.f : 1.f;
-        }
         // error of window offset o = j + 1: x^{k+1}_{t+j+1} against x^k_{t+j+1}
-        const float xold = (r + 1 < R && r + 1 < nr) ? xo[r + 1 < R ? r + 1 : r] : next_old;
-        const float dl = (in && valid && j + 1 < pe) ? __fsub_rn(xn, xold) : 0.f;
-        d2[r] = dl * dl;
+        const V xold = (r + 1 < R && r + 1 < nr) ? xo[r + 1 < R ? r + 1 : r] : next_old;
+        V xn;
+        float acc = 0.f;
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+            col_at<VEC>(sy, c) = __fadd_rn(col_at<VEC>(sy, c), col_at<VEC>(y[r], c));
+            col_at<VEC>(sz, c) = __fadd_rn(col_at<VEC>(sz, c), col_at<VEC>(z[r], c));
+            const float v = __fadd_rn(
+                __fadd_rn(col_at<VEC>(anchor, c), __fadd_rn(col_at<VEC>(py, c), col_at<VEC>(sy, c))),
+                __fadd_rn(col_at<VEC>(pz, c), col_at<VEC>(sz, c)));
+            col_at<VEC>(xn, c) = v;
+            if (j + 1 < pe) {
+                const float dl = __fsub_rn(v, col_at<VEC>(xold, c));
+                acc += dl * dl;
+            } else {
+                acc += isfinite(v) ? 0.f : 1.f;     // last row: count non-finite points
+            }
+        }
+        if (in && valid) *reinterpret_cast<V*>(ring + (int64_t)((t + j + 1) % P1) * slotsz + col) = xn;
+        sh.d2[w * R + r][lane] = (in && valid) ? acc : 0.f;
     }
-    int idx;
-    const float s = multi_wave_sum<R>(d2, lane, idx);
-    if ((lane & (64 / R - 1)) == 0 && idx < nr && j0 + idx + 1 < pe)
-        partials[((int64_t)b * p + j0 + idx + 1) * nblk + blk] = s;
-    bad = wave_sum(bad);
-    if (lane == 0) s_bad[w] = bad;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        float nb = 0.f;
-        for (int v = 0; v < kScanWaves; ++v) nb += s_bad[v];
-        partials[((int64_t)b * p + 0) * nblk + blk] = nb;
+    // row q of the NW * R (wave, row) pairs is summed by 64 / R threads
+    constexpr int TPR = 64 / R;
+    const int q = threadIdx.x / TPR, part = threadIdx.x % TPR;
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 64 / TPR; ++i) s += sh.d2[q][part + TPR * i];
+#pragma unroll
+    for (int off = TPR / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+    const int qw = q / R, qr = q % R;
+    const int q0 = min(qw * ch, pe), nq = min(q0 + ch, pe) - q0;
+    if (part == 0 && qr < nq) {
+        const int jq = q0 + qr;
+        partials[((int64_t)b * p + (jq + 1 < pe ? jq + 1 : 0)) * nblk + blk] = s;
     }
 }
 
@@ -259,7 +284,10 @@ __global__ __launch_bounds__(256) void k_seq_step(float* __restrict__ x,
 
 }  // namespace
 
-int picard_partial_blocks(int64_t D) { return (int)((D + kScanCols - 1) / kScanCols); }
+int picard_partial_blocks(int64_t D) {
+    const int64_t cols = 64 * (int64_t)scan_vec(D);
+    return (int)((D + cols - 1) / cols);
+}
 
 void launch_picard_init(LoopState* st, int32_t* slot, int32_t* nrow, const int32_t* model_t,
                         int T, int p, hipStream_t s) {
@@ -267,26 +295,34 @@ void launch_picard_init(LoopState* st, int32_t* slot, int32_t* nrow, const int32
     PD_HIP(hipGetLastError());
 }
 
+template <int R, int VEC>
+static void launch_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
+                        const float* A, const float* B, int p, int batch, int64_t D,
+                        float* partials, hipStream_t s) {
+    const dim3 grid((unsigned)picard_partial_blocks(D), (unsigned)batch);
+    if (noise)
+        hipLaunchKernelGGL((k_picard_scan<R, VEC, true>), grid, dim3(kScanWaves * 64), 0, s, st,
+                           ring, eps, noise, A, B, p, batch, D, partials);
+    else
+        hipLaunchKernelGGL((k_picard_scan<R, VEC, false>), grid, dim3(kScanWaves * 64), 0, s, st,
+                           ring, eps, noise, A, B, p, batch, D, partials);
+    PD_HIP(hipGetLastError());
+}
+
 void launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
                         const float* A, const float* B, int p, int batch, int64_t D,
                         float* partials, hipStream_t s) {
     if (p > kMaxWindow) fail(PD_ERR_UNSUPPORTED, "window larger than 128 points");
-    const dim3 grid((unsigned)picard_partial_blocks(D), (unsigned)batch);
     const int ch = (p + kScanWaves - 1) / kScanWaves;    // rows per wave at a full window
-#define PD_SCAN(R)                                                                           \
-    if (ch <= R) {                                                                           \
-        if (noise)                                                                           \
-            hipLaunchKernelGGL((k_picard_scan<R, true>), grid, dim3(kScanWaves * 64), 0, s, st, \
-                               ring, eps, noise, A, B, p, batch, D, partials);               \
-        else                                                                                 \
-            hipLaunchKernelGGL((k_picard_scan<R, false>), grid, dim3(kScanWaves * 64), 0, s,    \
-                               st, ring, eps, noise, A, B, p, batch, D, partials);           \
-        PD_HIP(hipGetLastError());                                                           \
-        return;                                                                              \
+    const bool v4 = scan_vec(D) == 4;
+#define PD_SCAN(R)                                                                         \
+    if (ch <= R) {                                                                         \
+        if (v4) launch_scan<R, 4>(st, ring, eps, noise, A, B, p, batch, D, partials, s);   \
+        else launch_scan<R, 1>(st, ring, eps, noise, A, B, p, batch, D, partials, s);      \
+        return;                                                                            \
     }
-    PD_SCAN(1) PD_SCAN(2) PD_SCAN(4) PD_SCAN(8) PD_SCAN(16) PD_SCAN(32)
+    PD_SCAN(1) PD_SCAN(2) PD_SCAN(4) PD_SCAN(8)
 #undef PD_SCAN
-    PD_HIP(hipGetLastError());
 }
 
 void launch_picard_finalize(LoopState* st, const float* partials, int p, int batch, int64_t D,

@@ -326,3 +326,18 @@ def test_full_size_sequential_matches_oracle(name):
     wl = W.WORKLOADS[name]
     got, st = _run(wl, W.make_weights(wl.model), "sequential")
     _check_summary(got, g["sequential"], REL_F32)
+
+
+def test_full_size_bf16_picard_matches_oracle():
+    """Guided bf16 workload at full size (4x96x96, width 320, T=1000, p=128):
+    sampled outputs and the norm within 2e-2 of the oracle run with the same
+    bf16 operand rounding; the iteration count within 10% (a stride decision
+    may sit within rounding noise of the tolerance)."""
+    name = "latent_cfg_bf16_ddpm1000_p128"
+    g = _golden(name)
+    wl = W.WORKLOADS[name]
+    got, st = _run(wl, W.make_weights(wl.model))
+    gp = g["picard"]
+    assert abs(st.iters - gp["iters"]) <= max(1, gp["iters"] // 10), (st.iters, gp["iters"])
+    assert st.network_rows == st.evals_per_sample * 2
+    _check_summary(got, gp, 2e-2)
