@@ -210,15 +210,31 @@ def main() -> int:
                                    "finalize": fin_ms / a.steps,
                                    "other": ms_per_step - (den_ms + upd_ms + fin_ms) / a.steps},
     }
+    # sample latency per noise seed without kernel events (they cost a few
+    # microseconds of GPU time each): median over seeds 0..9, and the range of K
+    lat, ks = [], []
+    for s in range(10):
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        st = pd.pd_sample_picard(sched, den, wl.p, wl.tau, s, wl.batch, shape, x, workspace=ws,
+                                 stream=stream)
+        torch.cuda.synchronize()
+        lat.append(1e3 * (time.perf_counter() - t1))
+        ks.append(st.iters)
+    out["latency_ms_median_seeds_0_9"] = float(np.median(lat))
+    out["iters_K_seeds_0_9"] = {"seed0": ks[0], "min": min(ks), "max": max(ks)}
     if not a.no_sequential:
         pd.pd_sample_sequential(sched, den, 0, wl.batch, shape, x, workspace=ws)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        pd.pd_sample_sequential(sched, den, 0, wl.batch, shape, x, workspace=ws)
-        torch.cuda.synchronize()
-        seq_ms = 1e3 * (time.perf_counter() - t0)
+        seq = []
+        for _ in range(3):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            pd.pd_sample_sequential(sched, den, 0, wl.batch, shape, x, workspace=ws)
+            torch.cuda.synchronize()
+            seq.append(1e3 * (time.perf_counter() - t0))
+        seq_ms = float(np.median(seq))
         out["sequential_ms"] = seq_ms
-        out["speedup_vs_sequential"] = seq_ms / ms_per_step
+        out["speedup_vs_sequential"] = seq_ms / out["latency_ms_median_seeds_0_9"]
     if a.copy_bytes > 0:
         n = a.copy_bytes // 4
         src = torch.ones(n, device="cuda")

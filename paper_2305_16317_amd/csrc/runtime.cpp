@@ -116,10 +116,14 @@ struct KernelTimer {
     ~KernelTimer() {
         for (hipEvent_t e : ev) (void)hipEventDestroy(e);
     }
-    void mark(int category) {        // category < 0: start of an interval
+    // category < 0: start of an interval.  Consecutive intervals share their
+    // boundary event, so a start mark is only needed after a gap (a host
+    // synchronisation or a copy).  The events carry no system-scope fence:
+    // they are read only after the stream has been synchronised.
+    void mark(int category) {
         if (!on) return;
         hipEvent_t e;
-        PD_HIP(hipEventCreate(&e));
+        PD_HIP(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
         ev.push_back(e);
         cat.push_back(category);
         PD_HIP(hipEventRecord(e, st));
@@ -633,9 +637,9 @@ extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoise
             for (int i = 0; i < n && stats->stride_trace; ++i) stats->stride_trace[i] = 1;
             return;
         }
+        tm.mark(-1);
         for (int i = 0; i < s->T; ++i) {
             const RowSrc src{x, nullptr, BD, batch, 1, w.model_t.as<int32_t>() + i, nullptr};
-            tm.mark(-1);
             d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
             tm.mark(CAT_DENOISER);
             const float* z = w.noise.p ? w.noise.as<float>() + (int64_t)i * BD : nullptr;
@@ -695,20 +699,25 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         int t_host = 0, k_host = 0, issued = 0;
         for (;;) {
             // every iteration advances t by at most pc, so at least this many
-            // more are needed; once two strides have been seen, enqueue as many
-            // as the mean stride after the first predicts (the first window is
-            // all copies of x_0 and always slides by one).  Iterations enqueued
-            // past the end find p_eff = 0 on the device and return at once.
+            // more are needed.  Beyond that, enqueue as many as the mean stride
+            // after the first predicts (the first window holds copies of x_0 and
+            // in practice slides by one), but at most as many as are already
+            // done: strides grow as the trajectory converges, so early means
+            // overestimate what is left, and iterations enqueued past the end
+            // (they find p_eff = 0 on the device and return at once) still cost
+            // a dispatch each.
             int need = (T - t_host + pc - 1) / pc;
+            if (issued == 0 && T > 1) need = 1 + (T - 1 + pc - 1) / pc;
             const int first_stride = w.h_state->first_stride;
             if (k_host >= 2 && t_host > first_stride) {
                 const double mean = (double)(t_host - first_stride) / (double)(k_host - 1);
-                const int est = (int)std::ceil((double)(T - t_host) / mean);
+                int est = (int)std::ceil((double)(T - t_host) / mean);
+                est = est < issued ? est : issued;
                 need = need > est ? need : est;
             }
             need = need < T - t_host ? need : T - t_host;   // stride >= 1 bounds the rest
+            tm.mark(-1);
             for (int it = 0; it < need; ++it) {
-                tm.mark(-1);
                 d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
                 tm.mark(CAT_DENOISER);
                 launch_picard_scan(dst, w.ring.as<float>(), w.eps.as<float>(), w.noise.as<float>(),
