@@ -53,23 +53,32 @@ def update_bytes(wl, p_eff_sum: int, has_noise: bool) -> float:
     return float(per) * wl.batch * wl.model.D * p_eff_sum
 
 
-def _source_hash() -> str:
+KERNEL_SOURCES = {"k_conv": ["conv.hip"], "k_picard": ["picard.hip"], "k_linear": ["mlp.hip"],
+                  "k_gmm": ["gmm.hip"], "k_normals": ["rng.hip"]}
+
+
+def source_hash(kernel_tag: str) -> str:
+    """Hash of the source file(s) a kernel is built from (plus the shared
+    internal header): counter figures are void once it changes."""
+    files = next((v for k, v in KERNEL_SOURCES.items() if kernel_tag.startswith(k)), None)
+    csrc = os.path.join(ROOT, "paper_2305_16317_amd", "csrc")
+    files = sorted(os.listdir(csrc)) if files is None else files + ["pd_internal.h"]
     h = hashlib.sha256()
-    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2305_16317_amd", "csrc"))):
-        h.update(open(os.path.join(ROOT, "paper_2305_16317_amd", "csrc", f), "rb").read())
+    for f in files:
+        h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 
 
-def traffic_from_profiles(kernel_tag: str):
+def traffic_from_profiles(workload: str, kernel_tag: str):
     """HBM bytes per launch from committed rocprofv3 counter summaries, or None
-    if they are missing or were taken on other kernel sources."""
+    if they are missing or were taken on another version of the kernel's source."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     try:
         d = json.load(open(path))
-        e = d.get(kernel_tag)
-        if not e or e.get("source_hash") != _source_hash():
+        e = d.get(workload, {}).get(kernel_tag)
+        if not e or e.get("source_hash") != source_hash(kernel_tag):
             return None
         return e["bytes_per_launch"]
     except Exception:
@@ -173,7 +182,7 @@ def main() -> int:
     has_noise = bool(np.any(sched.tables()["noise_std"] > 0))
     ub = update_bytes(wl, evals, has_noise)
     upd_rate = ub / (upd_ms * 1e-3) if upd_ms > 0 else 0.0
-    traffic = traffic_from_profiles("k_conv_f32" if dtype == "f32" else "k_conv_bf16")
+    traffic = traffic_from_profiles(wl.name, "k_conv_f32" if dtype == "f32" else "k_conv_bf16")
     out = {
         "metric": METRIC,
         "value": value,
@@ -202,7 +211,7 @@ def main() -> int:
                      "mean_launch_ms": den_ms / max(den_n, 1), "launches": den_n},
         "roofline_update": {"bound": "hbm", "achieved": upd_rate / 1e9, "peak": HBM_PEAK / 1e9,
                             "unit": "GB/s", "frac": upd_rate / HBM_PEAK,
-                            "traffic": traffic_from_profiles("k_picard_scan"),
+                            "traffic": traffic_from_profiles(wl.name, "k_picard_scan"),
                             "kernel": "k_picard_scan", "bytes_per_launch": ub / max(upd_n, 1),
                             "mean_launch_us": 1e3 * upd_ms / max(upd_n, 1), "launches": upd_n,
                             "finalize_mean_us": 1e3 * fin_ms / max(upd_n, 1)},
