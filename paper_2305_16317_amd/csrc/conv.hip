@@ -63,6 +63,20 @@ __device__ __forceinline__ float silu(float v) {
     return v * __builtin_amdgcn_rcpf(1.0f + __expf(-v));
 }
 
+// Shift and bias vectors of the activations, staged in LDS: rows 0..3 hold
+// each wave's first-layer shift (b1 + e_n, plus Wc c on the guided branch)
+// for the tile it is on, rows 4 and 5 the biases b2 and b3.  Read from LDS,
+// these values share the LDS counter with the weight fragments; read from
+// global memory through a generic pointer they were flat loads, and every
+// wait for a fragment also waited for them.
+template <int NB>
+struct ActVecs {
+    static constexpr int W = 32 * NB;
+    static constexpr int STRIDE = (W + 255) / 256 * 256;   // floats per row: whole 1 KB copies
+    static constexpr int ROWS = 6;
+    static constexpr int F4 = ROWS * STRIDE / 4;
+};
+
 // Blocks are persistent: each loops over groups of 4 tiles (one per wave),
 // and the next pass's first weight slab is copied during the current pass's
 // last layer, so a tile starts without waiting for weights.
@@ -85,7 +99,9 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
     constexpr int NBP = (NB + 1) / 2;                        // output-block pairs
     constexpr int SLOTS = 4 * NBP;                           // MFMA slots of a mid slab
     using SP = Spread<SLOTS, NB>;
+    using AV = ActVecs<NB>;
     __shared__ f4 lds[2][L::SLM / 4];
+    __shared__ f4 vec4[AV::F4];
 
     const int groups = src.active ? *src.active : src.max_groups;
     const int64_t ntiles = (int64_t)groups * src.group * tiles_per_row;
@@ -118,16 +134,29 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     };
-    // SiLU(acc + v) for block nb: the 4 features of register group q4 are contiguous
-    auto act = [&](const f16v& c, const float* v0, int nb) -> f16v {
-        // opaque per call: keeps these loads next to their use instead of
-        // hoisted out of the tile loop (they do not change between tiles)
-        const float* v = v0;
-        asm volatile("" : "+s"(v));
+    // first-layer shift of the next pass (tile row n, branch br) -> this wave's row
+    auto dma_shift = [&](int n, int br) {
+        const float* row = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * AV::W;
+        float* dst = reinterpret_cast<float*>(vec4) + wave * AV::STRIDE;
+        for (int c = 0; c < AV::STRIDE / 256; ++c) {
+            int off = c * 256 + lane * 4;
+            off = off <= AV::W - 4 ? off : AV::W - 4;      // lanes past the row re-read its end
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(row + off),
+                (__attribute__((address_space(3))) void*)(dst + c * 256), 16, 0, 0);
+        }
+    };
+    // SiLU(acc + v) for block nb, v = LDS vector row `vrow`: the 4 features of
+    // register group q4 are contiguous
+    auto act = [&](const f16v& c, int vrow, int nb) -> f16v {
+        // opaque per call: keeps these reads next to their use instead of
+        // hoisted out of the tile loop (the bias rows do not change)
+        int o = vrow * (AV::STRIDE / 4);
+        asm volatile("" : "+s"(o));
         f16v h;
         static_for<4>([&](auto q4c) {
             constexpr int q4 = decltype(q4c)::value;
-            const f4 sh = *reinterpret_cast<const f4*>(v + 32 * nb + 8 * q4 + 4 * half);
+            const f4 sh = vec4[o + 8 * nb + 2 * q4 + half];
             static_for<4>([&](auto qc) {
                 constexpr int q = decltype(qc)::value;
                 h[4 * q4 + q] = silu(c[4 * q4 + q] + sh[q]);
@@ -159,9 +188,14 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
     };
     const int nbranch = a.shift_c ? 2 : 1;
 
-    dma(0, 0);
-    land();
     Tile cur = locate(blockIdx.x);
+    dma(0, 0);
+    dma_shift(cur.n, 0);
+    for (int i = tid; i < AV::W; i += 256) {
+        reinterpret_cast<float*>(vec4)[4 * AV::STRIDE + i] = a.b2[i];
+        reinterpret_cast<float*>(vec4)[5 * AV::STRIDE + i] = a.b3[i];
+    }
+    land();
     float xin[L::KS1];
 #pragma unroll
     for (int s = 0; s < L::KS1; ++s) xin[s] = cur.pxok ? cur.x[(2 * s + half) * P + cur.px] : 0.f;
@@ -176,7 +210,6 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
 
         float eu[4] = {0.f, 0.f, 0.f, 0.f};
         for (int br = 0; br < nbranch; ++br) {
-            const float* shift = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)cur.n * a.width;
             f16v acc[NB], H[NB];
 
             // ---- layer 1 (slab 0, buffer 0): K = C
@@ -194,7 +227,7 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
             // ---- layers 2 and 3: one slab per input block
             static_for<2>([&](auto lc) {
                 constexpr int layer = decltype(lc)::value;
-                const float* vin = layer == 0 ? shift : a.b2;   // shift of the activation
+                const int vin = layer == 0 ? wave : 4;        // shift of the activation
                 H[0] = act(acc[0], vin, 0);
                 f16v nacc[NB];
                 static_for<NB>([&](auto nbc) { nacc[decltype(nbc)::value] = f16v{}; });
@@ -239,8 +272,12 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
                 constexpr int buf = slab & 1;
                 land();
                 const bool more = br + 1 < nbranch || !last_group;
-                if (more) dma(0, 0);                             // next pass's layer 1
-                H[0] = act(acc[0], a.b3, 0);
+                if (more) {                                      // next pass's layer 1
+                    dma(0, 0);
+                    if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
+                    else dma_shift(nxt.n, 0);
+                }
+                H[0] = act(acc[0], 5, 0);
                 f16v o4[4] = {f16v{}, f16v{}, f16v{}, f16v{}};
                 static_for<NB>([&](auto bc) {
                     constexpr int b = decltype(bc)::value;
@@ -253,7 +290,7 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
                                                                           o4[g4], 0, 0, 0);
                         });
                     });
-                    if constexpr (b + 1 < NB) H[b + 1] = act(acc[b + 1], a.b3, b + 1);
+                    if constexpr (b + 1 < NB) H[b + 1] = act(acc[b + 1], 5, b + 1);
                 });
                 const f16v o = (o4[0] + o4[1]) + (o4[2] + o4[3]);
                 float* out = eps + cur.row * (int64_t)C * P;
@@ -311,7 +348,9 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
     // one barrier); the packed layout keeps consecutive blocks contiguous
     constexpr int SB = (NB % 2 == 0) ? 2 : 1;
     constexpr int NSB = NB / SB;                             // slabs per mid layer
+    using AV = ActVecs<NB>;
     __shared__ bf8 lds[2][SB * L::SLM];
+    __shared__ f4 vec4[AV::F4];
 
     const int groups = src.active ? *src.active : src.max_groups;
     const int64_t ntiles = (int64_t)groups * src.group * tiles_per_row;
@@ -340,18 +379,28 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     };
-    // SiLU(acc + v) of block nb, rounded to bf16 and packed as two B operands
-    auto act = [&](const f16v& c, const float* v0, int nb, bf8 (&hb)[2]) {
-        const float* v = v0;
-        asm volatile("" : "+s"(v));
-        static_for<4>([&](auto q4c) {
-            constexpr int q4 = decltype(q4c)::value;
-            const f4 sh = *reinterpret_cast<const f4*>(v + 32 * nb + 8 * q4 + 4 * half);
-            static_for<4>([&](auto qc) {
-                constexpr int q = decltype(qc)::value;
-                hb[q4 / 2][4 * (q4 % 2) + q] = (__bf16)silu(c[4 * q4 + q] + sh[q]);
-            });
-        });
+    auto dma_shift = [&](int n, int br) {
+        const float* row = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * AV::W;
+        float* dst = reinterpret_cast<float*>(vec4) + wave * AV::STRIDE;
+        for (int c = 0; c < AV::STRIDE / 256; ++c) {
+            int off = c * 256 + lane * 4;
+            off = off <= AV::W - 4 ? off : AV::W - 4;
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(row + off),
+                (__attribute__((address_space(3))) void*)(dst + c * 256), 16, 0, 0);
+        }
+    };
+    // one quad (features 8 q4 + 4 half + 0..3) of SiLU(acc + v) of block nb,
+    // rounded to bf16 into its place in the two packed B operands
+    auto act_q = [&](const f16v& c, int vrow, int nb, int q4, bf8 (&hb)[2]) {
+        int o = vrow * (AV::STRIDE / 4);
+        asm volatile("" : "+s"(o));
+        const f4 sh = vec4[o + 8 * nb + 2 * q4 + half];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) hb[q4 / 2][4 * (q4 % 2) + q] = (__bf16)silu(c[4 * q4 + q] + sh[q]);
+    };
+    auto act = [&](const f16v& c, int vrow, int nb, bf8 (&hb)[2]) {
+        static_for<4>([&](auto q4c) { act_q(c, vrow, nb, decltype(q4c)::value, hb); });
     };
     struct Tile {
         int64_t row, px;
@@ -386,9 +435,14 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
     };
     const int nbranch = a.shift_c ? 2 : 1;
 
-    dma(0, 1, 0);
-    land();
     Tile cur = locate(blockIdx.x);
+    dma(0, 1, 0);
+    dma_shift(cur.n, 0);
+    for (int i = tid; i < AV::W; i += 256) {
+        reinterpret_cast<float*>(vec4)[4 * AV::STRIDE + i] = a.b2[i];
+        reinterpret_cast<float*>(vec4)[5 * AV::STRIDE + i] = a.b3[i];
+    }
+    land();
     bf8 xb = load_x(cur);
 
     for (int64_t tg = blockIdx.x; tg < ngroups; tg += gridDim.x) {
@@ -398,7 +452,6 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 
         float eu[4] = {0.f, 0.f, 0.f, 0.f};
         for (int br = 0; br < nbranch; ++br) {
-            const float* shift = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)cur.n * a.width;
             f16v acc[NB];
             bf8 H[NB][2];
 
@@ -414,7 +467,7 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
             // activated (its old accumulators stay live until then)
             static_for<2>([&](auto lc) {
                 constexpr int layer = decltype(lc)::value;
-                const float* vin = layer == 0 ? shift : a.b2;
+                const int vin = layer == 0 ? wave : 4;
                 act(acc[0], vin, 0, H[0]);
                 f16v nacc[NB];
                 static_for<NB>([&](auto nbc) { nacc[decltype(nbc)::value] = f16v{}; });
@@ -446,8 +499,13 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                             if constexpr (nb + 1 < NB)
                                 nacc[nb + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, H[b][g2],
                                                                                        nacc[nb + 1], 0, 0, 0);
-                            if constexpr (b + 1 < NB && slot == SLOTS / 2)   // just in time
-                                act(acc[b + 1], vin, b + 1, H[b + 1]);
+                            // next block's activation, its 4 quads spread evenly over the slots
+                            if constexpr (b + 1 < NB)
+                                static_for<4>([&](auto q4c) {
+                                    constexpr int q4 = decltype(q4c)::value;
+                                    if constexpr ((q4 * SLOTS) / 4 == slot)
+                                        act_q(acc[b + 1], vin, b + 1, q4, H[b + 1]);
+                                });
                             w0 = n0;
                             w1 = n1;
                         });
@@ -461,8 +519,12 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                 constexpr int buf = (2 * NSB + 1) & 1;
                 land();
                 const bool more = br + 1 < nbranch || !last_group;
-                if (more) dma(0, 1, buf ^ 1);                    // next pass's layer 1
-                act(acc[0], a.b3, 0, H[0]);
+                if (more) {                                      // next pass's layer 1
+                    dma(0, 1, buf ^ 1);
+                    if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
+                    else dma_shift(nxt.n, 0);
+                }
+                act(acc[0], 5, 0, H[0]);
                 f16v o2[2] = {f16v{}, f16v{}};
                 static_for<NB>([&](auto bc) {
                     constexpr int b = decltype(bc)::value;
@@ -471,7 +533,7 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                         o2[g2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[buf][(b * 2 + g2) * 64 + lane],
                                                                          H[b][g2], o2[g2], 0, 0, 0);
                     });
-                    if constexpr (b + 1 < NB) act(acc[b + 1], a.b3, b + 1, H[b + 1]);
+                    if constexpr (b + 1 < NB) act(acc[b + 1], 5, b + 1, H[b + 1]);
                 });
                 const f16v o = o2[0] + o2[1];
                 float* out = eps + cur.row * (int64_t)C * P;
