@@ -122,6 +122,70 @@ def cpu_baseline(wl, weights, budget_s: float):
                        f"(+{setup:.1f} s noise setup not counted)")}
 
 
+def sweep(a) -> int:
+    """Speed/quality trade-off of the stopping rule (Sec. 3.3 tolerance tau,
+    Prop. 2's eps: tau = 2 eps / T) or of the window size p, one JSON line per
+    setting: mean K and evaluations, median latency, the speed-up over the
+    sequential sampler, and the relative L2 distance of the Picard sample to
+    the sequential sample of the same noise seed."""
+    import numpy as np
+    import torch
+
+    import paper_2305_16317_amd as pd
+    import workloads as W
+
+    wl = W.WORKLOADS[a.workload]
+    weights = W.make_weights(wl.model)
+    sched, den = pd.from_workload(wl, weights, a.tol_offset)
+    shape = wl.model.sample_shape
+    n = wl.batch * wl.model.D
+    x = torch.empty(n, device="cuda")
+    T = wl.schedule.T
+    values = [float(v) for v in a.sweep_values.split(",")]
+    seeds = range(a.seeds)
+
+    ws_seq = pd.pd_workspace_create(sched, den, 1, wl.batch)
+    seq, seq_ms = {}, []
+    for s in seeds:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        pd.pd_sample_sequential(sched, den, s, wl.batch, shape, x, workspace=ws_seq)
+        torch.cuda.synchronize()
+        seq_ms.append(1e3 * (time.perf_counter() - t0))
+        seq[s] = x.double().cpu().numpy()
+    seq_med = float(np.median(seq_ms[1:] if len(seq_ms) > 1 else seq_ms))
+    for v in values:
+        if a.sweep == "window":
+            p, tau = int(v), wl.tau
+        elif a.sweep == "eps":
+            p, tau = wl.p, 2.0 * v / T
+        else:
+            p, tau = wl.p, v
+        ws = pd.pd_workspace_create(sched, den, min(p, T), wl.batch)
+        pd.pd_sample_picard(sched, den, p, tau, 0, wl.batch, shape, x, workspace=ws)   # warm-up
+        ks, evals, lat, dist = [], [], [], []
+        for s in seeds:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            st = pd.pd_sample_picard(sched, den, p, tau, s, wl.batch, shape, x, workspace=ws)
+            torch.cuda.synchronize()
+            lat.append(1e3 * (time.perf_counter() - t0))
+            ks.append(st.iters)
+            evals.append(st.evals_per_sample)
+            got = x.double().cpu().numpy()
+            dist.append(float(np.linalg.norm(got - seq[s]) / max(np.linalg.norm(seq[s]), 1e-300)))
+        med = float(np.median(lat))
+        print(json.dumps({"sweep": a.sweep, "workload": wl.name, "value": v, "p": p, "tau": tau,
+                          "tol_index_offset": a.tol_offset, "seeds": len(seeds),
+                          "K_mean": float(np.mean(ks)), "K_range": [min(ks), max(ks)],
+                          "evals_mean": float(np.mean(evals)), "latency_ms_median": med,
+                          "sequential_ms_median": seq_med, "speedup_vs_sequential": seq_med / med,
+                          "rel_l2_to_sequential_mean": float(np.mean(dist)),
+                          "rel_l2_to_sequential_max": float(np.max(dist))}), flush=True)
+        del ws
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -131,6 +195,13 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sequential", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--sweep", choices=["tau", "eps", "window"], default=None,
+                    help="instead of the benchmark line, one JSON line per setting of the "
+                         "tolerance tau, of Prop. 2's eps (tau = 2 eps / T) or of the window p")
+    ap.add_argument("--sweep-values", default="0.01,0.05,0.1,0.2,0.5,1.0")
+    ap.add_argument("--seeds", type=int, default=5, help="noise seeds per sweep setting")
+    ap.add_argument("--tol-offset", type=int, default=0, choices=[0, -1],
+                    help="sigma index of the tolerance: 0 = sigma_{t+j}, -1 = sigma_{t+j-1}")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after the run, copy this many bytes device-to-device 3 times "
                          "(a plain copy of known size, to scale rocprofv3 byte counters)")
@@ -139,6 +210,8 @@ def main() -> int:
         print(f"bench.py runs on one GPU only: --gpus {a.gpus} is not supported "
               "(the window is not split across GPUs in this build)", file=sys.stderr)
         return 2
+    if a.sweep:
+        return sweep(a)
 
     import numpy as np
     import torch

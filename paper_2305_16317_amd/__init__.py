@@ -307,12 +307,13 @@ def pd_sample_picard(sched: Schedule, den: Denoiser, p: int, tau: float, noise_s
 
 
 # ------------------------------------------------------------ workload helpers
-def from_workload(w, weights: Dict[str, np.ndarray]):
+def from_workload(w, weights: Dict[str, np.ndarray], tol_index_offset: int = 0):
     """(schedule, denoiser) handles for a ``workloads.Workload``.  The schedule
     carries the training chain (T_train, abar) that the denoiser needs."""
     s = w.schedule
     kind = PD_DDPM if s.kind == "ddpm" else PD_DDIM
-    sched = pd_init_schedule(kind, s.T_train, s.T, s.beta_start, s.beta_end, s.eta)
+    sched = pd_init_schedule(kind, s.T_train, s.T, s.beta_start, s.beta_end, s.eta,
+                             tol_index_offset)
     m = w.model
     mk = {"gmm2d": PD_MODEL_GMM2D, "mlp": PD_MODEL_MLP, "conv1x1": PD_MODEL_CONV1X1}[m.kind]
     den = pd_denoiser_create(mk, m.sample_shape, weights, sched, width=m.width,
