@@ -317,39 +317,54 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
 }
 
 // ---------------------------------------------------------------- bf16
-// Same design on v_mfma_f32_32x32x16_bf16: A[i][k] holds k = 8 (l/32) + u
-// (u = 0..7) in lane i + 32 (l/32) as 8 packed bf16, B[k][j] likewise in lane
-// j + 32 (k/8), D as for the fp32 instruction.  Accumulator registers
-// 8 g2 .. 8 g2 + 7 of block b, rounded to bf16 and packed, are the B operand
-// of k-step (b, g2): lane half h then carries input features
+// Same transposed design on v_mfma_f32_32x32x16_bf16: A[i][k] holds
+// k = 8 (l/32) + u (u = 0..7) in lane i + 32 (l/32) as 8 packed bf16, B[k][j]
+// likewise in lane j + 32 (k/8), D as for the fp32 instruction.  Accumulator
+// registers 8 g2 .. 8 g2 + 7 of block b, rounded to bf16 and packed, are the
+// B operand of k-step (b, g2): lane half h then carries input features
 // 32 b + 16 g2 + 8 (u/4) + 4 h + u%4, and the packed weights use the same
 // order.  Layer 1 pads K = C to 16 with zeros, layer 4 pads its C output rows
 // to 32.  Every matmul operand is bf16 (round to nearest even); accumulation,
 // bias, shift, SiLU and the guidance combination stay in fp32.
+//
+// A 32x32x16 bf16 MFMA and the SiLU of one accumulator register cost about
+// the same issue time, so the kernel runs two waves per SIMD (two blocks per
+// CU, each wave at most 256 registers) and lets the hardware overlap one
+// wave's activations with the other's MFMAs.  To fit, each layer is computed
+// in two halves of its output blocks: the accumulators of one half (HB
+// blocks) are live at a time, and a half is activated into the next layer's
+// operands as soon as its reduction ends.
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 
 template <int NB, int C>
 struct ConvLayoutBf16 {                          // units of 16 B (one lane's A operand)
-    static constexpr int SL1 = NB * 64;          // layer 1: one k-step per output block
-    static constexpr int SLM = 2 * NB * 64;      // layers 2, 3 per input block; layer 4 (all)
-    static constexpr int TOTAL = SL1 + (2 * NB + 1) * SLM;
-    static constexpr __host__ __device__ int off(int i) { return i == 0 ? 0 : SL1 + (i - 1) * SLM; }
-    static constexpr __host__ __device__ int size(int i) { return i == 0 ? SL1 : SLM; }
+    static constexpr int HB = NB % 2 == 0 ? NB / 2 : NB;   // output blocks per half
+    static constexpr int NH = NB / HB;                      // halves per layer
+    static constexpr int SB = NB % 2 == 0 ? 2 : 1;          // input blocks per mid slab
+    static constexpr int NG = NB / SB;                      // mid slabs per half
+    static constexpr int NMS = NH * NG;                     // mid slabs per layer
+    static constexpr int SL1 = NB * 64;                     // layer 1: one k-step per output block
+    static constexpr int SLM = SB * 2 * HB * 64;            // (input block, g2, output block of the half)
+    static constexpr int SL4 = 2 * NB * 64;                 // layer 4: (input block, g2)
+    static constexpr int BUF = SL1 > SLM ? (SL1 > SL4 ? SL1 : SL4) : (SLM > SL4 ? SLM : SL4);
+    static constexpr int TOTAL = SL1 + 2 * NMS * SLM + SL4;
+    // slab 0: layer 1; 1 + layer * NMS + half * NG + g: mid layers; 1 + 2 NMS: layer 4
+    static constexpr __host__ __device__ int off(int i) {
+        return i == 0 ? 0 : SL1 + (i - 1) * SLM;
+    }
+    static constexpr __host__ __device__ int size(int i) {
+        return i == 0 ? SL1 : (i <= 2 * NMS ? SLM : SL4);
+    }
 };
 
 template <int NB, int C>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
     using L = ConvLayoutBf16<NB, C>;
-    static_assert(C <= 8, "layer 1 holds at most 8 channels in one lane half");
-    constexpr int NBP = (NB + 1) / 2;                        // output-block pairs
-    constexpr int SLOTS = 2 * NBP;                           // MFMA-pair slots per input block
-    // a bf16 input block is only 2 NB MFMAs, so SB blocks share one slab (and
-    // one barrier); the packed layout keeps consecutive blocks contiguous
-    constexpr int SB = (NB % 2 == 0) ? 2 : 1;
-    constexpr int NSB = NB / SB;                             // slabs per mid layer
     using AV = ActVecs<NB>;
-    __shared__ bf8 lds[2][SB * L::SLM];
+    static_assert(C <= 8, "layer 1 holds at most 8 channels in one lane half");
+    constexpr int HB = L::HB, NH = L::NH, SB = L::SB, NG = L::NG, NMS = L::NMS;
+    __shared__ bf8 lds[2][L::BUF];
     __shared__ f4 vec4[AV::F4];
 
     const int groups = src.active ? *src.active : src.max_groups;
@@ -361,9 +376,9 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t P = a.P;
 
-    // packed slabs [i, i + n) -> LDS buffer `buf` (they are contiguous)
-    auto dma = [&](int i, int n, int buf) {
-        const int nch = (L::off(i + n - 1) + L::size(i + n - 1) - L::off(i)) / 64;   // 1 KB chunks
+    // packed slab i -> LDS buffer `buf`, 1 KB per wave instruction
+    auto dma = [&](int i, int buf) {
+        const int nch = L::size(i) / 64;
         const char* gb = reinterpret_cast<const char*>(a.frags);
         uint32_t lo = (uint32_t)lane * 16u;
         asm volatile("" : "+s"(gb), "+v"(lo));
@@ -390,17 +405,21 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                 (__attribute__((address_space(3))) void*)(dst + c * 256), 16, 0, 0);
         }
     };
-    // one quad (features 8 q4 + 4 half + 0..3) of SiLU(acc + v) of block nb,
-    // rounded to bf16 into its place in the two packed B operands
-    auto act_q = [&](const f16v& c, int vrow, int nb, int q4, bf8 (&hb)[2]) {
+    // SiLU(acc + v) of block nb (v = LDS vector row vrow), rounded to bf16 and
+    // packed as the block's two B operands
+    auto act = [&](const f16v& c, int vrow, int nb, bf8 (&hb)[2]) {
         int o = vrow * (AV::STRIDE / 4);
         asm volatile("" : "+s"(o));
-        const f4 sh = vec4[o + 8 * nb + 2 * q4 + half];
+        static_for<4>([&](auto q4c) {
+            constexpr int q4 = decltype(q4c)::value;
+            const f4 sh = vec4[o + 8 * nb + 2 * q4 + half];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) hb[q4 / 2][4 * (q4 % 2) + q] = (__bf16)silu(c[4 * q4 + q] + sh[q]);
-    };
-    auto act = [&](const f16v& c, int vrow, int nb, bf8 (&hb)[2]) {
-        static_for<4>([&](auto q4c) { act_q(c, vrow, nb, decltype(q4c)::value, hb); });
+            for (int q = 0; q < 4; ++q) hb[q4 / 2][4 * (q4 % 2) + q] = (__bf16)silu(c[4 * q4 + q] + sh[q]);
+        });
+        // pinned here: left to itself the compiler sinks the activation to the
+        // slab that first reads it, keeping 16 fp32 accumulators live in place
+        // of 8 packed registers, and spills
+        asm volatile("" : "+v"(hb[0]), "+v"(hb[1]));
     };
     struct Tile {
         int64_t row, px;
@@ -436,7 +455,7 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
     const int nbranch = a.shift_c ? 2 : 1;
 
     Tile cur = locate(blockIdx.x);
-    dma(0, 1, 0);
+    dma(0, 0);
     dma_shift(cur.n, 0);
     for (int i = tid; i < AV::W; i += 256) {
         reinterpret_cast<float*>(vec4)[4 * AV::STRIDE + i] = a.b2[i];
@@ -452,79 +471,80 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 
         float eu[4] = {0.f, 0.f, 0.f, 0.f};
         for (int br = 0; br < nbranch; ++br) {
-            f16v acc[NB];
             bf8 H[NB][2];
 
-            // ---- layer 1 (slab 0, buffer 0): K = C padded to 16
-            dma(1, SB, 1);
-            static_for<NB>([&](auto nbc) {
-                constexpr int nb = decltype(nbc)::value;
-                acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[0][nb * 64 + lane], xb, f16v{},
-                                                                  0, 0, 0);
+            // ---- layer 1 (slab 0, buffer 0): K = C padded to 16, activated
+            // with this wave's shift (LDS row `wave`)
+            dma(1, 1);
+            static_for<NH>([&](auto hc) {
+                constexpr int h = decltype(hc)::value;
+                f16v acc[HB];
+                static_for<HB>([&](auto jc) {
+                    constexpr int j = decltype(jc)::value;
+                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[0][(h * HB + j) * 64 + lane], xb,
+                                                                     f16v{}, 0, 0, 0);
+                });
+                static_for<HB>([&](auto jc) {
+                    constexpr int j = decltype(jc)::value;
+                    act(acc[j], wave, h * HB + j, H[h * HB + j]);
+                });
             });
 
-            // ---- layers 2 and 3: block b's MFMAs run while block b+1 is
-            // activated (its old accumulators stay live until then)
+            // ---- layers 2 and 3, output half by output half
             static_for<2>([&](auto lc) {
                 constexpr int layer = decltype(lc)::value;
-                const int vin = layer == 0 ? wave : 4;
-                act(acc[0], vin, 0, H[0]);
-                f16v nacc[NB];
-                static_for<NB>([&](auto nbc) { nacc[decltype(nbc)::value] = f16v{}; });
-                static_for<NSB>([&](auto sc) {
-                    constexpr int sb = decltype(sc)::value;
-                    constexpr int gslab = layer * NSB + sb;          // mid slab counter
-                    constexpr int buf = (gslab + 1) & 1;
-                    land();                                          // this slab has landed
-                    if constexpr (gslab + 1 < 2 * NSB)
-                        dma(1 + (gslab + 1) * SB, SB, buf ^ 1);
-                    else
-                        dma(1 + 2 * NB, 1, buf ^ 1);                 // layer 4
-                    static_for<SB>([&](auto ic) {
-                        constexpr int b = sb * SB + decltype(ic)::value;
-                        constexpr int base = decltype(ic)::value * L::SLM;
-                        bf8 w0 = lds[buf][base + (0 * NB + 0) * 64 + lane];
-                        bf8 w1 = NB > 1 ? lds[buf][base + (0 * NB + 1) * 64 + lane] : bf8{};
-                        static_for<SLOTS>([&](auto tc) {
-                            constexpr int slot = decltype(tc)::value;
-                            constexpr int g2 = slot / NBP, nb = 2 * (slot % NBP);
-                            constexpr int ns = slot + 1;
-                            constexpr int ng2 = ns / NBP, nnb = 2 * (ns % NBP);
-                            bf8 n0 = bf8{}, n1 = bf8{};
-                            if constexpr (ns < SLOTS) {
-                                n0 = lds[buf][base + (ng2 * NB + nnb) * 64 + lane];
-                                if constexpr (nnb + 1 < NB) n1 = lds[buf][base + (ng2 * NB + nnb + 1) * 64 + lane];
-                            }
-                            nacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, H[b][g2], nacc[nb], 0, 0, 0);
-                            if constexpr (nb + 1 < NB)
-                                nacc[nb + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, H[b][g2],
-                                                                                       nacc[nb + 1], 0, 0, 0);
-                            // next block's activation, its 4 quads spread evenly over the slots
-                            if constexpr (b + 1 < NB)
-                                static_for<4>([&](auto q4c) {
-                                    constexpr int q4 = decltype(q4c)::value;
-                                    if constexpr ((q4 * SLOTS) / 4 == slot)
-                                        act_q(acc[b + 1], vin, b + 1, q4, H[b + 1]);
+                bf8 Hn[NB][2];
+                static_for<NH>([&](auto hc) {
+                    constexpr int h = decltype(hc)::value;
+                    f16v acc[HB];
+                    static_for<HB>([&](auto jc) { acc[decltype(jc)::value] = f16v{}; });
+                    static_for<NG>([&](auto gc) {
+                        constexpr int g = decltype(gc)::value;
+                        constexpr int slab = 1 + layer * NMS + h * NG + g;
+                        constexpr int buf = slab & 1;
+                        land();                                      // this slab has landed
+                        dma(slab + 1, buf ^ 1);                      // the next mid slab or layer 4
+                        static_for<SB>([&](auto ic) {
+                            constexpr int i = decltype(ic)::value;
+                            constexpr int b = g * SB + i;
+                            static_for<2>([&](auto g2c) {
+                                constexpr int g2 = decltype(g2c)::value;
+                                static_for<HB>([&](auto jc) {
+                                    constexpr int j = decltype(jc)::value;
+                                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                        lds[buf][((i * 2 + g2) * HB + j) * 64 + lane], H[b][g2], acc[j],
+                                        0, 0, 0);
                                 });
-                            w0 = n0;
-                            w1 = n1;
+                                // keep each step's fragment reads next to its MFMAs: hoisted
+                                // reads overflow the 256 registers of a two-wave SIMD, and the
+                                // other wave hides their latency
+                                __builtin_amdgcn_sched_barrier(0);
+                            });
                         });
                     });
+                    static_for<HB>([&](auto jc) {
+                        constexpr int j = decltype(jc)::value;
+                        act(acc[j], 4 + layer, h * HB + j, Hn[h * HB + j]);   // b2 or b3
+                    });
                 });
-                static_for<NB>([&](auto nbc) { acc[decltype(nbc)::value] = nacc[decltype(nbc)::value]; });
+                static_for<NB>([&](auto bc) {
+                    constexpr int b = decltype(bc)::value;
+                    H[b][0] = Hn[b][0];
+                    H[b][1] = Hn[b][1];
+                });
             });
 
-            // ---- layer 4 (slab 2NB+1, buffer 1)
+            // ---- layer 4 (slab 1 + 2 NMS, buffer 1)
             {
-                constexpr int buf = (2 * NSB + 1) & 1;
+                constexpr int slab = 1 + 2 * NMS;
+                constexpr int buf = slab & 1;
                 land();
                 const bool more = br + 1 < nbranch || !last_group;
                 if (more) {                                      // next pass's layer 1
-                    dma(0, 1, buf ^ 1);
+                    dma(0, buf ^ 1);
                     if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
                     else dma_shift(nxt.n, 0);
                 }
-                act(acc[0], 5, 0, H[0]);
                 f16v o2[2] = {f16v{}, f16v{}};
                 static_for<NB>([&](auto bc) {
                     constexpr int b = decltype(bc)::value;
@@ -533,7 +553,6 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                         o2[g2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[buf][(b * 2 + g2) * 64 + lane],
                                                                          H[b][g2], o2[g2], 0, 0, 0);
                     });
-                    if constexpr (b + 1 < NB) act(acc[b + 1], 5, b + 1, H[b + 1]);
                 });
                 const f16v o = o2[0] + o2[1];
                 float* out = eps + cur.row * (int64_t)C * P;
@@ -584,19 +603,24 @@ void pack_bf16_t(const float* W1, const float* W2, const float* W3, const float*
     auto fin = [](int b, int g2, int l, int u) { return 32 * b + 16 * g2 + 8 * (u / 4) + 4 * (l / 32) + u % 4; };
     for (int layer = 0; layer < 2; ++layer) {
         const float* Wm = layer == 0 ? W2 : W3;
-        for (int b = 0; b < NB; ++b)
-            for (int g2 = 0; g2 < 2; ++g2)
-                for (int nb = 0; nb < NB; ++nb)
-                    for (int l = 0; l < 64; ++l)
-                        for (int u = 0; u < 8; ++u)
-                            unit(L::off(1 + layer * NB + b) + (g2 * NB + nb) * 64 + l)[u] =
-                                to_bf16(Wm[(32 * nb + l % 32) * W + fin(b, g2, l, u)]);
+        for (int h = 0; h < L::NH; ++h)
+            for (int g = 0; g < L::NG; ++g)
+                for (int i = 0; i < L::SB; ++i)
+                    for (int g2 = 0; g2 < 2; ++g2)
+                        for (int j = 0; j < L::HB; ++j) {
+                            const int b = g * L::SB + i, nb = h * L::HB + j;
+                            const int base = L::off(1 + layer * L::NMS + h * L::NG + g) +
+                                             ((i * 2 + g2) * L::HB + j) * 64;
+                            for (int l = 0; l < 64; ++l)
+                                for (int u = 0; u < 8; ++u)
+                                    unit(base + l)[u] = to_bf16(Wm[(32 * nb + l % 32) * W + fin(b, g2, l, u)]);
+                        }
     }
     for (int b = 0; b < NB; ++b)
         for (int g2 = 0; g2 < 2; ++g2)
             for (int l = 0; l < 64; ++l)
                 for (int u = 0; u < 8; ++u)
-                    unit(L::off(1 + 2 * NB) + (b * 2 + g2) * 64 + l)[u] =
+                    unit(L::off(1 + 2 * L::NMS) + (b * 2 + g2) * 64 + l)[u] =
                         (l % 32 < C) ? to_bf16(W4[(l % 32) * W + fin(b, g2, l, u)]) : (uint16_t)0;
 }
 
@@ -607,8 +631,8 @@ void launch_bf16_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t
     const int tiles_per_row = (int)((a.P + 31) / 32);
     const int64_t ntiles = (int64_t)src.max_groups * src.group * tiles_per_row;
     if (ntiles == 0) return;
-    int64_t blocks = (ntiles + 3) / 4;                       // persistent: one block per CU
-    if (blocks > device_cus()) blocks = device_cus();
+    int64_t blocks = (ntiles + 3) / 4;                       // persistent: two blocks per CU
+    if (blocks > 2 * device_cus()) blocks = 2 * device_cus();
     hipLaunchKernelGGL((k_conv_bf16<NB, C>), dim3((unsigned)blocks), dim3(256), 0, s, a, src, eps,
                        tiles_per_row);
     PD_HIP(hipGetLastError());
