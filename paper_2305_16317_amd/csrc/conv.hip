@@ -63,17 +63,18 @@ __device__ __forceinline__ float silu(float v) {
     return v * __builtin_amdgcn_rcpf(1.0f + __expf(-v));
 }
 
-// Shift and bias vectors of the activations, staged in LDS: rows 0..3 hold
+// Shift and bias vectors of the activations, staged in LDS: rows 0..NW-1 hold
 // each wave's first-layer shift (b1 + e_n, plus Wc c on the guided branch)
-// for the tile it is on, rows 4 and 5 the biases b2 and b3.  Read from LDS,
+// for the tile it is on, rows NW and NW+1 the biases b2 and b3.  Read from LDS,
 // these values share the LDS counter with the weight fragments; read from
 // global memory through a generic pointer they were flat loads, and every
 // wait for a fragment also waited for them.
-template <int NB>
+template <int NB, int NW>
 struct ActVecs {
     static constexpr int W = 32 * NB;
     static constexpr int STRIDE = (W + 255) / 256 * 256;   // floats per row: whole 1 KB copies
-    static constexpr int ROWS = 6;
+    static constexpr int B2 = NW, B3 = NW + 1;              // bias rows
+    static constexpr int ROWS = NW + 2;
     static constexpr int F4 = ROWS * STRIDE / 4;
 };
 
@@ -99,7 +100,7 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
     constexpr int NBP = (NB + 1) / 2;                        // output-block pairs
     constexpr int SLOTS = 4 * NBP;                           // MFMA slots of a mid slab
     using SP = Spread<SLOTS, NB>;
-    using AV = ActVecs<NB>;
+    using AV = ActVecs<NB, 4>;
     __shared__ f4 lds[2][L::SLM / 4];
     __shared__ f4 vec4[AV::F4];
 
@@ -192,8 +193,8 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
     dma(0, 0);
     dma_shift(cur.n, 0);
     for (int i = tid; i < AV::W; i += 256) {
-        reinterpret_cast<float*>(vec4)[4 * AV::STRIDE + i] = a.b2[i];
-        reinterpret_cast<float*>(vec4)[5 * AV::STRIDE + i] = a.b3[i];
+        reinterpret_cast<float*>(vec4)[AV::B2 * AV::STRIDE + i] = a.b2[i];
+        reinterpret_cast<float*>(vec4)[AV::B3 * AV::STRIDE + i] = a.b3[i];
     }
     land();
     float xin[L::KS1];
@@ -227,7 +228,7 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
             // ---- layers 2 and 3: one slab per input block
             static_for<2>([&](auto lc) {
                 constexpr int layer = decltype(lc)::value;
-                const int vin = layer == 0 ? wave : 4;        // shift of the activation
+                const int vin = layer == 0 ? wave : AV::B2;   // shift of the activation
                 H[0] = act(acc[0], vin, 0);
                 f16v nacc[NB];
                 static_for<NB>([&](auto nbc) { nacc[decltype(nbc)::value] = f16v{}; });
@@ -277,7 +278,7 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
                     if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
                     else dma_shift(nxt.n, 0);
                 }
-                H[0] = act(acc[0], 5, 0);
+                H[0] = act(acc[0], AV::B3, 0);
                 f16v o4[4] = {f16v{}, f16v{}, f16v{}, f16v{}};
                 static_for<NB>([&](auto bc) {
                     constexpr int b = decltype(bc)::value;
@@ -290,7 +291,7 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
                                                                           o4[g4], 0, 0, 0);
                         });
                     });
-                    if constexpr (b + 1 < NB) H[b + 1] = act(acc[b + 1], 5, b + 1);
+                    if constexpr (b + 1 < NB) H[b + 1] = act(acc[b + 1], AV::B3, b + 1);
                 });
                 const f16v o = (o4[0] + o4[1]) + (o4[2] + o4[3]);
                 float* out = eps + cur.row * (int64_t)C * P;
@@ -328,48 +329,43 @@ void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_r
 // bias, shift, SiLU and the guidance combination stay in fp32.
 //
 // A 32x32x16 bf16 MFMA and the SiLU of one accumulator register cost about
-// the same issue time, so the kernel runs two waves per SIMD (two blocks per
-// CU, each wave at most 256 registers) and lets the hardware overlap one
-// wave's activations with the other's MFMAs.  To fit, each layer is computed
-// in two halves of its output blocks: the accumulators of one half (HB
-// blocks) are live at a time, and a half is activated into the next layer's
-// operands as soon as its reduction ends.
+// the same issue time, so the work is arranged for the hardware to overlap
+// them across waves: two blocks of 4 waves run per CU (two waves per SIMD, at
+// most 256 registers each, one tile of 32 pixels per wave).  Each mid layer
+// is streamed one output block at a time -- a slab holds that block's weights
+// for every input -- and a wave activates the block as soon as its MFMAs end,
+// so its SiLU work runs while the other block's wave on the SIMD is in its
+// MFMAs.  Only one output block's accumulators are live at a time.
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+
+constexpr int kBf16Waves = 4;
 
 template <int NB, int C>
 struct ConvLayoutBf16 {                          // units of 16 B (one lane's A operand)
-    static constexpr int HB = NB % 2 == 0 ? NB / 2 : NB;   // output blocks per half
-    static constexpr int NH = NB / HB;                      // halves per layer
-    static constexpr int SB = NB % 2 == 0 ? 2 : 1;          // input blocks per mid slab
-    static constexpr int NG = NB / SB;                      // mid slabs per half
-    static constexpr int NMS = NH * NG;                     // mid slabs per layer
-    static constexpr int SL1 = NB * 64;                     // layer 1: one k-step per output block
-    static constexpr int SLM = SB * 2 * HB * 64;            // (input block, g2, output block of the half)
-    static constexpr int SL4 = 2 * NB * 64;                 // layer 4: (input block, g2)
-    static constexpr int BUF = SL1 > SLM ? (SL1 > SL4 ? SL1 : SL4) : (SLM > SL4 ? SLM : SL4);
-    static constexpr int TOTAL = SL1 + 2 * NMS * SLM + SL4;
-    // slab 0: layer 1; 1 + layer * NMS + half * NG + g: mid layers; 1 + 2 NMS: layer 4
-    static constexpr __host__ __device__ int off(int i) {
-        return i == 0 ? 0 : SL1 + (i - 1) * SLM;
-    }
-    static constexpr __host__ __device__ int size(int i) {
-        return i == 0 ? SL1 : (i <= 2 * NMS ? SLM : SL4);
-    }
+    static constexpr int SL1 = NB * 64;          // layer 1: one k-step per output block
+    static constexpr int SLM = 2 * NB * 64;      // one output block, every (input block, g2);
+                                                 // layer 4 likewise (its C rows padded to 32)
+    static constexpr int BUF = SL1 > SLM ? SL1 : SLM;
+    static constexpr int TOTAL = SL1 + (2 * NB + 1) * SLM;
+    // slab 0: layer 1; 1 + layer * NB + j: output block j of layer 2 or 3;
+    // 1 + 2 NB: layer 4
+    static constexpr __host__ __device__ int off(int i) { return i == 0 ? 0 : SL1 + (i - 1) * SLM; }
+    static constexpr __host__ __device__ int size(int i) { return i == 0 ? SL1 : SLM; }
 };
 
 template <int NB, int C>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(kBf16Waves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
     using L = ConvLayoutBf16<NB, C>;
-    using AV = ActVecs<NB>;
+    constexpr int NW = kBf16Waves;
+    using AV = ActVecs<NB, NW>;
     static_assert(C <= 8, "layer 1 holds at most 8 channels in one lane half");
-    constexpr int HB = L::HB, NH = L::NH, SB = L::SB, NG = L::NG, NMS = L::NMS;
     __shared__ bf8 lds[2][L::BUF];
     __shared__ f4 vec4[AV::F4];
 
     const int groups = src.active ? *src.active : src.max_groups;
     const int64_t ntiles = (int64_t)groups * src.group * tiles_per_row;
-    const int64_t ngroups = (ntiles + 3) / 4;
+    const int64_t ngroups = (ntiles + NW - 1) / NW;
     if ((int64_t)blockIdx.x >= ngroups) return;              // uniform over the block
 
     const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
@@ -383,7 +379,7 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
         uint32_t lo = (uint32_t)lane * 16u;
         asm volatile("" : "+s"(gb), "+v"(lo));
         bf8* ls = lds[buf];
-        for (int c = wave; c < nch; c += 4) {
+        for (int c = wave; c < nch; c += NW) {
             const uint32_t ob = (uint32_t)(L::off(i) + c * 64) * 16u + lo;
             __builtin_amdgcn_global_load_lds(
                 (const __attribute__((address_space(1))) void*)(gb + (size_t)ob),
@@ -429,7 +425,7 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
     };
     auto locate = [&](int64_t tg) -> Tile {
         Tile T;
-        const int64_t tile = tg * 4 + wave;
+        const int64_t tile = tg * NW + wave;
         T.active = tile < ntiles;
         const int64_t tt = T.active ? tile : ntiles - 1;
         T.row = tt / tiles_per_row;
@@ -457,9 +453,9 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
     Tile cur = locate(blockIdx.x);
     dma(0, 0);
     dma_shift(cur.n, 0);
-    for (int i = tid; i < AV::W; i += 256) {
-        reinterpret_cast<float*>(vec4)[4 * AV::STRIDE + i] = a.b2[i];
-        reinterpret_cast<float*>(vec4)[5 * AV::STRIDE + i] = a.b3[i];
+    for (int i = tid; i < AV::W; i += NW * 64) {
+        reinterpret_cast<float*>(vec4)[AV::B2 * AV::STRIDE + i] = a.b2[i];
+        reinterpret_cast<float*>(vec4)[AV::B3 * AV::STRIDE + i] = a.b3[i];
     }
     land();
     bf8 xb = load_x(cur);
@@ -476,56 +472,33 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
             // ---- layer 1 (slab 0, buffer 0): K = C padded to 16, activated
             // with this wave's shift (LDS row `wave`)
             dma(1, 1);
-            static_for<NH>([&](auto hc) {
-                constexpr int h = decltype(hc)::value;
-                f16v acc[HB];
-                static_for<HB>([&](auto jc) {
-                    constexpr int j = decltype(jc)::value;
-                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[0][(h * HB + j) * 64 + lane], xb,
-                                                                     f16v{}, 0, 0, 0);
-                });
-                static_for<HB>([&](auto jc) {
-                    constexpr int j = decltype(jc)::value;
-                    act(acc[j], wave, h * HB + j, H[h * HB + j]);
-                });
+            static_for<NB>([&](auto jc) {
+                constexpr int j = decltype(jc)::value;
+                const f16v acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[0][j * 64 + lane], xb, f16v{},
+                                                                         0, 0, 0);
+                act(acc, wave, j, H[j]);
             });
 
-            // ---- layers 2 and 3, output half by output half
+            // ---- layers 2 and 3: one slab (and one activation) per output block
             static_for<2>([&](auto lc) {
                 constexpr int layer = decltype(lc)::value;
                 bf8 Hn[NB][2];
-                static_for<NH>([&](auto hc) {
-                    constexpr int h = decltype(hc)::value;
-                    f16v acc[HB];
-                    static_for<HB>([&](auto jc) { acc[decltype(jc)::value] = f16v{}; });
-                    static_for<NG>([&](auto gc) {
-                        constexpr int g = decltype(gc)::value;
-                        constexpr int slab = 1 + layer * NMS + h * NG + g;
-                        constexpr int buf = slab & 1;
-                        land();                                      // this slab has landed
-                        dma(slab + 1, buf ^ 1);                      // the next mid slab or layer 4
-                        static_for<SB>([&](auto ic) {
-                            constexpr int i = decltype(ic)::value;
-                            constexpr int b = g * SB + i;
-                            static_for<2>([&](auto g2c) {
-                                constexpr int g2 = decltype(g2c)::value;
-                                static_for<HB>([&](auto jc) {
-                                    constexpr int j = decltype(jc)::value;
-                                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                                        lds[buf][((i * 2 + g2) * HB + j) * 64 + lane], H[b][g2], acc[j],
-                                        0, 0, 0);
-                                });
-                                // keep each step's fragment reads next to its MFMAs: hoisted
-                                // reads overflow the 256 registers of a two-wave SIMD, and the
-                                // other wave hides their latency
-                                __builtin_amdgcn_sched_barrier(0);
-                            });
+                static_for<NB>([&](auto jc) {
+                    constexpr int j = decltype(jc)::value;
+                    constexpr int slab = 1 + layer * NB + j;
+                    constexpr int buf = slab & 1;
+                    land();                                      // this slab has landed
+                    dma(slab + 1, buf ^ 1);                      // the next block or layer 4
+                    f16v acc = f16v{};
+                    static_for<NB>([&](auto bc) {
+                        constexpr int b = decltype(bc)::value;
+                        static_for<2>([&](auto g2c) {
+                            constexpr int g2 = decltype(g2c)::value;
+                            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[buf][(b * 2 + g2) * 64 + lane],
+                                                                          H[b][g2], acc, 0, 0, 0);
                         });
                     });
-                    static_for<HB>([&](auto jc) {
-                        constexpr int j = decltype(jc)::value;
-                        act(acc[j], 4 + layer, h * HB + j, Hn[h * HB + j]);   // b2 or b3
-                    });
+                    act(acc, layer == 0 ? AV::B2 : AV::B3, j, Hn[j]);
                 });
                 static_for<NB>([&](auto bc) {
                     constexpr int b = decltype(bc)::value;
@@ -534,9 +507,9 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                 });
             });
 
-            // ---- layer 4 (slab 1 + 2 NMS, buffer 1)
+            // ---- layer 4 (slab 1 + 2 NB, buffer 1)
             {
-                constexpr int slab = 1 + 2 * NMS;
+                constexpr int slab = 1 + 2 * NB;
                 constexpr int buf = slab & 1;
                 land();
                 const bool more = br + 1 < nbranch || !last_group;
@@ -603,24 +576,19 @@ void pack_bf16_t(const float* W1, const float* W2, const float* W3, const float*
     auto fin = [](int b, int g2, int l, int u) { return 32 * b + 16 * g2 + 8 * (u / 4) + 4 * (l / 32) + u % 4; };
     for (int layer = 0; layer < 2; ++layer) {
         const float* Wm = layer == 0 ? W2 : W3;
-        for (int h = 0; h < L::NH; ++h)
-            for (int g = 0; g < L::NG; ++g)
-                for (int i = 0; i < L::SB; ++i)
-                    for (int g2 = 0; g2 < 2; ++g2)
-                        for (int j = 0; j < L::HB; ++j) {
-                            const int b = g * L::SB + i, nb = h * L::HB + j;
-                            const int base = L::off(1 + layer * L::NMS + h * L::NG + g) +
-                                             ((i * 2 + g2) * L::HB + j) * 64;
-                            for (int l = 0; l < 64; ++l)
-                                for (int u = 0; u < 8; ++u)
-                                    unit(base + l)[u] = to_bf16(Wm[(32 * nb + l % 32) * W + fin(b, g2, l, u)]);
-                        }
+        for (int j = 0; j < NB; ++j)
+            for (int b = 0; b < NB; ++b)
+                for (int g2 = 0; g2 < 2; ++g2)
+                    for (int l = 0; l < 64; ++l)
+                        for (int u = 0; u < 8; ++u)
+                            unit(L::off(1 + layer * NB + j) + (b * 2 + g2) * 64 + l)[u] =
+                                to_bf16(Wm[(32 * j + l % 32) * W + fin(b, g2, l, u)]);
     }
     for (int b = 0; b < NB; ++b)
         for (int g2 = 0; g2 < 2; ++g2)
             for (int l = 0; l < 64; ++l)
                 for (int u = 0; u < 8; ++u)
-                    unit(L::off(1 + 2 * L::NMS) + (b * 2 + g2) * 64 + l)[u] =
+                    unit(L::off(1 + 2 * NB) + (b * 2 + g2) * 64 + l)[u] =
                         (l % 32 < C) ? to_bf16(W4[(l % 32) * W + fin(b, g2, l, u)]) : (uint16_t)0;
 }
 
@@ -631,10 +599,10 @@ void launch_bf16_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t
     const int tiles_per_row = (int)((a.P + 31) / 32);
     const int64_t ntiles = (int64_t)src.max_groups * src.group * tiles_per_row;
     if (ntiles == 0) return;
-    int64_t blocks = (ntiles + 3) / 4;                       // persistent: two blocks per CU
+    int64_t blocks = (ntiles + kBf16Waves - 1) / kBf16Waves;   // persistent: two blocks per CU
     if (blocks > 2 * device_cus()) blocks = 2 * device_cus();
-    hipLaunchKernelGGL((k_conv_bf16<NB, C>), dim3((unsigned)blocks), dim3(256), 0, s, a, src, eps,
-                       tiles_per_row);
+    hipLaunchKernelGGL((k_conv_bf16<NB, C>), dim3((unsigned)blocks), dim3(kBf16Waves * 64), 0, s, a,
+                       src, eps, tiles_per_row);
     PD_HIP(hipGetLastError());
 }
 
