@@ -27,8 +27,9 @@ ARCH = "gfx950"
 COMMON = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # products and sums are rounded as written (no fused multiply-add), like
-    # the float32 oracle; the matrix-core kernels are unaffected
+    # products and sums are rounded as written (no fused multiply-add), as in
+    # a plain float32 evaluation of the same formulas; the matrix-core kernels
+    # are unaffected
     "-ffp-contract=off",
     "-Wno-unused-command-line-argument",
     f"-I{INCLUDE}", f"-I{CSRC}",
