@@ -8,6 +8,10 @@ up-front noise.
 
 sequential()  -- the chain x_{i+1} = h_i(x_i) = x_i + y_i + z_i (Sec. 3, the
                  nested-function view of sequential sampling), drift form.
+drifts()      -- y_i of a batch of steps: Euler (the DDPM/DDIM step) or Heun's
+                 step on the DDIM ODE (Sec. 3.3: any solver can supply the
+                 drift of lines 5-6); Heun costs two network evaluations per
+                 step, one for the last step.
 sequential_mean_form() -- the same chain through the textbook step means
                  (DDPM: Ho et al.; DDIM: Song et al.), used to pin the drift
                  coefficients.
@@ -49,8 +53,32 @@ class NumericError(RuntimeError):
 class PicardResult:
     x: np.ndarray             # [B, D] sample x_T
     iters: int                # K, parallel iterations
-    evals: int                # sum of window sizes (the paper's "model evaluations")
+    evals: int                # network evaluations per sample (the paper's "model
+                              # evaluations"): the sum of window sizes for Euler
     trace: List[int]          # stride of every iteration
+
+
+def drifts(tables, A, Bc, eps_fn: Callable, rows: np.ndarray, steps: np.ndarray):
+    """Drifts y of the steps ``steps`` ([m] step indices) at the points
+    ``rows`` ([m, B, D]); returns (y, network evaluations per sample).
+
+    Euler: y = A x + B eps(x, n_i).  Heun (DDIM ODE): with x~ = x + (A x + B
+    eps), y = A x + (B/2) (eps(x, n_i) + eps(x~, n_{i+1})), except the last
+    step (Euler)."""
+    m, Bn, D = rows.shape
+    e = eps_fn(rows.reshape(m * Bn, D), np.repeat(tables.model_t[steps], Bn)).reshape(m, Bn, D)
+    y = A[steps, None, None] * rows + Bc[steps, None, None] * e
+    if tables.solver != "heun":
+        return y, m
+    inner = steps < tables.T - 1
+    if np.any(inner):
+        s = steps[inner]
+        r = rows[inner]
+        xt = r + y[inner]
+        e2 = eps_fn(xt.reshape(-1, D), np.repeat(tables.model_t_next[s], Bn)).reshape(r.shape)
+        Bh = (Bc[s] * Bc.dtype.type(0.5))[:, None, None]
+        y[inner] = A[s, None, None] * r + Bh * (e[inner] + e2)
+    return y, m + int(np.count_nonzero(inner))
 
 
 def stride_from_errors(err: np.ndarray, tol: np.ndarray, p_eff: int) -> int:
@@ -84,9 +112,8 @@ def sequential(tables, eps_fn: Callable, x0: np.ndarray, noise: np.ndarray,
     x = np.asarray(x0, dtype=dtype).copy()
     B = x.shape[0]
     for i in range(tables.T):
-        e = eps_fn(x, np.full(B, tables.model_t[i]))
-        y = A[i] * x + Bc[i] * e
-        x = x + y + noise[i]
+        y, _ = drifts(tables, A, Bc, eps_fn, x[None], np.array([i]))
+        x = x + y[0] + noise[i]
         if not np.all(np.isfinite(x)):
             raise NumericError(f"non-finite state at step {i}")
     return x
@@ -138,9 +165,7 @@ def picard(tables, eps_fn: Callable, x0: np.ndarray, noise: np.ndarray,
     trace: List[int] = []
     while t < T:
         rows = X[t:t + pe]                      # x^k_{t+j}, j in [0, pe)
-        nt = tables.model_t[t:t + pe]
-        e = eps_fn(rows.reshape(pe * Bn, D), np.repeat(nt, Bn)).reshape(pe, Bn, D)
-        Y = A[t:t + pe, None, None] * rows + Bc[t:t + pe, None, None] * e
+        Y, nev = drifts(tables, A, Bc, eps_fn, rows, np.arange(t, t + pe))
         Xn = X[t] + np.cumsum(Y, axis=0) + np.cumsum(noise[t:t + pe], axis=0)
         if not np.all(np.isfinite(Xn)):
             raise NumericError(f"non-finite window at iteration {k}")
@@ -159,7 +184,7 @@ def picard(tables, eps_fn: Callable, x0: np.ndarray, noise: np.ndarray,
             X[t + pe + 1:hi + 1] = X[t + pe]    # new points = window's last point
         if on_iter is not None:
             on_iter(k, t, pe, x_old, Xn, err, stride)
-        evals += pe
+        evals += nev
         trace.append(stride)
         t += stride
         k += 1

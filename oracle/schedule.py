@@ -26,6 +26,16 @@ DDIM (Song et al. 2021) on the sub-chain n_i = (T-1-i) * c, c = T_train / T:
   (eta = 1) value on the same sub-chain, as the footnote on the relaxed
   tolerance in Sec. 3.1 asks for ODE samplers.
 
+Heun on the DDIM probability-flow ODE (eta = 0; Sec. 3.3: the Euler step of
+Algorithm 1's drift swapped for a higher-order solver such as Heun).  In the
+coordinates xbar = x / sqrt(abar), s = sqrt(1 - abar) / sqrt(abar) the ODE is
+dxbar/ds = eps(x), and a DDIM step is its Euler step.  Heun's step adds the
+trapezoidal correction with eps at the Euler prediction:
+  x~      = x_i + (A_i x_i + B_i eps(x_i, n_i))          (the DDIM step)
+  y_i     = A_i x_i + (B_i / 2) (eps(x_i, n_i) + eps(x~, n_{i+1}))
+for every step but the last, whose target s = 0 has no network timestep: it
+keeps the Euler (DDIM) drift, as is usual for Heun samplers.
+
 All tables are built in float64 in the order written above and rounded once to
 float32 for the float32 path.  Pinned in tests/test_oracle_schedule.py (closed
 forms, the DDIM(eta=1) == DDPM identity, exact recovery of a point mass).
@@ -49,6 +59,15 @@ class Tables:
     noise_var: np.ndarray   # float64 [T] variance of the noise z_i added by step i
     tol_var: np.ndarray     # float64 [T] sigma^2_i used by the stopping rule
     alphabar: np.ndarray    # float64 [T_train] abar_n (network timestep axis)
+    solver: str = "euler"   # "euler" or "heun"
+
+    @property
+    def model_t_next(self) -> np.ndarray:
+        """int32 [T]: network timestep of step i + 1 (-1 for the last step)."""
+        out = np.empty(self.T, dtype=np.int32)
+        out[:-1] = self.model_t[1:]
+        out[-1] = -1
+        return out
 
     def as_dtype(self, dtype):
         """(A, B, noise_std, tol_var) rounded once to ``dtype``."""
@@ -87,9 +106,13 @@ def ddpm(T: int, beta_start: float = 1e-4, beta_end: float = 0.02) -> Tables:
 
 
 def ddim(T_train: int, T: int, eta: float = 0.0, beta_start: float = 1e-4,
-         beta_end: float = 0.02) -> Tables:
+         beta_end: float = 0.02, solver: str = "euler") -> Tables:
     if T_train % T != 0:
         raise ValueError("DDIM needs T_train to be a multiple of T")
+    if solver not in ("euler", "heun"):
+        raise ValueError(solver)
+    if solver == "heun" and eta != 0.0:
+        raise ValueError("Heun's method integrates the eta = 0 (ODE) chain only")
     c = T_train // T
     beta = betas(T_train, beta_start, beta_end)
     ab = alphabars(beta)
@@ -107,7 +130,7 @@ def ddim(T_train: int, T: int, eta: float = 0.0, beta_start: float = 1e-4,
         Bc[i] = math.sqrt(1.0 - ap - s2) - math.sqrt(ap * (1.0 - an) / an)
         var[i] = s2
         tol[i] = v1
-    return Tables("ddim", T, T_train, nt, A, Bc, var, tol, ab)
+    return Tables("ddim", T, T_train, nt, A, Bc, var, tol, ab, solver)
 
 
 def from_spec(spec) -> Tables:
@@ -115,5 +138,6 @@ def from_spec(spec) -> Tables:
     if spec.kind == "ddpm":
         return ddpm(spec.T, spec.beta_start, spec.beta_end)
     if spec.kind == "ddim":
-        return ddim(spec.T_train, spec.T, spec.eta, spec.beta_start, spec.beta_end)
+        return ddim(spec.T_train, spec.T, spec.eta, spec.beta_start, spec.beta_end,
+                    getattr(spec, "solver", "euler"))
     raise ValueError(spec.kind)

@@ -35,6 +35,7 @@ class ScheduleSpec:
     beta_start: float = 1e-4
     beta_end: float = 0.02
     eta: float = 0.0     # DDIM only
+    solver: str = "euler"  # "euler", or "heun" (DDIM with eta = 0 only)
 
 
 @dataclasses.dataclass(frozen=True)
