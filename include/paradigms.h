@@ -72,21 +72,29 @@ const char* pd_version(void);
  *     noise variance s2, tolerance variance = the eta = 1 value (the paper
  *     keeps the tolerance of ODE samplers relative to the variance of the
  *     corresponding DDPM SDE, footnote in Sec. 3.1).
+ *   PD_DDIM_HEUN: the PD_DDIM chain with eta = 0 (required), integrated with
+ *     Heun's method instead of its Euler step (Sec. 3.3: any solver can supply
+ *     the drift of Algorithm 1's lines 5-6).  With the DDIM step as the Euler
+ *     prediction x~ = x + (A_i x + B_i eps(x, n_i)), the drift of every step
+ *     but the last is y_i = A_i x + (B_i / 2) (eps(x, n_i) + eps(x~, n_{i+1}));
+ *     the last step (to abar = 1, no network timestep) keeps the DDIM drift.
+ *     Two network evaluations per step, one for the last.
  * Tables are computed in double precision and rounded once to float.
  * tol_index_offset selects which variance the stride test of Algorithm 1
  * uses for the point x_{t+j}: 0 = sigma^2_{t+j} (default), -1 = sigma^2_{t+j-1}.
  */
 #define PD_DDPM 0
 #define PD_DDIM 1
+#define PD_DDIM_HEUN 2
 
 typedef struct pd_schedule_desc {
-    int32_t kind;              /* PD_DDPM or PD_DDIM                               */
+    int32_t kind;              /* PD_DDPM, PD_DDIM or PD_DDIM_HEUN                 */
     int32_t T_train;           /* length of the training chain, >= 2              */
     int32_t T;                 /* sampling steps; == T_train for DDPM             */
     int32_t tol_index_offset;  /* 0 or -1                                          */
     double beta_start;         /* 0 < beta_start <= beta_end < 1                   */
     double beta_end;
-    double eta;                /* DDIM only, in [0, 1]                             */
+    double eta;                /* DDIM only, in [0, 1]; 0 for PD_DDIM_HEUN         */
 } pd_schedule_desc;
 
 typedef struct pd_schedule pd_schedule;
@@ -177,7 +185,9 @@ pd_status pd_normals(uint64_t seed, uint32_t rng_stream, int64_t count, float* o
 typedef struct pd_sample_stats {
     int32_t iters;             /* K: sampler iterations (sequential: T)               */
     int32_t trace_cap;         /* capacity of stride_trace (in)                        */
-    int64_t evals_per_sample;  /* sum of window sizes: the paper's "model evaluations" */
+    int64_t evals_per_sample;  /* network evaluations per sample, the paper's "model
+                                  evaluations": the sum of window sizes (Heun: two
+                                  per window point, one for the last step)        */
     int64_t network_rows;      /* evals_per_sample * batch * (2 with guidance)         */
     int32_t* stride_trace;     /* optional host array: stride of each iteration        */
     int32_t time_kernels;      /* in: nonzero = bracket every denoiser, update and     */

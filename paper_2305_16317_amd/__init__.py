@@ -29,7 +29,7 @@ __all__ = [
 PD_OK, PD_ERR_INVALID_ARG, PD_ERR_OOM, PD_ERR_DEVICE, PD_ERR_NUMERIC, PD_ERR_UNSUPPORTED = range(6)
 STATUS_NAMES = {0: "PD_OK", 1: "PD_ERR_INVALID_ARG", 2: "PD_ERR_OOM", 3: "PD_ERR_DEVICE",
                 4: "PD_ERR_NUMERIC", 5: "PD_ERR_UNSUPPORTED"}
-PD_DDPM, PD_DDIM = 0, 1
+PD_DDPM, PD_DDIM, PD_DDIM_HEUN = 0, 1, 2
 PD_MODEL_GMM2D, PD_MODEL_MLP, PD_MODEL_CONV1X1 = 0, 1, 2
 PD_F32, PD_BF16 = 0, 1
 
@@ -311,7 +311,10 @@ def from_workload(w, weights: Dict[str, np.ndarray], tol_index_offset: int = 0):
     """(schedule, denoiser) handles for a ``workloads.Workload``.  The schedule
     carries the training chain (T_train, abar) that the denoiser needs."""
     s = w.schedule
-    kind = PD_DDPM if s.kind == "ddpm" else PD_DDIM
+    if s.kind == "ddpm":
+        kind = PD_DDPM
+    else:
+        kind = PD_DDIM_HEUN if getattr(s, "solver", "euler") == "heun" else PD_DDIM
     sched = pd_init_schedule(kind, s.T_train, s.T, s.beta_start, s.beta_end, s.eta,
                              tol_index_offset)
     m = w.model

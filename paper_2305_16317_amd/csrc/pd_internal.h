@@ -119,8 +119,20 @@ bool conv_supported(int C, int width, bool bf16);
 void launch_conv1x1(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s);
 
 // picard.hip
+// model_t_next / nrow2: Heun only (nullptr otherwise), the network timestep of
+// each window row's next step and its per-window copy.
 void launch_picard_init(LoopState* st, int32_t* slot, int32_t* nrow, const int32_t* model_t,
-                        int T, int p, hipStream_t s);
+                        const int32_t* model_t_next, int32_t* nrow2, int T, int p,
+                        hipStream_t s);
+// Heun on the window: Euler prediction of every row, then eps <- (eps + eps2)/2
+// for every row but the last step.
+void launch_heun_predict(const LoopState* st, const float* ring, const float* eps, const float* A,
+                         const float* B, int p, int64_t BD, float* xt, hipStream_t s);
+void launch_heun_combine(const LoopState* st, float* eps, const float* eps2, int p, int T,
+                         int64_t BD, hipStream_t s);
+void launch_seq_heun_predict(const float* x, const float* eps, float A, float B, int64_t n,
+                             float* xt, hipStream_t s);
+void launch_seq_heun_combine(float* eps, const float* eps2, int64_t n, hipStream_t s);
 int picard_partial_blocks(int64_t D);
 void launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
                         const float* A, const float* B, int p, int batch, int64_t D,
@@ -128,7 +140,8 @@ void launch_picard_scan(const LoopState* st, float* ring, const float* eps, cons
 void launch_picard_finalize(LoopState* st, const float* partials, int p, int batch, int64_t D,
                             int T, const float* tol_var, float tau2, int tol_offset,
                             const int32_t* model_t, int32_t* trace, int32_t* slot,
-                            int32_t* nrow, hipStream_t s);
+                            int32_t* nrow, const int32_t* model_t_next, int32_t* nrow2,
+                            hipStream_t s);
 void launch_seq_step(float* x, const float* eps, const float* z, float A, float B, int64_t n,
                      hipStream_t s);
 

@@ -47,8 +47,12 @@ __device__ __forceinline__ float drift(float A, float x, float B, float e) {
     return __fadd_rn(__fmul_rn(A, x), __fmul_rn(B, e));
 }
 
+// model_t_next / nrow2 (Heun only, else nullptr): the network timestep of the
+// step after each window row, for the second evaluation at the Euler prediction.
 __global__ void k_picard_init(LoopState* st, int32_t* slot, int32_t* nrow,
-                              const int32_t* __restrict__ model_t, int T, int p) {
+                              const int32_t* __restrict__ model_t,
+                              const int32_t* __restrict__ model_t_next, int32_t* nrow2, int T,
+                              int p) {
     const int pe = p < T ? p : T;
     if (threadIdx.x == 0) {
         st->t = 0;
@@ -62,7 +66,44 @@ __global__ void k_picard_init(LoopState* st, int32_t* slot, int32_t* nrow,
     for (int j = threadIdx.x; j < pe; j += blockDim.x) {
         slot[j] = 0;            // every initial window point is a copy of x_0
         nrow[j] = model_t[j];
+        if (nrow2) nrow2[j] = model_t_next[j];
     }
+}
+
+// Heun's method, window side (rows j < p_eff of the current window):
+// predict:  xt[j] = x_{t+j} + (A x_{t+j} + B eps[j])      (the Euler step)
+// combine:  eps[j] = (eps[j] + eps2[j]) / 2  for every step but the last, so
+//           that the scan's A x + B eps is A x + (B / 2)(eps + eps2) rounded
+//           exactly as written (halving is exact).
+__global__ __launch_bounds__(256) void k_heun_predict(const LoopState* __restrict__ st,
+                                                      const float* __restrict__ ring,
+                                                      const float* __restrict__ eps,
+                                                      const float* __restrict__ Atab,
+                                                      const float* __restrict__ Btab, int p,
+                                                      int64_t BD, float* __restrict__ xt) {
+    const int pe = st->p_eff;
+    const int t = st->t, f = st->f, P1 = p + 1;
+    const int64_t n = (int64_t)pe * BD;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int j = (int)(i / BD);
+        const int64_t c = i - (int64_t)j * BD;
+        const int m = t + j;
+        const float x = ring[(int64_t)((m <= f ? m : f) % P1) * BD + c];
+        xt[i] = __fadd_rn(x, drift(Atab[m], x, Btab[m], eps[i]));
+    }
+}
+
+__global__ __launch_bounds__(256) void k_heun_combine(const LoopState* __restrict__ st,
+                                                      float* __restrict__ eps,
+                                                      const float* __restrict__ eps2, int T,
+                                                      int64_t BD) {
+    const int pe = st->p_eff, t = st->t;
+    const int inner = t + pe < T ? pe : pe - 1;   // the last step keeps its Euler drift
+    const int64_t n = (int64_t)inner * BD;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        eps[i] = __fmul_rn(__fadd_rn(eps[i], eps2[i]), 0.5f);
 }
 
 // One block: 64 * VEC consecutive columns of one sample b, all window rows,
@@ -209,7 +250,8 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
 __global__ __launch_bounds__(1024) void k_picard_finalize(
     LoopState* st, const float* __restrict__ partials, int nblk, int p, int batch, int64_t D,
     int T, const float* __restrict__ tol_var, float tau2, int tol_offset,
-    const int32_t* __restrict__ model_t, int32_t* trace, int32_t* slot, int32_t* nrow) {
+    const int32_t* __restrict__ model_t, int32_t* trace, int32_t* slot, int32_t* nrow,
+    const int32_t* __restrict__ model_t_next, int32_t* nrow2) {
     const int pe = st->p_eff;
     if (pe <= 0) return;
     const int t = st->t, k = st->k;
@@ -258,7 +300,8 @@ __global__ __launch_bounds__(1024) void k_picard_finalize(
         trace[k] = stride;
         if (k == 0) st->first_stride = stride;
         st->k = k + 1;
-        st->evals += pe;
+        // network evaluations: Heun evaluates twice per point but the last step
+        st->evals += nrow2 ? 2 * pe - (t + pe == T ? 1 : 0) : pe;
         st->f = fn;
         st->t = s_bad ? T : tn;
         st->p_eff = pn > 0 ? pn : 0;
@@ -268,7 +311,27 @@ __global__ __launch_bounds__(1024) void k_picard_finalize(
         const int m = tn + j;
         slot[j] = (m < fn ? m : fn) % (p + 1);
         nrow[j] = model_t[m];
+        if (nrow2) nrow2[j] = model_t_next[m];
     }
+}
+
+// Heun's method, sequential side: the Euler prediction of one step, and the
+// averaged epsilon (both as in the window kernels above).
+__global__ __launch_bounds__(256) void k_seq_heun_predict(const float* __restrict__ x,
+                                                          const float* __restrict__ eps, float A,
+                                                          float B, int64_t n,
+                                                          float* __restrict__ xt) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    xt[i] = __fadd_rn(x[i], drift(A, x[i], B, eps[i]));
+}
+
+__global__ __launch_bounds__(256) void k_seq_heun_combine(float* __restrict__ eps,
+                                                          const float* __restrict__ eps2,
+                                                          int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    eps[i] = __fmul_rn(__fadd_rn(eps[i], eps2[i]), 0.5f);
 }
 
 __global__ __launch_bounds__(256) void k_seq_step(float* __restrict__ x,
@@ -290,8 +353,44 @@ int picard_partial_blocks(int64_t D) {
 }
 
 void launch_picard_init(LoopState* st, int32_t* slot, int32_t* nrow, const int32_t* model_t,
-                        int T, int p, hipStream_t s) {
-    hipLaunchKernelGGL(k_picard_init, dim3(1), dim3(256), 0, s, st, slot, nrow, model_t, T, p);
+                        const int32_t* model_t_next, int32_t* nrow2, int T, int p,
+                        hipStream_t s) {
+    hipLaunchKernelGGL(k_picard_init, dim3(1), dim3(256), 0, s, st, slot, nrow, model_t,
+                       model_t_next, nrow2, T, p);
+    PD_HIP(hipGetLastError());
+}
+
+static unsigned stream_blocks(int64_t n) {
+    const int64_t b = (n + 255) / 256;
+    return (unsigned)(b < 4096 ? (b > 0 ? b : 1) : 4096);
+}
+
+void launch_heun_predict(const LoopState* st, const float* ring, const float* eps, const float* A,
+                         const float* B, int p, int64_t BD, float* xt, hipStream_t s) {
+    hipLaunchKernelGGL(k_heun_predict, dim3(stream_blocks((int64_t)p * BD)), dim3(256), 0, s, st,
+                       ring, eps, A, B, p, BD, xt);
+    PD_HIP(hipGetLastError());
+}
+
+void launch_heun_combine(const LoopState* st, float* eps, const float* eps2, int p, int T,
+                         int64_t BD, hipStream_t s) {
+    hipLaunchKernelGGL(k_heun_combine, dim3(stream_blocks((int64_t)p * BD)), dim3(256), 0, s, st,
+                       eps, eps2, T, BD);
+    PD_HIP(hipGetLastError());
+}
+
+void launch_seq_heun_predict(const float* x, const float* eps, float A, float B, int64_t n,
+                             float* xt, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_seq_heun_predict, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, x,
+                       eps, A, B, n, xt);
+    PD_HIP(hipGetLastError());
+}
+
+void launch_seq_heun_combine(float* eps, const float* eps2, int64_t n, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_seq_heun_combine, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, eps,
+                       eps2, n);
     PD_HIP(hipGetLastError());
 }
 
@@ -328,10 +427,11 @@ void launch_picard_scan(const LoopState* st, float* ring, const float* eps, cons
 void launch_picard_finalize(LoopState* st, const float* partials, int p, int batch, int64_t D,
                             int T, const float* tol_var, float tau2, int tol_offset,
                             const int32_t* model_t, int32_t* trace, int32_t* slot,
-                            int32_t* nrow, hipStream_t s) {
+                            int32_t* nrow, const int32_t* model_t_next, int32_t* nrow2,
+                            hipStream_t s) {
     hipLaunchKernelGGL(k_picard_finalize, dim3(1), dim3(1024), 0, s, st, partials,
                        picard_partial_blocks(D), p, batch, D, T, tol_var, tau2, tol_offset,
-                       model_t, trace, slot, nrow);
+                       model_t, trace, slot, nrow, model_t_next, nrow2);
     PD_HIP(hipGetLastError());
 }
 

@@ -158,8 +158,10 @@ struct pd_schedule {
     int T = 0, T_train = 0;
     std::vector<float> A, B, noise_std, tol_var;
     std::vector<int32_t> model_t;
+    std::vector<int32_t> model_t_next;   // n_{i+1}; the last step repeats n_{T-1}
     std::vector<double> alphabar;
     bool has_noise = false;
+    bool heun = false;
 };
 
 static void build_tables(pd_schedule& s) {
@@ -181,7 +183,9 @@ static void build_tables(pd_schedule& s) {
     s.noise_std.resize(T);
     s.tol_var.resize(T);
     s.model_t.resize(T);
+    s.model_t_next.resize(T);
     s.has_noise = false;
+    s.heun = d.kind == PD_DDIM_HEUN;
     for (int i = 0; i < T; ++i) {
         double A, B, var, tol;
         int n;
@@ -213,6 +217,9 @@ static void build_tables(pd_schedule& s) {
         s.tol_var[i] = (float)tol;
         if (var > 0.0) s.has_noise = true;
     }
+    // the step after i; the last step has none and keeps its Euler drift, so
+    // its (unused) second evaluation is pointed at a valid timestep
+    for (int i = 0; i < T; ++i) s.model_t_next[i] = s.model_t[i + 1 < T ? i + 1 : i];
 }
 
 extern "C" pd_status pd_init_schedule(const pd_schedule_desc* desc, pd_schedule** out) {
@@ -220,15 +227,17 @@ extern "C" pd_status pd_init_schedule(const pd_schedule_desc* desc, pd_schedule*
         require(desc != nullptr && out != nullptr, "desc and out must not be NULL");
         *out = nullptr;
         const pd_schedule_desc& d = *desc;
-        require(d.kind == PD_DDPM || d.kind == PD_DDIM, "kind must be PD_DDPM or PD_DDIM");
+        require(d.kind == PD_DDPM || d.kind == PD_DDIM || d.kind == PD_DDIM_HEUN,
+                "kind must be PD_DDPM, PD_DDIM or PD_DDIM_HEUN");
         require(d.T_train >= 2, "T_train must be >= 2");
         require(d.T >= 1 && d.T <= d.T_train, "T must be in [1, T_train]");
         require(d.kind != PD_DDPM || d.T == d.T_train, "DDPM needs T == T_train");
-        require(d.kind != PD_DDIM || d.T_train % d.T == 0, "DDIM needs T_train % T == 0");
+        require(d.kind == PD_DDPM || d.T_train % d.T == 0, "DDIM needs T_train % T == 0");
         require(std::isfinite(d.beta_start) && std::isfinite(d.beta_end) && d.beta_start > 0.0 &&
                     d.beta_end < 1.0 && d.beta_start <= d.beta_end,
                 "need 0 < beta_start <= beta_end < 1");
         require(d.kind != PD_DDIM || (d.eta >= 0.0 && d.eta <= 1.0), "eta must be in [0, 1]");
+        require(d.kind != PD_DDIM_HEUN || d.eta == 0.0, "Heun integrates the eta = 0 (ODE) chain only");
         require(d.tol_index_offset == 0 || d.tol_index_offset == -1,
                 "tol_index_offset must be 0 or -1");
         auto s = std::make_unique<pd_schedule>();
@@ -474,6 +483,7 @@ struct pd_workspace {
     int p = 0, batch = 0, T = 0;
     int64_t D = 0;
     DevBuf ring, eps, noise, A, B, zstd, tolv, model_t, state, trace, slot, nrow, partials, scratch;
+    DevBuf xt, eps2, model_t_next, nrow2;   // Heun: predictions, second epsilons, n_{i+1}
     LoopState* h_state = nullptr;
     ~pd_workspace() {
         if (h_state) (void)hipHostFree(h_state);
@@ -505,6 +515,12 @@ static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, 
     w.slot.alloc(sizeof(int32_t) * (size_t)p);
     w.nrow.alloc(sizeof(int32_t) * (size_t)p);
     w.partials.alloc(sizeof(float) * (size_t)picard_partial_blocks(d.D) * p * batch);
+    if (s.heun) {
+        w.xt.alloc(sizeof(float) * (size_t)p * BD);
+        w.eps2.alloc(sizeof(float) * (size_t)p * BD);
+        w.model_t_next.upload(s.model_t_next.data(), s.T);
+        w.nrow2.alloc(sizeof(int32_t) * (size_t)p);
+    }
     const size_t sc = d.scratch_floats((int64_t)p * batch);
     if (sc) w.scratch.alloc(sc * sizeof(float));
     PD_HIP(hipHostMalloc(reinterpret_cast<void**>(&w.h_state), sizeof(LoopState), hipHostMallocDefault));
@@ -584,8 +600,9 @@ static void fill_stats(pd_sample_stats* stats, int iters, int64_t evals, int bat
 // The mixture model's whole sampling loop fits in one workgroup's LDS.
 static constexpr size_t kFusedLoopLds = 64 * 1024;
 
-static bool use_fused_gmm_loop(const pd_denoiser& d, int T, int p, int batch) {
-    return d.desc.kind == PD_MODEL_GMM2D &&
+static bool use_fused_gmm_loop(const pd_schedule& s, const pd_denoiser& d, int T, int p,
+                               int batch) {
+    return d.desc.kind == PD_MODEL_GMM2D && !s.heun &&
            gmm_loop_lds_bytes(T, d.desc.n_components, p, batch) <= kFusedLoopLds;
 }
 
@@ -626,7 +643,7 @@ extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoise
         tm.on = stats && stats->time_kernels;
         tm.st = st;
         draw_noise(w, noise_seed, st);
-        if (use_fused_gmm_loop(*d, s->T, 1, batch)) {
+        if (use_fused_gmm_loop(*s, *d, s->T, 1, batch)) {
             tm.mark(-1);
             launch_gmm_sequential_loop(gmm_loop_args(*s, *d, w, 1, batch, 0.f, x_out), st);
             tm.mark(CAT_UPDATE);
@@ -638,9 +655,19 @@ extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoise
             return;
         }
         tm.mark(-1);
+        int64_t evals = 0;
         for (int i = 0; i < s->T; ++i) {
             const RowSrc src{x, nullptr, BD, batch, 1, w.model_t.as<int32_t>() + i, nullptr};
             d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
+            ++evals;
+            if (s->heun && i + 1 < s->T) {     // Heun: second evaluation at the Euler prediction
+                launch_seq_heun_predict(x, w.eps.as<float>(), s->A[i], s->B[i], BD, w.xt.as<float>(), st);
+                const RowSrc src2{w.xt.as<float>(), nullptr, BD, batch, 1,
+                                  w.model_t_next.as<int32_t>() + i, nullptr};
+                d->forward(src2, w.eps2.as<float>(), w.scratch.as<float>(), st);
+                launch_seq_heun_combine(w.eps.as<float>(), w.eps2.as<float>(), BD, st);
+                ++evals;
+            }
             tm.mark(CAT_DENOISER);
             const float* z = w.noise.p ? w.noise.as<float>() + (int64_t)i * BD : nullptr;
             launch_seq_step(x, w.eps.as<float>(), z, s->A[i], s->B[i], BD, st);
@@ -650,7 +677,7 @@ extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoise
         PD_HIP(hipStreamSynchronize(st));
         tm.collect();
         if (stats) {
-            fill_stats(stats, s->T, s->T, batch, d->guided(), nullptr, tm);
+            fill_stats(stats, s->T, evals, batch, d->guided(), nullptr, tm);
             const int n = s->T < stats->trace_cap ? s->T : stats->trace_cap;
             for (int i = 0; i < n && stats->stride_trace; ++i) stats->stride_trace[i] = 1;
         }
@@ -680,7 +707,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         tm.on = stats && stats->time_kernels;
         tm.st = st;
         draw_noise(w, noise_seed, st);
-        if (use_fused_gmm_loop(*d, T, pc, batch)) {
+        if (use_fused_gmm_loop(*s, *d, T, pc, batch)) {
             tm.mark(-1);
             launch_gmm_picard_loop(gmm_loop_args(*s, *d, w, pc, batch, tau2, x_out), kFusedLoopLds,
                                    st);
@@ -692,8 +719,11 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
             fill_stats(stats, w.h_state->k, w.h_state->evals, batch, d->guided(), w.trace.as<int32_t>(), tm);
             return;
         }
+        const int32_t* mtn = s->heun ? w.model_t_next.as<int32_t>() : nullptr;
+        int32_t* nrow2 = s->heun ? w.nrow2.as<int32_t>() : nullptr;
         launch_picard_init(dst, w.slot.as<int32_t>(), w.nrow.as<int32_t>(),
-                           w.model_t.as<int32_t>(), T, pc, st);
+                           w.model_t.as<int32_t>(), mtn, nrow2, T, pc, st);
+        const RowSrc src2{w.xt.as<float>(), nullptr, BD, batch, pc, nrow2, &dst->p_eff};
         const RowSrc src{w.ring.as<float>(), w.slot.as<int32_t>(), BD,     batch,
                          pc,                 w.nrow.as<int32_t>(), &dst->p_eff};
         int t_host = 0, k_host = 0, issued = 0;
@@ -719,6 +749,12 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
             tm.mark(-1);
             for (int it = 0; it < need; ++it) {
                 d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
+                if (s->heun) {   // second evaluation at every row's Euler prediction
+                    launch_heun_predict(dst, w.ring.as<float>(), w.eps.as<float>(), w.A.as<float>(),
+                                        w.B.as<float>(), pc, BD, w.xt.as<float>(), st);
+                    d->forward(src2, w.eps2.as<float>(), w.scratch.as<float>(), st);
+                    launch_heun_combine(dst, w.eps.as<float>(), w.eps2.as<float>(), pc, T, BD, st);
+                }
                 tm.mark(CAT_DENOISER);
                 launch_picard_scan(dst, w.ring.as<float>(), w.eps.as<float>(), w.noise.as<float>(),
                                    w.A.as<float>(), w.B.as<float>(), pc, batch, d->D,
@@ -727,7 +763,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                 launch_picard_finalize(dst, w.partials.as<float>(), pc, batch, d->D, T,
                                        w.tolv.as<float>(), tau2, s->desc.tol_index_offset,
                                        w.model_t.as<int32_t>(), w.trace.as<int32_t>(),
-                                       w.slot.as<int32_t>(), w.nrow.as<int32_t>(), st);
+                                       w.slot.as<int32_t>(), w.nrow.as<int32_t>(), mtn, nrow2, st);
                 tm.mark(CAT_FINALIZE);
             }
             issued += need;

@@ -59,6 +59,8 @@ def _status(fn, *args):
     (dict(beta_start=float("nan")), "beta"),
     (dict(kind=pd.PD_DDIM, T=200, eta=1.5), "eta"),
     (dict(tol_index_offset=2), "tol_index_offset"),
+    (dict(kind=pd.PD_DDIM_HEUN, T=200, eta=0.5), "Heun"),
+    (dict(kind=pd.PD_DDIM_HEUN, T=300), "T_train % T"),
 ])
 def test_schedule_validation(kw, msg):
     args = dict(kind=pd.PD_DDPM, T_train=1000, T=1000, beta_start=1e-4, beta_end=0.02,
@@ -71,12 +73,14 @@ def test_schedule_validation(kw, msg):
 
 @pytest.mark.parametrize("spec", [("ddpm", 1000, 1000, 0.0), ("ddpm", 100, 100, 0.0),
                                   ("ddim", 1000, 200, 0.0), ("ddim", 1000, 50, 0.7),
-                                  ("ddpm", 2, 2, 0.0)])
+                                  ("ddpm", 2, 2, 0.0), ("heun", 1000, 100, 0.0)])
 def test_schedule_tables_bitwise_equal_oracle(spec):
     kind, Tt, T, eta = spec
-    s = pd.pd_init_schedule(pd.PD_DDPM if kind == "ddpm" else pd.PD_DDIM, Tt, T, eta=eta)
+    k = {"ddpm": pd.PD_DDPM, "ddim": pd.PD_DDIM, "heun": pd.PD_DDIM_HEUN}[kind]
+    s = pd.pd_init_schedule(k, Tt, T, eta=eta)
     tb = s.tables()
-    ref = osched.ddpm(T) if kind == "ddpm" else osched.ddim(Tt, T, eta)
+    ref = osched.ddpm(T) if kind == "ddpm" else osched.ddim(Tt, T, eta,
+                                                             solver="heun" if kind == "heun" else "euler")
     A, B, zs, tv = ref.as_dtype(np.float32)
     for name, ours, theirs in (("A", tb["A"], A), ("B", tb["B"], B),
                                ("noise_std", tb["noise_std"], zs), ("tol_var", tb["tol_var"], tv)):

@@ -341,3 +341,42 @@ def test_full_size_bf16_picard_matches_oracle():
     assert abs(st.iters - gp["iters"]) <= max(1, gp["iters"] // 10), (st.iters, gp["iters"])
     assert st.network_rows == st.evals_per_sample * 2
     _check_summary(got, gp, 2e-2)
+
+
+# ------------------------------------------------------- Heun drift (DDIM ODE)
+def _heun(model, T, p, batch, tau=0.05, seed=0):
+    return W.Workload("heun", W.ScheduleSpec("ddim", 10 * T, T, solver="heun"), model,
+                      p=p, tau=tau, batch=batch, noise_seed=seed)
+
+
+HEUN = {
+    # the mixture runs the general kernels here (its fused loop is Euler only)
+    "heun_gmm": lambda: _heun(W.ModelSpec("gmm2d", (2,)), 40, 12, 2),
+    "heun_mlp": lambda: _heun(W.ModelSpec("mlp", (4, 3), width=32), 30, 9, 2),
+    "heun_conv": lambda: _heun(W.ModelSpec("conv1x1", (4, 6, 7), width=32), 24, 8, 3),
+    "heun_conv_full_window": lambda: _heun(W.ModelSpec("conv1x1", (4, 8, 8), width=64), 16, 16, 1),
+}
+
+
+@pytest.mark.parametrize("name", list(HEUN))
+def test_heun_picard_matches_oracle(name):
+    wl = HEUN[name]()
+    w = W.make_weights(wl.model)
+    got, st = _run(wl, w)
+    ref = Problem(wl, w, np.float32).picard()
+    assert (st.iters, st.trace, st.evals_per_sample) == (ref.iters, ref.trace, ref.evals)
+    assert st.network_rows == ref.evals * wl.batch
+    assert _rel(got, ref.x) <= REL_F32, _rel(got, ref.x)
+
+
+@pytest.mark.parametrize("name", ["heun_gmm", "heun_mlp", "heun_conv"])
+def test_heun_sequential_matches_oracle_and_window_of_one(name):
+    wl = HEUN[name]()
+    w = W.make_weights(wl.model)
+    seq, st = _run(wl, w, "sequential")
+    T = wl.schedule.T
+    assert st.evals_per_sample == 2 * T - 1
+    assert _rel(seq, Problem(wl, w, np.float32).sequential()) <= REL_F32
+    one, st1 = _run(wl, w, "picard", p=1)
+    assert st1.iters == T and st1.evals_per_sample == 2 * T - 1
+    assert np.array_equal(one.view(np.uint32), seq.view(np.uint32))

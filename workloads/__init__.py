@@ -96,6 +96,14 @@ WORKLOADS: Dict[str, Workload] = {
         ModelSpec("conv1x1", _LATENT, width=320, dtype="bf16", cond_dim=768,
                   guidance=7.5),
         p=128, tau=0.1),
+    # Heun's method on the DDIM ODE (a higher-order drift, Sec. 3.3): the
+    # 16x10 policy at 20 steps, and the 4x96x96 latent at 100 steps
+    "policy_mlp_heun20": Workload(
+        "policy_mlp_heun20", ScheduleSpec("ddim", 100, 20, solver="heun"),
+        ModelSpec("mlp", (16, 10), width=1024), p=20, tau=0.1),
+    "latent_heun100_p32": Workload(
+        "latent_heun100_p32", ScheduleSpec("ddim", 1000, 100, solver="heun"),
+        ModelSpec("conv1x1", _LATENT, width=320), p=32, tau=0.05),
 }
 
 
