@@ -46,6 +46,15 @@ def flops_per_row(model) -> float:
     return 0.0
 
 
+def window_points(trace, p: int, T: int) -> int:
+    """Sum of the window sizes min(p, T - t) over the iterations of a stride trace."""
+    t, n = 0, 0
+    for s in trace:
+        n += min(p, T - t)
+        t += s
+    return n
+
+
 def update_bytes(wl, p_eff_sum: int, has_noise: bool) -> float:
     """Algorithmic HBM bytes of the Picard update summed over launches:
     per window point and column, read x^k and eps (and z), write x^{k+1}."""
@@ -253,7 +262,8 @@ def main() -> int:
     fl = flops_per_row(wl.model) * rows
     achieved = fl / (den_ms * 1e-3) if den_ms > 0 else 0.0
     has_noise = bool(np.any(sched.tables()["noise_std"] > 0))
-    ub = update_bytes(wl, evals, has_noise)
+    points = sum(window_points(st.trace, wl.p, wl.schedule.T) for st in stats)
+    ub = update_bytes(wl, points, has_noise)
     upd_rate = ub / (upd_ms * 1e-3) if upd_ms > 0 else 0.0
     traffic = traffic_from_profiles(wl.name, "k_conv_f32" if dtype == "f32" else "k_conv_bf16")
     out = {
