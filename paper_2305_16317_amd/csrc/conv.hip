@@ -86,7 +86,9 @@ struct ActVecs {
 // computed up front; the next layer's first slab consumes block 0 alone, so
 // the SiLU of blocks 1..NB-1 is spread over that slab's MFMAs (the old
 // accumulators of those blocks stay live instead of their activations, which
-// costs no extra registers) and runs on the VALU while the matrix core works.
+// costs no extra registers).  fp32 MFMAs do not co-issue with VALU work on
+// this GPU, so this spreads the SiLU between the MFMAs rather than hiding it;
+// it keeps the matrix core fed without a burst of dependent VALU work.
 template <int S, int NB>
 struct Spread {   // block k in [lo(s), hi(s)) is activated after MFMA slot s of S
     static constexpr __device__ int lo(int s) { return 1 + (s * (NB - 1)) / S; }

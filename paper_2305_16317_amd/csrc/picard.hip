@@ -8,6 +8,8 @@
 // finalize kernel of one iteration writes the row descriptors (ring slot and
 // network timestep of every window point) that the next iteration's denoiser
 // and scan read, so no host round trip is needed between iterations.
+#include <type_traits>
+
 #include "pd_internal.h"
 
 namespace pd {
@@ -40,6 +42,26 @@ template <int VEC>
 __device__ __forceinline__ float col_at(const typename Cols<VEC>::type& v, int c) {
     if constexpr (VEC == 1) return v;
     else return v[c];
+}
+
+// Sum over aligned groups of N lanes (N a power of two <= 64); every lane of
+// a group ends with the group's sum.  Groups up to 16 lanes reduce with DPP
+// lane moves inside a row (quad swaps, then the 8- and 16-lane mirrors), with
+// no LDS traffic; wider groups finish with a cross-row shuffle.
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+    auto dpp = [](float x, auto ctrl) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                             0, __builtin_bit_cast(int, x), decltype(ctrl)::value,
+                                             0xF, 0xF, false));
+    };
+    if constexpr (N >= 2) v += dpp(v, std::integral_constant<int, 0xB1>{});   // quad_perm [1,0,3,2]
+    if constexpr (N >= 4) v += dpp(v, std::integral_constant<int, 0x4E>{});   // quad_perm [2,3,0,1]
+    if constexpr (N >= 8) v += dpp(v, std::integral_constant<int, 0x141>{});  // row_half_mirror
+    if constexpr (N >= 16) v += dpp(v, std::integral_constant<int, 0x140>{}); // row_mirror
+    if constexpr (N >= 32) v += __shfl_xor(v, 16, 64);
+    if constexpr (N >= 64) v += __shfl_xor(v, 32, 64);
+    return v;
 }
 
 __device__ __forceinline__ float drift(float A, float x, float B, float e) {
@@ -235,8 +257,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < 64 / TPR; ++i) s += sh.d2[q][part + TPR * i];
-#pragma unroll
-    for (int off = TPR / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+    s = group_sum<TPR>(s);
     const int qw = q / R, qr = q % R;
     const int q0 = min(qw * ch, pe), nq = min(q0 + ch, pe) - q0;
     if (part == 0 && qr < nq) {
@@ -278,8 +299,7 @@ __global__ __launch_bounds__(1024) void k_picard_finalize(
             }
         }
         float s = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
-#pragma unroll
-        for (int off = kTeam / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, kTeam);
+        s = group_sum<kTeam>(s);
         if (tl == 0) {
             if (o == 0) {
                 if (s != 0.f) atomicOr(&s_bad, 1);
