@@ -134,14 +134,29 @@ void launch_seq_heun_predict(const float* x, const float* eps, float A, float B,
                              float* xt, hipStream_t s);
 void launch_seq_heun_combine(float* eps, const float* eps2, int64_t n, hipStream_t s);
 int picard_partial_blocks(int64_t D);
-void launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
+// Everything the stride rule and the slide need (the finalize step).
+struct FinalizeArgs {
+    LoopState* st;
+    const float* partials;      // [batch][p][picard_partial_blocks(D)]
+    int32_t p, batch;
+    int64_t D;
+    int32_t T;
+    const float* tol_var;
+    float tau2;
+    int32_t tol_offset;
+    const int32_t* model_t;
+    int32_t* trace;
+    int32_t* slot;
+    int32_t* nrow;
+    const int32_t* model_t_next;   // Heun only, else nullptr
+    int32_t* nrow2;                // Heun only, else nullptr
+};
+// Scan + error partials of one iteration.  Returns true when the grid is a
+// single block, which then also ran the finalize step.
+bool launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
                         const float* A, const float* B, int p, int batch, int64_t D,
-                        float* partials, hipStream_t s);
-void launch_picard_finalize(LoopState* st, const float* partials, int p, int batch, int64_t D,
-                            int T, const float* tol_var, float tau2, int tol_offset,
-                            const int32_t* model_t, int32_t* trace, int32_t* slot,
-                            int32_t* nrow, const int32_t* model_t_next, int32_t* nrow2,
-                            hipStream_t s);
+                        float* partials, const FinalizeArgs& fin, hipStream_t s);
+void launch_picard_finalize(const FinalizeArgs& fin, hipStream_t s);
 void launch_seq_step(float* x, const float* eps, const float* z, float A, float B, int64_t n,
                      hipStream_t s);
 

@@ -128,6 +128,78 @@ __global__ __launch_bounds__(256) void k_heun_combine(const LoopState* __restric
         eps[i] = __fmul_rn(__fadd_rn(eps[i], eps2[i]), 0.5f);
 }
 
+// One block: reduce the partials of every (offset, sample), apply the stride
+// rule, slide the window and prepare the next iteration's row descriptors.
+// Every thread reads the loop state before the first barrier; thread 0
+// rewrites it after the last one.
+__device__ void finalize_body(const FinalizeArgs& a, int nblk) {
+    LoopState* st = a.st;
+    const int pe = st->p_eff;
+    if (pe <= 0) return;
+    const int t = st->t, k = st->k, p = a.p, T = a.T;
+    __shared__ int s_stride, s_bad;
+    if (threadIdx.x == 0) {
+        s_stride = pe;
+        s_bad = 0;
+    }
+    __syncthreads();
+    constexpr int kTeam = 16;
+    const int team = threadIdx.x / kTeam, tl = threadIdx.x % kTeam;
+    const int nteams = blockDim.x / kTeam;
+    const float Df = (float)a.D;
+    for (int pair = team; pair < pe * a.batch; pair += nteams) {
+        const int o = pair / a.batch, b = pair % a.batch;
+        const float* src = a.partials + ((int64_t)b * p + o) * nblk;
+        // 8 independent loads per step keep the team's reads in flight together
+        float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        for (int i0 = 0; i0 < nblk; i0 += 8 * kTeam) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int i = i0 + u * kTeam + tl;
+                acc[u] += i < nblk ? src[i] : 0.f;
+            }
+        }
+        float s = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
+        s = group_sum<kTeam>(s);
+        if (tl == 0) {
+            if (o == 0) {
+                if (s != 0.f) atomicOr(&s_bad, 1);
+            } else {
+                const float err = s / Df;
+                if (!isfinite(err)) atomicOr(&s_bad, 1);
+                const float s2 = a.tol_var[t + o + a.tol_offset];
+                const float tol = (s2 == 0.f) ? 0.f : a.tau2 * s2;
+                if (!(err <= tol)) atomicMin(&s_stride, o);
+            }
+        }
+    }
+    __syncthreads();
+    const int stride = s_stride;
+    const int fn = t + pe, tn = t + stride;
+    const int pn = s_bad ? 0 : (p < T - tn ? p : T - tn);
+    if (threadIdx.x == 0) {
+        a.trace[k] = stride;
+        if (k == 0) st->first_stride = stride;
+        st->k = k + 1;
+        // network evaluations: Heun evaluates twice per point but the last step
+        st->evals += a.nrow2 ? 2 * pe - (t + pe == T ? 1 : 0) : pe;
+        st->f = fn;
+        st->t = s_bad ? T : tn;
+        st->p_eff = pn > 0 ? pn : 0;
+        if (s_bad) st->status = PD_ERR_NUMERIC;
+    }
+    for (int j = threadIdx.x; j < pn; j += blockDim.x) {
+        const int m = tn + j;
+        a.slot[j] = (m < fn ? m : fn) % (p + 1);
+        a.nrow[j] = a.model_t[m];
+        if (a.nrow2) a.nrow2[j] = a.model_t_next[m];
+    }
+}
+
+__global__ __launch_bounds__(1024) void k_picard_finalize(FinalizeArgs a, int nblk) {
+    finalize_body(a, nblk);
+}
+
 // One block: 64 * VEC consecutive columns of one sample b, all window rows,
 // split over 16 waves (rows [w*ch, (w+1)*ch) per wave, ch <= R).  Drift and
 // noise are summed along the rows inside each wave, the wave totals are
@@ -144,7 +216,8 @@ template <int R, int VEC, bool NOISE>
 __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     const LoopState* __restrict__ st, float* ring, const float* __restrict__ eps,
     const float* __restrict__ noise, const float* __restrict__ Atab,
-    const float* __restrict__ Btab, int p, int batch, int64_t D, float* __restrict__ partials) {
+    const float* __restrict__ Btab, int p, int batch, int64_t D, float* __restrict__ partials,
+    FinalizeArgs fin, int fuse_finalize) {
     typedef typename Cols<VEC>::type V;
     constexpr int NW = kScanWaves;
     const int pe = st->p_eff;
@@ -264,76 +337,13 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
         const int jq = q0 + qr;
         partials[((int64_t)b * p + (jq + 1 < pe ? jq + 1 : 0)) * nblk + blk] = s;
     }
+    // a grid of one block finalizes the iteration itself: one launch fewer
+    if (fuse_finalize) {
+        __syncthreads();
+        finalize_body(fin, nblk);
+    }
 }
 
-// One block: reduce the partials of every (offset, sample), apply the stride
-// rule, slide the window and prepare the next iteration's row descriptors.
-__global__ __launch_bounds__(1024) void k_picard_finalize(
-    LoopState* st, const float* __restrict__ partials, int nblk, int p, int batch, int64_t D,
-    int T, const float* __restrict__ tol_var, float tau2, int tol_offset,
-    const int32_t* __restrict__ model_t, int32_t* trace, int32_t* slot, int32_t* nrow,
-    const int32_t* __restrict__ model_t_next, int32_t* nrow2) {
-    const int pe = st->p_eff;
-    if (pe <= 0) return;
-    const int t = st->t, k = st->k;
-    __shared__ int s_stride, s_bad;
-    if (threadIdx.x == 0) {
-        s_stride = pe;
-        s_bad = 0;
-    }
-    __syncthreads();
-    constexpr int kTeam = 16;
-    const int team = threadIdx.x / kTeam, tl = threadIdx.x % kTeam;
-    const int nteams = blockDim.x / kTeam;
-    const float Df = (float)D;
-    for (int pair = team; pair < pe * batch; pair += nteams) {
-        const int o = pair / batch, b = pair % batch;
-        const float* src = partials + ((int64_t)b * p + o) * nblk;
-        // 8 independent loads per step keep the team's reads in flight together
-        float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        for (int i0 = 0; i0 < nblk; i0 += 8 * kTeam) {
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int i = i0 + u * kTeam + tl;
-                acc[u] += i < nblk ? src[i] : 0.f;
-            }
-        }
-        float s = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
-        s = group_sum<kTeam>(s);
-        if (tl == 0) {
-            if (o == 0) {
-                if (s != 0.f) atomicOr(&s_bad, 1);
-            } else {
-                const float err = s / Df;
-                if (!isfinite(err)) atomicOr(&s_bad, 1);
-                const float s2 = tol_var[t + o + tol_offset];
-                const float tol = (s2 == 0.f) ? 0.f : tau2 * s2;
-                if (!(err <= tol)) atomicMin(&s_stride, o);
-            }
-        }
-    }
-    __syncthreads();
-    const int stride = s_stride;
-    const int fn = t + pe, tn = t + stride;
-    const int pn = s_bad ? 0 : (p < T - tn ? p : T - tn);
-    if (threadIdx.x == 0) {
-        trace[k] = stride;
-        if (k == 0) st->first_stride = stride;
-        st->k = k + 1;
-        // network evaluations: Heun evaluates twice per point but the last step
-        st->evals += nrow2 ? 2 * pe - (t + pe == T ? 1 : 0) : pe;
-        st->f = fn;
-        st->t = s_bad ? T : tn;
-        st->p_eff = pn > 0 ? pn : 0;
-        if (s_bad) st->status = PD_ERR_NUMERIC;
-    }
-    for (int j = threadIdx.x; j < pn; j += blockDim.x) {
-        const int m = tn + j;
-        slot[j] = (m < fn ? m : fn) % (p + 1);
-        nrow[j] = model_t[m];
-        if (nrow2) nrow2[j] = model_t_next[m];
-    }
-}
 
 // Heun's method, sequential side: the Euler prediction of one step, and the
 // averaged epsilon (both as in the window kernels above).
@@ -415,43 +425,39 @@ void launch_seq_heun_combine(float* eps, const float* eps2, int64_t n, hipStream
 }
 
 template <int R, int VEC>
-static void launch_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
+static bool launch_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
                         const float* A, const float* B, int p, int batch, int64_t D,
-                        float* partials, hipStream_t s) {
+                        float* partials, const FinalizeArgs& fin, hipStream_t s) {
     const dim3 grid((unsigned)picard_partial_blocks(D), (unsigned)batch);
+    const int fuse = grid.x * grid.y == 1;
     if (noise)
         hipLaunchKernelGGL((k_picard_scan<R, VEC, true>), grid, dim3(kScanWaves * 64), 0, s, st,
-                           ring, eps, noise, A, B, p, batch, D, partials);
+                           ring, eps, noise, A, B, p, batch, D, partials, fin, fuse);
     else
         hipLaunchKernelGGL((k_picard_scan<R, VEC, false>), grid, dim3(kScanWaves * 64), 0, s, st,
-                           ring, eps, noise, A, B, p, batch, D, partials);
+                           ring, eps, noise, A, B, p, batch, D, partials, fin, fuse);
     PD_HIP(hipGetLastError());
+    return fuse != 0;
 }
 
-void launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
+bool launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
                         const float* A, const float* B, int p, int batch, int64_t D,
-                        float* partials, hipStream_t s) {
+                        float* partials, const FinalizeArgs& fin, hipStream_t s) {
     if (p > kMaxWindow) fail(PD_ERR_UNSUPPORTED, "window larger than 128 points");
     const int ch = (p + kScanWaves - 1) / kScanWaves;    // rows per wave at a full window
     const bool v4 = scan_vec(D) == 4;
-#define PD_SCAN(R)                                                                         \
-    if (ch <= R) {                                                                         \
-        if (v4) launch_scan<R, 4>(st, ring, eps, noise, A, B, p, batch, D, partials, s);   \
-        else launch_scan<R, 1>(st, ring, eps, noise, A, B, p, batch, D, partials, s);      \
-        return;                                                                            \
-    }
+#define PD_SCAN(R)                                                                              \
+    if (ch <= R)                                                                                \
+        return v4 ? launch_scan<R, 4>(st, ring, eps, noise, A, B, p, batch, D, partials, fin, s) \
+                  : launch_scan<R, 1>(st, ring, eps, noise, A, B, p, batch, D, partials, fin, s);
     PD_SCAN(1) PD_SCAN(2) PD_SCAN(4) PD_SCAN(8)
 #undef PD_SCAN
+    return false;
 }
 
-void launch_picard_finalize(LoopState* st, const float* partials, int p, int batch, int64_t D,
-                            int T, const float* tol_var, float tau2, int tol_offset,
-                            const int32_t* model_t, int32_t* trace, int32_t* slot,
-                            int32_t* nrow, const int32_t* model_t_next, int32_t* nrow2,
-                            hipStream_t s) {
-    hipLaunchKernelGGL(k_picard_finalize, dim3(1), dim3(1024), 0, s, st, partials,
-                       picard_partial_blocks(D), p, batch, D, T, tol_var, tau2, tol_offset,
-                       model_t, trace, slot, nrow, model_t_next, nrow2);
+void launch_picard_finalize(const FinalizeArgs& fin, hipStream_t s) {
+    hipLaunchKernelGGL(k_picard_finalize, dim3(1), dim3(1024), 0, s, fin,
+                       picard_partial_blocks(fin.D));
     PD_HIP(hipGetLastError());
 }
 

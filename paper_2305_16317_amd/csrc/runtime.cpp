@@ -724,6 +724,10 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         launch_picard_init(dst, w.slot.as<int32_t>(), w.nrow.as<int32_t>(),
                            w.model_t.as<int32_t>(), mtn, nrow2, T, pc, st);
         const RowSrc src2{w.xt.as<float>(), nullptr, BD, batch, pc, nrow2, &dst->p_eff};
+        const FinalizeArgs fin{dst, w.partials.as<float>(), pc, batch, d->D, T, w.tolv.as<float>(),
+                               tau2, s->desc.tol_index_offset, w.model_t.as<int32_t>(),
+                               w.trace.as<int32_t>(), w.slot.as<int32_t>(), w.nrow.as<int32_t>(),
+                               mtn, nrow2};
         const RowSrc src{w.ring.as<float>(), w.slot.as<int32_t>(), BD,     batch,
                          pc,                 w.nrow.as<int32_t>(), &dst->p_eff};
         int t_host = 0, k_host = 0, issued = 0;
@@ -756,15 +760,15 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                     launch_heun_combine(dst, w.eps.as<float>(), w.eps2.as<float>(), pc, T, BD, st);
                 }
                 tm.mark(CAT_DENOISER);
-                launch_picard_scan(dst, w.ring.as<float>(), w.eps.as<float>(), w.noise.as<float>(),
-                                   w.A.as<float>(), w.B.as<float>(), pc, batch, d->D,
-                                   w.partials.as<float>(), st);
+                const bool fused = launch_picard_scan(dst, w.ring.as<float>(), w.eps.as<float>(),
+                                                      w.noise.as<float>(), w.A.as<float>(),
+                                                      w.B.as<float>(), pc, batch, d->D,
+                                                      w.partials.as<float>(), fin, st);
                 tm.mark(CAT_UPDATE);
-                launch_picard_finalize(dst, w.partials.as<float>(), pc, batch, d->D, T,
-                                       w.tolv.as<float>(), tau2, s->desc.tol_index_offset,
-                                       w.model_t.as<int32_t>(), w.trace.as<int32_t>(),
-                                       w.slot.as<int32_t>(), w.nrow.as<int32_t>(), mtn, nrow2, st);
-                tm.mark(CAT_FINALIZE);
+                if (!fused) {
+                    launch_picard_finalize(fin, st);
+                    tm.mark(CAT_FINALIZE);
+                }
             }
             issued += need;
             PD_HIP(hipMemcpyAsync(w.h_state, dst, sizeof(LoopState), hipMemcpyDeviceToHost, st));
