@@ -310,7 +310,7 @@ def _check_summary(got, g, tol):
 
 
 @pytest.mark.parametrize("name", ["gmm2d_ddpm100", "policy_mlp_ddpm100", "latent_ddpm1000_p64",
-                                  "latent_ddim200_b4"])
+                                  "latent_ddim200_b4", "policy_mlp_heun20", "latent_heun100_p32"])
 def test_full_size_picard_matches_oracle(name):
     g = _golden(name)
     wl = W.WORKLOADS[name]
