@@ -8,10 +8,12 @@ up-front noise.
 
 sequential()  -- the chain x_{i+1} = h_i(x_i) = x_i + y_i + z_i (Sec. 3, the
                  nested-function view of sequential sampling), drift form.
-drifts()      -- y_i of a batch of steps: Euler (the DDPM/DDIM step) or Heun's
+drifts()      -- y_i of a batch of steps: Euler (the DDPM/DDIM step), Heun's
                  step on the DDIM ODE (Sec. 3.3: any solver can supply the
-                 drift of lines 5-6); Heun costs two network evaluations per
-                 step, one for the last step.
+                 drift of lines 5-6; two network evaluations per step, one for
+                 the last), or DPM-Solver++(2M), whose drift also reads the
+                 previous step's point and epsilon (Picard evaluates the point
+                 before the window once per iteration for it).
 sequential_mean_form() -- the same chain through the textbook step means
                  (DDPM: Ho et al.; DDIM: Song et al.), used to pin the drift
                  coefficients.
@@ -58,18 +60,29 @@ class PicardResult:
     trace: List[int]          # stride of every iteration
 
 
-def drifts(tables, A, Bc, eps_fn: Callable, rows: np.ndarray, steps: np.ndarray):
-    """Drifts y of the steps ``steps`` ([m] step indices) at the points
-    ``rows`` ([m, B, D]); returns (y, network evaluations per sample).
+def drifts(tables, A, Bc, eps_fn: Callable, rows: np.ndarray, steps: np.ndarray, prev=None):
+    """Drifts y of the consecutive steps ``steps`` ([m] step indices) at the
+    points ``rows`` ([m, B, D]); returns (y, network evaluations per sample,
+    eps of the rows).
 
     Euler: y = A x + B eps(x, n_i).  Heun (DDIM ODE): with x~ = x + (A x + B
     eps), y = A x + (B/2) (eps(x, n_i) + eps(x~, n_{i+1})), except the last
-    step (Euler)."""
+    step (Euler).  DPM-Solver++(2M): y = ((A x + B eps) + R x_{i-1}) + S
+    eps_{i-1} on its second-order steps, where row 0 takes x_{i-1}, eps_{i-1}
+    from ``prev`` = (x, eps) of the step before ``steps[0]``."""
     m, Bn, D = rows.shape
     e = eps_fn(rows.reshape(m * Bn, D), np.repeat(tables.model_t[steps], Bn)).reshape(m, Bn, D)
     y = A[steps, None, None] * rows + Bc[steps, None, None] * e
+    if tables.solver == "dpm2m":
+        R, S = tables.rs_dtype(Bc.dtype)
+        for j, i in enumerate(steps):
+            if R[i] == 0:
+                continue                      # first-order step
+            xp, ep = (rows[j - 1], e[j - 1]) if j > 0 else prev
+            y[j] = (y[j] + R[i] * xp) + S[i] * ep
+        return y, m, e
     if tables.solver != "heun":
-        return y, m
+        return y, m, e
     inner = steps < tables.T - 1
     if np.any(inner):
         s = steps[inner]
@@ -78,7 +91,7 @@ def drifts(tables, A, Bc, eps_fn: Callable, rows: np.ndarray, steps: np.ndarray)
         e2 = eps_fn(xt.reshape(-1, D), np.repeat(tables.model_t_next[s], Bn)).reshape(r.shape)
         Bh = (Bc[s] * Bc.dtype.type(0.5))[:, None, None]
         y[inner] = A[s, None, None] * r + Bh * (e[inner] + e2)
-    return y, m + int(np.count_nonzero(inner))
+    return y, m + int(np.count_nonzero(inner)), e
 
 
 def stride_from_errors(err: np.ndarray, tol: np.ndarray, p_eff: int) -> int:
@@ -111,8 +124,10 @@ def sequential(tables, eps_fn: Callable, x0: np.ndarray, noise: np.ndarray,
     A, Bc, _, _ = _tables(tables, dtype)
     x = np.asarray(x0, dtype=dtype).copy()
     B = x.shape[0]
+    prev = None
     for i in range(tables.T):
-        y, _ = drifts(tables, A, Bc, eps_fn, x[None], np.array([i]))
+        y, _, e = drifts(tables, A, Bc, eps_fn, x[None], np.array([i]), prev)
+        prev = (x, e[0])
         x = x + y[0] + noise[i]
         if not np.all(np.isfinite(x)):
             raise NumericError(f"non-finite state at step {i}")
@@ -165,7 +180,12 @@ def picard(tables, eps_fn: Callable, x0: np.ndarray, noise: np.ndarray,
     trace: List[int] = []
     while t < T:
         rows = X[t:t + pe]                      # x^k_{t+j}, j in [0, pe)
-        Y, nev = drifts(tables, A, Bc, eps_fn, rows, np.arange(t, t + pe))
+        prev, nh = None, 0
+        if tables.solver == "dpm2m" and t >= 1:  # the multistep drift needs x_{t-1}, eps_{t-1}
+            eh = eps_fn(X[t - 1], np.full(Bn, tables.model_t[t - 1]))
+            prev, nh = (X[t - 1], eh), 1
+        Y, nev, _ = drifts(tables, A, Bc, eps_fn, rows, np.arange(t, t + pe), prev)
+        nev += nh
         Xn = X[t] + np.cumsum(Y, axis=0) + np.cumsum(noise[t:t + pe], axis=0)
         if not np.all(np.isfinite(Xn)):
             raise NumericError(f"non-finite window at iteration {k}")

@@ -36,6 +36,20 @@ trapezoidal correction with eps at the Euler prediction:
 for every step but the last, whose target s = 0 has no network timestep: it
 keeps the Euler (DDIM) drift, as is usual for Heun samplers.
 
+DPM-Solver++ second-order multistep on the same eta = 0 chain (the paper's
+ParaDPMSolver, Sec. 4: DPMSolver's steps solved by Picard iteration).  With
+alpha = sqrt(abar), sig = sqrt(1 - abar), lambda = log(alpha / sig), the data
+prediction x0 = (x - sig eps) / alpha and h_i = lambda_{i+1} - lambda_i,
+r_i = h_{i-1} / h_i, phi_i = exp(-h_i) - 1:
+  x_{i+1} = (sig_{i+1}/sig_i) x_i - alpha_{i+1} phi_i D_i,
+  D_i = (1 + 1/(2 r_i)) x0_i - (1/(2 r_i)) x0_{i-1},
+so the drift is y_i = P_i x_i + Q_i eps_i + R_i x_{i-1} + S_i eps_{i-1} with
+  P_i = sig_{i+1}/sig_i - alpha_{i+1} phi_i (1 + 1/(2 r_i)) / alpha_i - 1,
+  Q_i = alpha_{i+1} phi_i (1 + 1/(2 r_i)) sig_i / alpha_i,
+  R_i = alpha_{i+1} phi_i / (2 r_i alpha_{i-1}),  S_i = -R_i sig_{i-1}.
+The first step (no x_{i-1}) and the last (sig = 0: lambda infinite) are first
+order, i.e. the DDIM step (P = A, Q = B, R = S = 0).  Tables A, B hold P, Q.
+
 All tables are built in float64 in the order written above and rounded once to
 float32 for the float32 path.  Pinned in tests/test_oracle_schedule.py (closed
 forms, the DDIM(eta=1) == DDPM identity, exact recovery of a point mass).
@@ -59,7 +73,9 @@ class Tables:
     noise_var: np.ndarray   # float64 [T] variance of the noise z_i added by step i
     tol_var: np.ndarray     # float64 [T] sigma^2_i used by the stopping rule
     alphabar: np.ndarray    # float64 [T_train] abar_n (network timestep axis)
-    solver: str = "euler"   # "euler" or "heun"
+    solver: str = "euler"   # "euler", "heun" or "dpm2m"
+    R: np.ndarray = None    # float64 [T] (dpm2m) drift coefficient on x_{i-1}
+    S: np.ndarray = None    # float64 [T] (dpm2m) drift coefficient on eps_{i-1}
 
     @property
     def model_t_next(self) -> np.ndarray:
@@ -68,6 +84,12 @@ class Tables:
         out[:-1] = self.model_t[1:]
         out[-1] = -1
         return out
+
+    def rs_dtype(self, dtype):
+        """(R, S) rounded once to ``dtype`` (zeros unless dpm2m)."""
+        z = np.zeros(self.T)
+        return ((self.R if self.R is not None else z).astype(dtype),
+                (self.S if self.S is not None else z).astype(dtype))
 
     def as_dtype(self, dtype):
         """(A, B, noise_std, tol_var) rounded once to ``dtype``."""
@@ -109,10 +131,10 @@ def ddim(T_train: int, T: int, eta: float = 0.0, beta_start: float = 1e-4,
          beta_end: float = 0.02, solver: str = "euler") -> Tables:
     if T_train % T != 0:
         raise ValueError("DDIM needs T_train to be a multiple of T")
-    if solver not in ("euler", "heun"):
+    if solver not in ("euler", "heun", "dpm2m"):
         raise ValueError(solver)
-    if solver == "heun" and eta != 0.0:
-        raise ValueError("Heun's method integrates the eta = 0 (ODE) chain only")
+    if solver != "euler" and eta != 0.0:
+        raise ValueError("Heun and DPM-Solver integrate the eta = 0 (ODE) chain only")
     c = T_train // T
     beta = betas(T_train, beta_start, beta_end)
     ab = alphabars(beta)
@@ -130,7 +152,25 @@ def ddim(T_train: int, T: int, eta: float = 0.0, beta_start: float = 1e-4,
         Bc[i] = math.sqrt(1.0 - ap - s2) - math.sqrt(ap * (1.0 - an) / an)
         var[i] = s2
         tol[i] = v1
-    return Tables("ddim", T, T_train, nt, A, Bc, var, tol, ab, solver)
+    tb = Tables("ddim", T, T_train, nt, A, Bc, var, tol, ab, solver)
+    if solver == "dpm2m":
+        tb.R = np.zeros(T)
+        tb.S = np.zeros(T)
+        for i in range(1, T - 1):          # second order between the first and last steps
+            n = int(nt[i])
+            a, sg = math.sqrt(ab[n]), math.sqrt(1.0 - ab[n])
+            a1, s1 = math.sqrt(ab[n - c]), math.sqrt(1.0 - ab[n - c])
+            a0, s0 = math.sqrt(ab[n + c]), math.sqrt(1.0 - ab[n + c])
+            lam, lam1, lam0 = math.log(a / sg), math.log(a1 / s1), math.log(a0 / s0)
+            h, h0 = lam1 - lam, lam - lam0
+            r = h0 / h
+            phi = math.expm1(-h)
+            g = 1.0 + 1.0 / (2.0 * r)
+            A[i] = s1 / sg - a1 * phi * g / a - 1.0
+            Bc[i] = a1 * phi * g * sg / a
+            tb.R[i] = a1 * phi / (2.0 * r * a0)
+            tb.S[i] = -tb.R[i] * s0
+    return tb
 
 
 def from_spec(spec) -> Tables:

@@ -86,7 +86,7 @@ def test_heun_drift_definition():
     A, Bc = tb.A, tb.B
     x = pr.x0
     for i in (0, 5, 11):
-        y, nev = samplers.drifts(tb, A, Bc, pr.eps, x[None], np.array([i]))
+        y, nev, _ = samplers.drifts(tb, A, Bc, pr.eps, x[None], np.array([i]))
         e = pr.eps(x, np.full(x.shape[0], tb.model_t[i]))
         if i < 11:
             xt = x + (A[i] * x + Bc[i] * e)

@@ -96,7 +96,7 @@ WORKLOADS: Dict[str, Workload] = {
         ModelSpec("conv1x1", _LATENT, width=320, dtype="bf16", cond_dim=768,
                   guidance=7.5),
         p=128, tau=0.1),
-    # Heun's method on the DDIM ODE (a higher-order drift, Sec. 3.3): the
+    # Heun's method on the DDIM ODE (a higher-order solver, Sec. 3.3): the
     # 16x10 policy at 20 steps, and the 4x96x96 latent at 100 steps
     "policy_mlp_heun20": Workload(
         "policy_mlp_heun20", ScheduleSpec("ddim", 100, 20, solver="heun"),
