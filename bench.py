@@ -55,11 +55,40 @@ def window_points(trace, p: int, T: int) -> int:
     return n
 
 
-def update_bytes(wl, p_eff_sum: int, has_noise: bool) -> float:
+def history_rows(trace, T: int) -> int:
+    """Iterations of a stride trace whose window starts past step 0 (the
+    multistep drift reads x_{t-1} and eps_{t-1} there)."""
+    t, n = 0, 0
+    for s in trace:
+        n += t >= 1
+        t += s
+    return n
+
+
+def update_bytes(wl, p_eff_sum: int, has_noise: bool, hist_sum: int = 0) -> float:
     """Algorithmic HBM bytes of the Picard update summed over launches:
-    per window point and column, read x^k and eps (and z), write x^{k+1}."""
+    per window point and column, read x^k and eps (and z), write x^{k+1};
+    with the multistep drift also x_{t-1} and eps_{t-1} once per window."""
     per = 4 * (3 + (1 if has_noise else 0))
-    return float(per) * wl.batch * wl.model.D * p_eff_sum
+    return float(wl.batch * wl.model.D) * (per * p_eff_sum + 8 * hist_sum)
+
+
+def sampler_name(wl) -> str:
+    if wl.schedule.kind == "ddpm":
+        return "ParaDDPM"
+    return {"euler": "ParaDDIM", "heun": "ParaDDIM (Heun)",
+            "dpm2m": "ParaDPMSolver (DPM-Solver++(2M))"}[getattr(wl.schedule, "solver", "euler")]
+
+
+def metric_name(wl) -> str:
+    """The headline metric's name; the other workloads state their own T and p."""
+    if wl.name == "latent_ddpm1000_p64":
+        return METRIC
+    return f"sample latency (ms) + denoiser evals/s at T={wl.schedule.T}, p={wl.p}; % HBM / MFMA peak"
+
+
+def denoiser_kernel(wl, dtype: str) -> str:
+    return {"conv1x1": f"k_conv_{dtype}", "mlp": "k_linear", "gmm2d": "k_gmm"}[wl.model.kind]
 
 
 KERNEL_SOURCES = {"k_conv": ["conv.hip"], "k_picard": ["picard.hip"], "k_linear": ["mlp.hip"],
@@ -263,11 +292,14 @@ def main() -> int:
     achieved = fl / (den_ms * 1e-3) if den_ms > 0 else 0.0
     has_noise = bool(np.any(sched.tables()["noise_std"] > 0))
     points = sum(window_points(st.trace, wl.p, wl.schedule.T) for st in stats)
-    ub = update_bytes(wl, points, has_noise)
+    hist = (sum(history_rows(st.trace, wl.schedule.T) for st in stats)
+            if getattr(wl.schedule, "solver", "euler") == "dpm2m" else 0)
+    ub = update_bytes(wl, points, has_noise, hist)
     upd_rate = ub / (upd_ms * 1e-3) if upd_ms > 0 else 0.0
-    traffic = traffic_from_profiles(wl.name, "k_conv_f32" if dtype == "f32" else "k_conv_bf16")
+    kname = denoiser_kernel(wl, dtype)
+    traffic = traffic_from_profiles(wl.name, kname)
     out = {
-        "metric": METRIC,
+        "metric": metric_name(wl),
         "value": value,
         "unit": "denoiser evals/s",
         "n_gpus": 1,
@@ -279,7 +311,7 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": dtype,
         "data": "synthetic (seeded Xavier weights, Philox noise; no trained model or dataset)",
-        "config": {"workload": wl.name, "sampler": "ParaDDPM" if wl.schedule.kind == "ddpm" else "ParaDDIM",
+        "config": {"workload": wl.name, "sampler": sampler_name(wl),
                    "T": wl.schedule.T, "p": wl.p, "tau": wl.tau, "batch": wl.batch,
                    "sample_shape": list(shape), "denoiser_width": wl.model.width,
                    "guidance": wl.model.guidance if wl.model.cond_dim else None,
@@ -289,7 +321,7 @@ def main() -> int:
         "evals_per_sample": [st.evals_per_sample for st in stats],
         "roofline": {"bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK[dtype] / 1e12,
                      "unit": "TFLOP/s", "frac": achieved / PEAK[dtype],
-                     "traffic": traffic, "kernel": f"k_conv_{dtype}",
+                     "traffic": traffic, "kernel": kname,
                      "flops_per_launch": fl / max(den_n, 1),
                      "mean_launch_ms": den_ms / max(den_n, 1), "launches": den_n},
         "roofline_update": {"bound": "hbm", "achieved": upd_rate / 1e9, "peak": HBM_PEAK / 1e9,

@@ -79,6 +79,20 @@ const char* pd_version(void);
  *     but the last is y_i = A_i x + (B_i / 2) (eps(x, n_i) + eps(x~, n_{i+1}));
  *     the last step (to abar = 1, no network timestep) keeps the DDIM drift.
  *     Two network evaluations per step, one for the last.
+ *   PD_DDIM_DPM2M: the PD_DDIM chain with eta = 0 (required), integrated with
+ *     the second-order multistep DPM-Solver++(2M) (Sec. 3.3 combines the
+ *     method with DPM-Solver; its multistep form reuses the previous step's
+ *     network output).  With alpha_n = sqrt(abar_n), sigma_n = sqrt(1-abar_n),
+ *     lambda_n = log(alpha_n/sigma_n), step i from n = n_i to n' = n - c with
+ *     h = lambda_n' - lambda_n and r = (lambda_n - lambda_{n+c}) / h:
+ *       y_i = A_i x + B_i eps(x, n_i) + R_i x_{i-1} + S_i eps(x_{i-1}, n_{i-1}),
+ *       A_i = sigma_n'/sigma_n - alpha_n' expm1(-h) (1 + 1/(2r)) / alpha_n - 1,
+ *       B_i = alpha_n' expm1(-h) (1 + 1/(2r)) sigma_n / alpha_n,
+ *       R_i = alpha_n' expm1(-h) / (2r alpha_{n+c}),  S_i = -R_i sigma_{n+c},
+ *     summed as ((A x + B eps) + R x_{i-1}) + S eps_{i-1}, for 1 <= i <= T-2;
+ *     the first step (no previous one) and the last (to abar = 1) keep the
+ *     DDIM drift (R = S = 0).  Picard evaluates the window's points plus
+ *     x_{t-1} (once t >= 1), so one network evaluation more per iteration.
  * Tables are computed in double precision and rounded once to float.
  * tol_index_offset selects which variance the stride test of Algorithm 1
  * uses for the point x_{t+j}: 0 = sigma^2_{t+j} (default), -1 = sigma^2_{t+j-1}.
@@ -86,15 +100,16 @@ const char* pd_version(void);
 #define PD_DDPM 0
 #define PD_DDIM 1
 #define PD_DDIM_HEUN 2
+#define PD_DDIM_DPM2M 3
 
 typedef struct pd_schedule_desc {
-    int32_t kind;              /* PD_DDPM, PD_DDIM or PD_DDIM_HEUN                 */
+    int32_t kind;              /* PD_DDPM, PD_DDIM, PD_DDIM_HEUN or PD_DDIM_DPM2M  */
     int32_t T_train;           /* length of the training chain, >= 2              */
     int32_t T;                 /* sampling steps; == T_train for DDPM             */
     int32_t tol_index_offset;  /* 0 or -1                                          */
     double beta_start;         /* 0 < beta_start <= beta_end < 1                   */
     double beta_end;
-    double eta;                /* DDIM only, in [0, 1]; 0 for PD_DDIM_HEUN         */
+    double eta;                /* DDIM only, in [0, 1]; 0 for HEUN and DPM2M       */
 } pd_schedule_desc;
 
 typedef struct pd_schedule pd_schedule;
@@ -109,6 +124,10 @@ void pd_destroy_schedule(pd_schedule* s);
  * the stride test), model_t (network timestep n_i).  Also returns T. */
 pd_status pd_schedule_tables(const pd_schedule* s, int32_t* T, float* A, float* B,
                              float* noise_std, float* tol_var, int32_t* model_t);
+/* Host copies of the length-T multistep coefficients R (of x_{i-1}) and S (of
+ * eps_{i-1}); all zero unless the kind is PD_DDIM_DPM2M.  Either pointer may
+ * be NULL. */
+pd_status pd_schedule_multistep_tables(const pd_schedule* s, float* R, float* S);
 
 /* ------------------------------------------------------------------ denoiser
  * The network of Algorithm 1's drift line, as an epsilon predictor
@@ -187,7 +206,8 @@ typedef struct pd_sample_stats {
     int32_t trace_cap;         /* capacity of stride_trace (in)                        */
     int64_t evals_per_sample;  /* network evaluations per sample, the paper's "model
                                   evaluations": the sum of window sizes (Heun: two
-                                  per window point, one for the last step)        */
+                                  per window point, one for the last step;
+                                  DPM2M: plus x_{t-1} once t >= 1)                */
     int64_t network_rows;      /* evals_per_sample * batch * (2 with guidance)         */
     int32_t* stride_trace;     /* optional host array: stride of each iteration        */
     int32_t time_kernels;      /* in: nonzero = bracket every denoiser, update and     */

@@ -22,20 +22,20 @@ __all__ = [
     "PdError", "load", "lib_path", "Schedule", "Denoiser", "Workspace", "SampleStats",
     "pd_init_schedule", "pd_denoiser_create", "pd_denoiser_forward", "pd_normals",
     "pd_workspace_create", "pd_sample_sequential", "pd_sample_picard",
-    "PD_DDPM", "PD_DDIM", "PD_MODEL_GMM2D", "PD_MODEL_MLP", "PD_MODEL_CONV1X1",
+    "PD_DDPM", "PD_DDIM", "PD_DDIM_HEUN", "PD_DDIM_DPM2M", "PD_MODEL_GMM2D", "PD_MODEL_MLP", "PD_MODEL_CONV1X1",
     "PD_F32", "PD_BF16", "EXPORTED_SYMBOLS",
 ]
 
 PD_OK, PD_ERR_INVALID_ARG, PD_ERR_OOM, PD_ERR_DEVICE, PD_ERR_NUMERIC, PD_ERR_UNSUPPORTED = range(6)
 STATUS_NAMES = {0: "PD_OK", 1: "PD_ERR_INVALID_ARG", 2: "PD_ERR_OOM", 3: "PD_ERR_DEVICE",
                 4: "PD_ERR_NUMERIC", 5: "PD_ERR_UNSUPPORTED"}
-PD_DDPM, PD_DDIM, PD_DDIM_HEUN = 0, 1, 2
+PD_DDPM, PD_DDIM, PD_DDIM_HEUN, PD_DDIM_DPM2M = 0, 1, 2, 3
 PD_MODEL_GMM2D, PD_MODEL_MLP, PD_MODEL_CONV1X1 = 0, 1, 2
 PD_F32, PD_BF16 = 0, 1
 
 EXPORTED_SYMBOLS = [
     "pd_last_error", "pd_version", "pd_init_schedule", "pd_destroy_schedule",
-    "pd_schedule_tables", "pd_denoiser_create", "pd_denoiser_destroy", "pd_denoiser_forward",
+    "pd_schedule_tables", "pd_schedule_multistep_tables", "pd_denoiser_create", "pd_denoiser_destroy", "pd_denoiser_forward",
     "pd_normals", "pd_workspace_create", "pd_workspace_destroy", "pd_sample_sequential",
     "pd_sample_picard",
 ]
@@ -94,6 +94,7 @@ def load() -> ctypes.CDLL:
         "pd_init_schedule": ([P(_ScheduleDesc), P(vp)], i32),
         "pd_destroy_schedule": ([vp], None),
         "pd_schedule_tables": ([vp, P(i32), P(f32), P(f32), P(f32), P(f32), P(i32)], i32),
+        "pd_schedule_multistep_tables": ([vp, P(f32), P(f32)], i32),
         "pd_denoiser_create": ([P(_ModelDesc), P(i64), i32, P(P(f32)), i32, vp, P(vp)], i32),
         "pd_denoiser_destroy": ([vp], None),
         "pd_denoiser_forward": ([vp, vp, vp, i64, vp, vp], i32),
@@ -152,7 +153,9 @@ class Schedule:
         fp = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
         _check(load().pd_schedule_tables(self._h, ctypes.byref(Tout), fp(A), fp(B), fp(zs), fp(tv),
                                           nt.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))))
-        return {"A": A, "B": B, "noise_std": zs, "tol_var": tv, "model_t": nt}
+        R, S = np.empty(T, np.float32), np.empty(T, np.float32)
+        _check(load().pd_schedule_multistep_tables(self._h, fp(R), fp(S)))
+        return {"A": A, "B": B, "noise_std": zs, "tol_var": tv, "model_t": nt, "R": R, "S": S}
 
     def __del__(self):
         if getattr(self, "_h", None) and _LIB is not None:
@@ -314,7 +317,8 @@ def from_workload(w, weights: Dict[str, np.ndarray], tol_index_offset: int = 0):
     if s.kind == "ddpm":
         kind = PD_DDPM
     else:
-        kind = PD_DDIM_HEUN if getattr(s, "solver", "euler") == "heun" else PD_DDIM
+        kind = {"euler": PD_DDIM, "heun": PD_DDIM_HEUN,
+                "dpm2m": PD_DDIM_DPM2M}[getattr(s, "solver", "euler")]
     sched = pd_init_schedule(kind, s.T_train, s.T, s.beta_start, s.beta_end, s.eta,
                              tol_index_offset)
     m = w.model

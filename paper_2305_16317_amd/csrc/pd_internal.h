@@ -45,7 +45,9 @@ struct LoopState {
     int32_t p_eff;   // size of the current window; 0 once t >= T or after an error
     int32_t status;  // PD_OK or PD_ERR_NUMERIC
     int32_t first_stride;  // stride of iteration 0 (the window of copies of x_0)
-    int64_t evals;   // sum of window sizes
+    int32_t nrows;   // rows of the next denoiser batch: p_eff, plus one history
+                     // row (the point before the window) for the multistep drift
+    int64_t evals;   // network evaluations per sample
 };
 
 // ---------------------------------------------------------------- kernels
@@ -133,6 +135,8 @@ void launch_heun_combine(const LoopState* st, float* eps, const float* eps2, int
 void launch_seq_heun_predict(const float* x, const float* eps, float A, float B, int64_t n,
                              float* xt, hipStream_t s);
 void launch_seq_heun_combine(float* eps, const float* eps2, int64_t n, hipStream_t s);
+void launch_seq_step_dpm(float* x, const float* eps, float* xp, float* ep, float P, float Q, float R,
+                         float S, bool second, int64_t n, hipStream_t s);
 int picard_partial_blocks(int64_t D);
 // Everything the stride rule and the slide need (the finalize step).
 struct FinalizeArgs {
@@ -150,12 +154,17 @@ struct FinalizeArgs {
     int32_t* nrow;
     const int32_t* model_t_next;   // Heun only, else nullptr
     int32_t* nrow2;                // Heun only, else nullptr
+    int32_t ring_slots;            // p + 1, or p + 2 with a history row
+    int32_t history;               // 1: the next batch starts with x_{t-1} (multistep drift)
 };
 // Scan + error partials of one iteration.  Returns true when the grid is a
 // single block, which then also ran the finalize step.
+// R, S: the multistep (DPM-Solver) coefficients of x_{i-1} and eps_{i-1}, or
+// nullptr; eps then has the history row first when st->nrows > st->p_eff.
 bool launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
-                        const float* A, const float* B, int p, int batch, int64_t D,
-                        float* partials, const FinalizeArgs& fin, hipStream_t s);
+                        const float* A, const float* B, const float* R, const float* S, int p,
+                        int batch, int64_t D, float* partials, const FinalizeArgs& fin,
+                        hipStream_t s);
 void launch_picard_finalize(const FinalizeArgs& fin, hipStream_t s);
 void launch_seq_step(float* x, const float* eps, const float* z, float A, float B, int64_t n,
                      hipStream_t s);

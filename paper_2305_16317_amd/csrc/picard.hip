@@ -83,6 +83,7 @@ __global__ void k_picard_init(LoopState* st, int32_t* slot, int32_t* nrow,
         st->p_eff = pe;
         st->status = PD_OK;
         st->first_stride = 0;
+        st->nrows = pe;
         st->evals = 0;
     }
     for (int j = threadIdx.x; j < pe; j += blockDim.x) {
@@ -136,7 +137,7 @@ __device__ void finalize_body(const FinalizeArgs& a, int nblk) {
     LoopState* st = a.st;
     const int pe = st->p_eff;
     if (pe <= 0) return;
-    const int t = st->t, k = st->k, p = a.p, T = a.T;
+    const int t = st->t, k = st->k, p = a.p, T = a.T, rows_now = st->nrows;
     __shared__ int s_stride, s_bad;
     if (threadIdx.x == 0) {
         s_stride = pe;
@@ -181,17 +182,28 @@ __device__ void finalize_body(const FinalizeArgs& a, int nblk) {
         a.trace[k] = stride;
         if (k == 0) st->first_stride = stride;
         st->k = k + 1;
-        // network evaluations: Heun evaluates twice per point but the last step
-        st->evals += a.nrow2 ? 2 * pe - (t + pe == T ? 1 : 0) : pe;
+        // network evaluations: Heun evaluates twice per point but the last
+        // step; with a history row the batch had one row more than the window
+        st->evals += a.nrow2 ? 2 * pe - (t + pe == T ? 1 : 0) : rows_now;
         st->f = fn;
         st->t = s_bad ? T : tn;
         st->p_eff = pn > 0 ? pn : 0;
         if (s_bad) st->status = PD_ERR_NUMERIC;
     }
+    // next batch: [the point before the window, for the multistep drift] then
+    // the window's points
+    const int hn = (a.history && tn >= 1 && pn > 0) ? 1 : 0;
+    if (threadIdx.x == 0) {
+        st->nrows = pn > 0 ? pn + hn : 0;
+        if (hn) {
+            a.slot[0] = (tn - 1) % a.ring_slots;     // tn - 1 < fn: a computed point
+            a.nrow[0] = a.model_t[tn - 1];
+        }
+    }
     for (int j = threadIdx.x; j < pn; j += blockDim.x) {
         const int m = tn + j;
-        a.slot[j] = (m < fn ? m : fn) % (p + 1);
-        a.nrow[j] = a.model_t[m];
+        a.slot[hn + j] = (m < fn ? m : fn) % a.ring_slots;
+        a.nrow[hn + j] = a.model_t[m];
         if (a.nrow2) a.nrow2[j] = a.model_t_next[m];
     }
 }
@@ -212,11 +224,12 @@ __global__ __launch_bounds__(1024) void k_picard_finalize(FinalizeArgs a, int nb
 // offset into per-block partial sums partials[b][o][blk]; offset 0 (never
 // tested) carries the count of non-finite points in the window's last row
 // (a non-finite point in any other row makes its error non-finite).
-template <int R, int VEC, bool NOISE>
+template <int R, int VEC, bool NOISE, bool DPM>
 __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     const LoopState* __restrict__ st, float* ring, const float* __restrict__ eps,
     const float* __restrict__ noise, const float* __restrict__ Atab,
-    const float* __restrict__ Btab, int p, int batch, int64_t D, float* __restrict__ partials,
+    const float* __restrict__ Btab, const float* __restrict__ Rtab,
+    const float* __restrict__ Stab, int p, int batch, int64_t D, float* __restrict__ partials,
     FinalizeArgs fin, int fuse_finalize) {
     typedef typename Cols<VEC>::type V;
     constexpr int NW = kScanWaves;
@@ -231,7 +244,9 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     const bool valid = d < D;
     const int64_t slotsz = (int64_t)batch * D;
     const int64_t col = (int64_t)b * D + (valid ? d : 0);
-    const int P1 = p + 1;
+    const int P1 = fin.ring_slots;
+    // DPM-Solver: eps row 0 holds the point before the window (once t >= 1)
+    const int hist = DPM ? st->nrows - pe : 0;
     const int ch = (pe + NW - 1) / NW;
     const int j0 = min(w * ch, pe), j1 = min(j0 + ch, pe);
     const int nr = j1 - j0;
@@ -252,6 +267,15 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     const int slot_f = f % P1;
     const int jt = min(j0 + (lane < R ? lane : R - 1), pe - 1);   // lane r: row j0 + r
     const float ta = Atab[t + jt], tb = Btab[t + jt];
+    float tr = 0.f, ts = 0.f;
+    V xp = V(0.f), ep = V(0.f);   // DPM-Solver: x and eps of the step before row j0
+    if constexpr (DPM) {
+        tr = Rtab[t + jt];
+        ts = Stab[t + jt];
+        const int mp = max(t + j0 - 1, 0);           // clamped (step 0 is first order)
+        xp = *reinterpret_cast<const V*>(ring + (int64_t)(mp <= f ? mp % P1 : slot_f) * slotsz + col);
+        ep = *reinterpret_cast<const V*>(eps + (int64_t)max(j0 - 1 + hist, 0) * slotsz + col);
+    }
     V xo[R], y[R], z[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -259,7 +283,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
         const int m = t + j;
         const int sl = m <= f ? m % P1 : slot_f;      // points past f equal x_f
         xo[r] = *reinterpret_cast<const V*>(ring + (int64_t)sl * slotsz + col);
-        y[r] = *reinterpret_cast<const V*>(eps + (int64_t)j * slotsz + col);
+        y[r] = *reinterpret_cast<const V*>(eps + (int64_t)(j + hist) * slotsz + col);
         if constexpr (NOISE) z[r] = *reinterpret_cast<const V*>(noise + (int64_t)m * slotsz + col);
         else z[r] = V(0.f);
     }
@@ -270,9 +294,23 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
         const float ca = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ta), r));
         const float cb = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, tb), r));
         const bool in = r < nr;
+        float cr = 0.f, cs = 0.f;
+        if constexpr (DPM) {
+            cr = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, tr), r));
+            cs = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ts), r));
+        }
 #pragma unroll
         for (int c = 0; c < VEC; ++c) {
-            const float v = drift(ca, col_at<VEC>(xo[r], c), cb, col_at<VEC>(y[r], c));
+            const float e = col_at<VEC>(y[r], c);
+            float v = drift(ca, col_at<VEC>(xo[r], c), cb, e);
+            if constexpr (DPM) {
+                // second-order steps add R x_{m-1} + S eps_{m-1}, in that order
+                const float v2 = __fadd_rn(__fadd_rn(v, __fmul_rn(cr, col_at<VEC>(xp, c))),
+                                           __fmul_rn(cs, col_at<VEC>(ep, c)));
+                v = cr != 0.f ? v2 : v;
+                col_at<VEC>(xp, c) = col_at<VEC>(xo[r], c);
+                col_at<VEC>(ep, c) = e;
+            }
             col_at<VEC>(y[r], c) = in ? v : 0.f;
             if (!in) col_at<VEC>(z[r], c) = 0.f;
             col_at<VEC>(acc_y, c) = __fadd_rn(col_at<VEC>(acc_y, c), col_at<VEC>(y[r], c));
@@ -364,6 +402,23 @@ __global__ __launch_bounds__(256) void k_seq_heun_combine(float* __restrict__ ep
     eps[i] = __fmul_rn(__fadd_rn(eps[i], eps2[i]), 0.5f);
 }
 
+// DPM-Solver, sequential side: x <- x + (((P x + Q eps) + R xp) + S ep) on a
+// second-order step (else the first-order drift), then (xp, ep) <- (x, eps).
+__global__ __launch_bounds__(256) void k_seq_step_dpm(float* __restrict__ x,
+                                                      const float* __restrict__ eps,
+                                                      float* __restrict__ xp,
+                                                      float* __restrict__ ep, float P, float Q,
+                                                      float R, float S, int second, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const float xi = x[i], ei = eps[i];
+    float y = drift(P, xi, Q, ei);
+    if (second) y = __fadd_rn(__fadd_rn(y, __fmul_rn(R, xp[i])), __fmul_rn(S, ep[i]));
+    x[i] = __fadd_rn(xi, y);
+    xp[i] = xi;
+    ep[i] = ei;
+}
+
 __global__ __launch_bounds__(256) void k_seq_step(float* __restrict__ x,
                                                   const float* __restrict__ eps,
                                                   const float* __restrict__ z, float A, float B,
@@ -417,6 +472,14 @@ void launch_seq_heun_predict(const float* x, const float* eps, float A, float B,
     PD_HIP(hipGetLastError());
 }
 
+void launch_seq_step_dpm(float* x, const float* eps, float* xp, float* ep, float P, float Q, float R,
+                         float S, bool second, int64_t n, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_seq_step_dpm, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, x, eps, xp,
+                       ep, P, Q, R, S, (int)second, n);
+    PD_HIP(hipGetLastError());
+}
+
 void launch_seq_heun_combine(float* eps, const float* eps2, int64_t n, hipStream_t s) {
     if (n <= 0) return;
     hipLaunchKernelGGL(k_seq_heun_combine, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, eps,
@@ -426,30 +489,39 @@ void launch_seq_heun_combine(float* eps, const float* eps2, int64_t n, hipStream
 
 template <int R, int VEC>
 static bool launch_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
-                        const float* A, const float* B, int p, int batch, int64_t D,
-                        float* partials, const FinalizeArgs& fin, hipStream_t s) {
+                        const float* A, const float* B, const float* Rt, const float* St, int p,
+                        int batch, int64_t D, float* partials, const FinalizeArgs& fin,
+                        hipStream_t s) {
     const dim3 grid((unsigned)picard_partial_blocks(D), (unsigned)batch);
     const int fuse = grid.x * grid.y == 1;
-    if (noise)
-        hipLaunchKernelGGL((k_picard_scan<R, VEC, true>), grid, dim3(kScanWaves * 64), 0, s, st,
-                           ring, eps, noise, A, B, p, batch, D, partials, fin, fuse);
+    const dim3 block(kScanWaves * 64);
+    if (Rt)      // DPM-Solver integrates the noise-free chain
+        hipLaunchKernelGGL((k_picard_scan<R, VEC, false, true>), grid, block, 0, s, st, ring, eps,
+                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse);
+    else if (noise)
+        hipLaunchKernelGGL((k_picard_scan<R, VEC, true, false>), grid, block, 0, s, st, ring, eps,
+                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse);
     else
-        hipLaunchKernelGGL((k_picard_scan<R, VEC, false>), grid, dim3(kScanWaves * 64), 0, s, st,
-                           ring, eps, noise, A, B, p, batch, D, partials, fin, fuse);
+        hipLaunchKernelGGL((k_picard_scan<R, VEC, false, false>), grid, block, 0, s, st, ring, eps,
+                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse);
     PD_HIP(hipGetLastError());
     return fuse != 0;
 }
 
 bool launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
-                        const float* A, const float* B, int p, int batch, int64_t D,
-                        float* partials, const FinalizeArgs& fin, hipStream_t s) {
+                        const float* A, const float* B, const float* R, const float* S, int p,
+                        int batch, int64_t D, float* partials, const FinalizeArgs& fin,
+                        hipStream_t s) {
     if (p > kMaxWindow) fail(PD_ERR_UNSUPPORTED, "window larger than 128 points");
+    if (R && noise) fail(PD_ERR_INVALID_ARG, "the multistep drift is for the noise-free chain");
     const int ch = (p + kScanWaves - 1) / kScanWaves;    // rows per wave at a full window
     const bool v4 = scan_vec(D) == 4;
-#define PD_SCAN(R)                                                                              \
-    if (ch <= R)                                                                                \
-        return v4 ? launch_scan<R, 4>(st, ring, eps, noise, A, B, p, batch, D, partials, fin, s) \
-                  : launch_scan<R, 1>(st, ring, eps, noise, A, B, p, batch, D, partials, fin, s);
+#define PD_SCAN(RR)                                                                             \
+    if (ch <= RR)                                                                               \
+        return v4 ? launch_scan<RR, 4>(st, ring, eps, noise, A, B, R, S, p, batch, D, partials,  \
+                                       fin, s)                                                   \
+                  : launch_scan<RR, 1>(st, ring, eps, noise, A, B, R, S, p, batch, D, partials,  \
+                                       fin, s);
     PD_SCAN(1) PD_SCAN(2) PD_SCAN(4) PD_SCAN(8)
 #undef PD_SCAN
     return false;

@@ -159,9 +159,11 @@ struct pd_schedule {
     std::vector<float> A, B, noise_std, tol_var;
     std::vector<int32_t> model_t;
     std::vector<int32_t> model_t_next;   // n_{i+1}; the last step repeats n_{T-1}
+    std::vector<float> R, S;   // multistep coefficients of x_{i-1}, eps_{i-1} (zero: first order)
     std::vector<double> alphabar;
     bool has_noise = false;
     bool heun = false;
+    bool dpm = false;          // the drift also reads the previous step (DPM-Solver++(2M))
 };
 
 static void build_tables(pd_schedule& s) {
@@ -184,8 +186,11 @@ static void build_tables(pd_schedule& s) {
     s.tol_var.resize(T);
     s.model_t.resize(T);
     s.model_t_next.resize(T);
+    s.R.assign(T, 0.f);
+    s.S.assign(T, 0.f);
     s.has_noise = false;
     s.heun = d.kind == PD_DDIM_HEUN;
+    s.dpm = d.kind == PD_DDIM_DPM2M;
     for (int i = 0; i < T; ++i) {
         double A, B, var, tol;
         int n;
@@ -217,6 +222,33 @@ static void build_tables(pd_schedule& s) {
         s.tol_var[i] = (float)tol;
         if (var > 0.0) s.has_noise = true;
     }
+    if (s.dpm) {
+        // DPM-Solver++(2M) in the data-prediction form x0 = (x - sigma eps)/alpha,
+        // with alpha_n = sqrt(abar_n), sigma_n = sqrt(1 - abar_n), lambda = log(alpha/sigma).
+        // Step i goes from n = n_i to n - c with h = lambda(n - c) - lambda(n); the
+        // previous step's data prediction (from n + c) enters through
+        // r = (lambda(n) - lambda(n + c)) / h:
+        //   x' = (sigma'/sigma) x - alpha' expm1(-h) ((1 + 1/(2r)) x0 - x0_prev/(2r)).
+        // Written as x' - x = P x + Q eps + R x_prev + S eps_prev (A, B hold P, Q).
+        // The first step has no previous one and the last (to abar = 1) is
+        // taken to first order: both keep the DDIM drift.
+        const int c = Tt / T;
+        auto alpha = [&](int n) { return std::sqrt(ab[n]); };
+        auto sigma = [&](int n) { return std::sqrt(1.0 - ab[n]); };
+        auto lambda = [&](int n) { return std::log(alpha(n) / sigma(n)); };
+        for (int i = 1; i + 1 < T; ++i) {
+            const int n = s.model_t[i], nn = n - c, np = n + c;
+            const double h = lambda(nn) - lambda(n);
+            const double r = (lambda(n) - lambda(np)) / h;
+            const double em = std::expm1(-h);
+            const double w_cur = 1.0 + 1.0 / (2.0 * r), w_prev = 1.0 / (2.0 * r);
+            s.A[i] = (float)(sigma(nn) / sigma(n) - alpha(nn) * em * w_cur / alpha(n) - 1.0);
+            s.B[i] = (float)(alpha(nn) * em * w_cur * sigma(n) / alpha(n));
+            const double Rc = alpha(nn) * em * w_prev / alpha(np);
+            s.R[i] = (float)Rc;
+            s.S[i] = (float)(-Rc * sigma(np));
+        }
+    }
     // the step after i; the last step has none and keeps its Euler drift, so
     // its (unused) second evaluation is pointed at a valid timestep
     for (int i = 0; i < T; ++i) s.model_t_next[i] = s.model_t[i + 1 < T ? i + 1 : i];
@@ -227,8 +259,9 @@ extern "C" pd_status pd_init_schedule(const pd_schedule_desc* desc, pd_schedule*
         require(desc != nullptr && out != nullptr, "desc and out must not be NULL");
         *out = nullptr;
         const pd_schedule_desc& d = *desc;
-        require(d.kind == PD_DDPM || d.kind == PD_DDIM || d.kind == PD_DDIM_HEUN,
-                "kind must be PD_DDPM, PD_DDIM or PD_DDIM_HEUN");
+        require(d.kind == PD_DDPM || d.kind == PD_DDIM || d.kind == PD_DDIM_HEUN ||
+                    d.kind == PD_DDIM_DPM2M,
+                "kind must be PD_DDPM, PD_DDIM, PD_DDIM_HEUN or PD_DDIM_DPM2M");
         require(d.T_train >= 2, "T_train must be >= 2");
         require(d.T >= 1 && d.T <= d.T_train, "T must be in [1, T_train]");
         require(d.kind != PD_DDPM || d.T == d.T_train, "DDPM needs T == T_train");
@@ -238,6 +271,8 @@ extern "C" pd_status pd_init_schedule(const pd_schedule_desc* desc, pd_schedule*
                 "need 0 < beta_start <= beta_end < 1");
         require(d.kind != PD_DDIM || (d.eta >= 0.0 && d.eta <= 1.0), "eta must be in [0, 1]");
         require(d.kind != PD_DDIM_HEUN || d.eta == 0.0, "Heun integrates the eta = 0 (ODE) chain only");
+        require(d.kind != PD_DDIM_DPM2M || d.eta == 0.0,
+                "DPM-Solver integrates the eta = 0 (ODE) chain only");
         require(d.tol_index_offset == 0 || d.tol_index_offset == -1,
                 "tol_index_offset must be 0 or -1");
         auto s = std::make_unique<pd_schedule>();
@@ -261,6 +296,15 @@ extern "C" pd_status pd_schedule_tables(const pd_schedule* s, int32_t* T, float*
         if (noise_std) std::memcpy(noise_std, s->noise_std.data(), n * sizeof(float));
         if (tol_var) std::memcpy(tol_var, s->tol_var.data(), n * sizeof(float));
         if (model_t) std::memcpy(model_t, s->model_t.data(), n * sizeof(int32_t));
+    });
+}
+
+extern "C" pd_status pd_schedule_multistep_tables(const pd_schedule* s, float* R, float* S) {
+    return guard([&] {
+        require(s != nullptr, "schedule must not be NULL");
+        const size_t n = (size_t)s->T;
+        if (R) std::memcpy(R, s->R.data(), n * sizeof(float));
+        if (S) std::memcpy(S, s->S.data(), n * sizeof(float));
     });
 }
 
@@ -484,6 +528,8 @@ struct pd_workspace {
     int64_t D = 0;
     DevBuf ring, eps, noise, A, B, zstd, tolv, model_t, state, trace, slot, nrow, partials, scratch;
     DevBuf xt, eps2, model_t_next, nrow2;   // Heun: predictions, second epsilons, n_{i+1}
+    DevBuf Rt, St, xprev, eprev;            // multistep: tables; the sequential loop's last step
+    int ring_slots() const { return p + 1 + (s->dpm ? 1 : 0); }
     LoopState* h_state = nullptr;
     ~pd_workspace() {
         if (h_state) (void)hipHostFree(h_state);
@@ -502,8 +548,10 @@ static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, 
     w.T = s.T;
     w.D = d.D;
     const int64_t BD = (int64_t)batch * d.D;
-    w.ring.alloc(sizeof(float) * (size_t)(p + 1) * BD);
-    w.eps.alloc(sizeof(float) * (size_t)p * BD);
+    // multistep: the ring also keeps x_{t-1}, and the batch starts with it
+    const int hist = s.dpm ? 1 : 0;
+    w.ring.alloc(sizeof(float) * (size_t)(p + 1 + hist) * BD);
+    w.eps.alloc(sizeof(float) * (size_t)(p + hist) * BD);
     if (s.has_noise) w.noise.alloc(sizeof(float) * (size_t)s.T * BD);
     w.A.upload(s.A.data(), s.T);
     w.B.upload(s.B.data(), s.T);
@@ -512,8 +560,8 @@ static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, 
     w.model_t.upload(s.model_t.data(), s.T);
     w.state.alloc(sizeof(LoopState));
     w.trace.alloc(sizeof(int32_t) * (size_t)s.T);
-    w.slot.alloc(sizeof(int32_t) * (size_t)p);
-    w.nrow.alloc(sizeof(int32_t) * (size_t)p);
+    w.slot.alloc(sizeof(int32_t) * (size_t)(p + hist));
+    w.nrow.alloc(sizeof(int32_t) * (size_t)(p + hist));
     w.partials.alloc(sizeof(float) * (size_t)picard_partial_blocks(d.D) * p * batch);
     if (s.heun) {
         w.xt.alloc(sizeof(float) * (size_t)p * BD);
@@ -521,7 +569,13 @@ static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, 
         w.model_t_next.upload(s.model_t_next.data(), s.T);
         w.nrow2.alloc(sizeof(int32_t) * (size_t)p);
     }
-    const size_t sc = d.scratch_floats((int64_t)p * batch);
+    if (s.dpm) {
+        w.Rt.upload(s.R.data(), s.T);
+        w.St.upload(s.S.data(), s.T);
+        w.xprev.alloc(sizeof(float) * (size_t)BD);
+        w.eprev.alloc(sizeof(float) * (size_t)BD);
+    }
+    const size_t sc = d.scratch_floats((int64_t)(p + hist) * batch);
     if (sc) w.scratch.alloc(sc * sizeof(float));
     PD_HIP(hipHostMalloc(reinterpret_cast<void**>(&w.h_state), sizeof(LoopState), hipHostMallocDefault));
 }
@@ -602,7 +656,7 @@ static constexpr size_t kFusedLoopLds = 64 * 1024;
 
 static bool use_fused_gmm_loop(const pd_schedule& s, const pd_denoiser& d, int T, int p,
                                int batch) {
-    return d.desc.kind == PD_MODEL_GMM2D && !s.heun &&
+    return d.desc.kind == PD_MODEL_GMM2D && !s.heun && !s.dpm &&
            gmm_loop_lds_bytes(T, d.desc.n_components, p, batch) <= kFusedLoopLds;
 }
 
@@ -669,8 +723,13 @@ extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoise
                 ++evals;
             }
             tm.mark(CAT_DENOISER);
-            const float* z = w.noise.p ? w.noise.as<float>() + (int64_t)i * BD : nullptr;
-            launch_seq_step(x, w.eps.as<float>(), z, s->A[i], s->B[i], BD, st);
+            if (s->dpm) {
+                launch_seq_step_dpm(x, w.eps.as<float>(), w.xprev.as<float>(), w.eprev.as<float>(),
+                                    s->A[i], s->B[i], s->R[i], s->S[i], s->R[i] != 0.f, BD, st);
+            } else {
+                const float* z = w.noise.p ? w.noise.as<float>() + (int64_t)i * BD : nullptr;
+                launch_seq_step(x, w.eps.as<float>(), z, s->A[i], s->B[i], BD, st);
+            }
             tm.mark(CAT_UPDATE);
         }
         PD_HIP(hipMemcpyAsync(x_out, x, sizeof(float) * BD, hipMemcpyDeviceToDevice, st));
@@ -724,12 +783,14 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         launch_picard_init(dst, w.slot.as<int32_t>(), w.nrow.as<int32_t>(),
                            w.model_t.as<int32_t>(), mtn, nrow2, T, pc, st);
         const RowSrc src2{w.xt.as<float>(), nullptr, BD, batch, pc, nrow2, &dst->p_eff};
+        const int hist = s->dpm ? 1 : 0;     // the multistep drift's row x_{t-1}
+        const int slots = pc + 1 + hist;
         const FinalizeArgs fin{dst, w.partials.as<float>(), pc, batch, d->D, T, w.tolv.as<float>(),
                                tau2, s->desc.tol_index_offset, w.model_t.as<int32_t>(),
                                w.trace.as<int32_t>(), w.slot.as<int32_t>(), w.nrow.as<int32_t>(),
-                               mtn, nrow2};
+                               mtn, nrow2, slots, hist};
         const RowSrc src{w.ring.as<float>(), w.slot.as<int32_t>(), BD,     batch,
-                         pc,                 w.nrow.as<int32_t>(), &dst->p_eff};
+                         pc + hist,          w.nrow.as<int32_t>(), &dst->nrows};
         int t_host = 0, k_host = 0, issued = 0;
         for (;;) {
             // every iteration advances t by at most pc, so at least this many
@@ -762,7 +823,8 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                 tm.mark(CAT_DENOISER);
                 const bool fused = launch_picard_scan(dst, w.ring.as<float>(), w.eps.as<float>(),
                                                       w.noise.as<float>(), w.A.as<float>(),
-                                                      w.B.as<float>(), pc, batch, d->D,
+                                                      w.B.as<float>(), w.Rt.as<float>(),
+                                                      w.St.as<float>(), pc, batch, d->D,
                                                       w.partials.as<float>(), fin, st);
                 tm.mark(CAT_UPDATE);
                 if (!fused) {
@@ -781,7 +843,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         }
         const int iters = w.h_state->k;
         const int64_t evals = w.h_state->evals;
-        const float* xT = w.ring.as<float>() + (int64_t)(T % (pc + 1)) * BD;
+        const float* xT = w.ring.as<float>() + (int64_t)(T % slots) * BD;
         PD_HIP(hipMemcpyAsync(x_out, xT, sizeof(float) * BD, hipMemcpyDeviceToDevice, st));
         PD_HIP(hipStreamSynchronize(st));
         tm.collect();

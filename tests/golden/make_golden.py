@@ -27,7 +27,8 @@ import workloads as W  # noqa: E402
 from oracle import Problem  # noqa: E402
 
 N_SAMPLE = 4096
-SEQUENTIAL = {"gmm2d_ddpm100", "policy_mlp_ddpm100", "latent_ddpm1000_p64"}
+SEQUENTIAL = {"gmm2d_ddpm100", "policy_mlp_ddpm100", "latent_ddpm1000_p64",
+              "policy_mlp_dpm15", "latent_dpm200_p64"}
 
 
 def sample_indices(n: int) -> np.ndarray:

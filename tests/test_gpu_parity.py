@@ -310,7 +310,8 @@ def _check_summary(got, g, tol):
 
 
 @pytest.mark.parametrize("name", ["gmm2d_ddpm100", "policy_mlp_ddpm100", "latent_ddpm1000_p64",
-                                  "latent_ddim200_b4", "policy_mlp_heun20", "latent_heun100_p32"])
+                                  "latent_ddim200_b4", "policy_mlp_heun20", "latent_heun100_p32",
+                                  "policy_mlp_dpm15", "latent_dpm200_p64"])
 def test_full_size_picard_matches_oracle(name):
     g = _golden(name)
     wl = W.WORKLOADS[name]
@@ -320,7 +321,8 @@ def test_full_size_picard_matches_oracle(name):
     _check_summary(got, gp, REL_F32)
 
 
-@pytest.mark.parametrize("name", ["gmm2d_ddpm100", "policy_mlp_ddpm100", "latent_ddpm1000_p64"])
+@pytest.mark.parametrize("name", ["gmm2d_ddpm100", "policy_mlp_ddpm100", "latent_ddpm1000_p64",
+                                  "policy_mlp_dpm15", "latent_dpm200_p64"])
 def test_full_size_sequential_matches_oracle(name):
     g = _golden(name)
     wl = W.WORKLOADS[name]
@@ -376,6 +378,59 @@ def test_heun_sequential_matches_oracle_and_window_of_one(name):
     seq, st = _run(wl, w, "sequential")
     T = wl.schedule.T
     assert st.evals_per_sample == 2 * T - 1
+    assert _rel(seq, Problem(wl, w, np.float32).sequential()) <= REL_F32
+    one, st1 = _run(wl, w, "picard", p=1)
+    assert st1.iters == T and st1.evals_per_sample == 2 * T - 1
+    assert np.array_equal(one.view(np.uint32), seq.view(np.uint32))
+
+
+# ------------------------------------------- DPM-Solver++(2M) (ParaDPMSolver)
+def _dpm(model, T, p, batch, tau=0.05, seed=0, T_train=None):
+    return W.Workload("dpm", W.ScheduleSpec("ddim", T_train or 10 * T, T, solver="dpm2m"), model,
+                      p=p, tau=tau, batch=batch, noise_seed=seed)
+
+
+DPM = {
+    # two columns: the scan's one-column-per-lane layout (the mixture's fused
+    # loop is Euler only, so this runs the general kernels)
+    "dpm_gmm": lambda: _dpm(W.ModelSpec("gmm2d", (2,)), 40, 12, 2),
+    "dpm_mlp": lambda: _dpm(W.ModelSpec("mlp", (4, 5), width=32), 30, 9, 2),
+    "dpm_conv": lambda: _dpm(W.ModelSpec("conv1x1", (4, 6, 7), width=32), 24, 8, 3),
+    # several scan blocks per sample (finalize runs as its own launch)
+    "dpm_conv_blocks": lambda: _dpm(W.ModelSpec("conv1x1", (4, 16, 17), width=32), 20, 7, 1),
+    # 40-point window: waves hold 4 rows each, so the step before a wave's
+    # first row sits in the previous wave's chunk
+    "dpm_mlp_wide": lambda: _dpm(W.ModelSpec("mlp", (4, 3), width=32), 60, 40, 2, tau=0.1),
+    "dpm_conv_full_window": lambda: _dpm(W.ModelSpec("conv1x1", (4, 8, 8), width=64), 16, 16, 1),
+    # whole-window slides (x_{t-1} is the previous window's last point) and
+    # single-point slides
+    "dpm_mlp_tau_inf": lambda: _dpm(W.ModelSpec("mlp", (4, 3), width=32), 25, 6, 2,
+                                    tau=float("inf")),
+    "dpm_mlp_tau0": lambda: _dpm(W.ModelSpec("mlp", (4, 3), width=32), 12, 5, 1, tau=0.0),
+}
+
+
+@pytest.mark.parametrize("name", list(DPM))
+def test_dpm_picard_matches_oracle(name):
+    wl = DPM[name]()
+    w = W.make_weights(wl.model)
+    got, st = _run(wl, w)
+    ref = Problem(wl, w, np.float32).picard()
+    assert (st.iters, st.trace, st.evals_per_sample) == (ref.iters, ref.trace, ref.evals)
+    assert st.network_rows == ref.evals * wl.batch
+    assert _rel(got, ref.x) <= REL_F32, _rel(got, ref.x)
+
+
+@pytest.mark.parametrize("name", ["dpm_gmm", "dpm_mlp", "dpm_conv"])
+def test_dpm_sequential_matches_oracle_and_window_of_one(name):
+    """The sequential multistep loop against the oracle; Picard with p = 1
+    re-evaluates x_{t-1} each step (T - 1 extra evaluations) and must give the
+    sequential sample bit for bit."""
+    wl = DPM[name]()
+    w = W.make_weights(wl.model)
+    seq, st = _run(wl, w, "sequential")
+    T = wl.schedule.T
+    assert st.evals_per_sample == T
     assert _rel(seq, Problem(wl, w, np.float32).sequential()) <= REL_F32
     one, st1 = _run(wl, w, "picard", p=1)
     assert st1.iters == T and st1.evals_per_sample == 2 * T - 1

@@ -49,3 +49,20 @@ def test_seeded_input_module_holds_no_method_arithmetic():
     text = open(os.path.join(ROOT, "workloads", "__init__.py"), encoding="utf-8").read()
     for word in ("alphabar", "cumsum", "picard", "drift", "stride"):
         assert word not in text.lower(), word
+
+
+def test_bench_window_accounting():
+    """Window points and history rows of a stride trace (the update's
+    algorithmic bytes are priced from them)."""
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("bench_mod", os.path.join(ROOT, "bench.py"))
+    b = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(b)
+    # T = 10, p = 4: windows start at 0, 1, 3, 7 -> sizes 4, 4, 4, 3
+    assert b.window_points([1, 2, 4, 3], 4, 10) == 15
+    assert b.history_rows([1, 2, 4, 3], 10) == 3
+    import workloads as W
+    wl = W.WORKLOADS["policy_mlp_dpm15"]
+    assert b.update_bytes(wl, 15, False, 3) == 160 * (12 * 15 + 8 * 3)
+    assert b.sampler_name(wl).startswith("ParaDPMSolver")
+    assert b.metric_name(W.WORKLOADS["latent_ddpm1000_p64"]) == b.METRIC

@@ -35,7 +35,7 @@ class ScheduleSpec:
     beta_start: float = 1e-4
     beta_end: float = 0.02
     eta: float = 0.0     # DDIM only
-    solver: str = "euler"  # "euler", or "heun" (DDIM with eta = 0 only)
+    solver: str = "euler"  # "euler"; "heun" or "dpm2m" (DDIM with eta = 0 only)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -104,6 +104,15 @@ WORKLOADS: Dict[str, Workload] = {
     "latent_heun100_p32": Workload(
         "latent_heun100_p32", ScheduleSpec("ddim", 1000, 100, solver="heun"),
         ModelSpec("conv1x1", _LATENT, width=320), p=32, tau=0.05),
+    # DPM-Solver++(2M) (ParaDPMSolver, Sec. 4): the 16x10 policy at 15 steps
+    # (T_train = 90 gives the 6-apart timesteps that 15 of 100 steps take), and
+    # the 4x96x96 latent at 200 steps with tau = 0.1
+    "policy_mlp_dpm15": Workload(
+        "policy_mlp_dpm15", ScheduleSpec("ddim", 90, 15, solver="dpm2m"),
+        ModelSpec("mlp", (16, 10), width=1024), p=15, tau=0.1),
+    "latent_dpm200_p64": Workload(
+        "latent_dpm200_p64", ScheduleSpec("ddim", 1000, 200, solver="dpm2m"),
+        ModelSpec("conv1x1", _LATENT, width=320), p=64, tau=0.1),
 }
 
 
