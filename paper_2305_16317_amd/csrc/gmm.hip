@@ -150,6 +150,7 @@ __global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noi
     int t = 0, k = 0, f = 0;
     int pe = a.p < T ? a.p : T;
     int64_t evals = 0;
+    int first_stride = 0;
     if (tid == 0) s_bad = 0;
     __syncthreads();
     while (t < T) {
@@ -208,6 +209,7 @@ __global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noi
         const int stride = s_stride;
         const bool bad = s_bad != 0;
         if (tid == 0) a.trace[k] = stride;
+        if (k == 0) first_stride = stride;
         evals += pe;
         f = t + pe;
         t += stride;
@@ -218,13 +220,17 @@ __global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noi
     }
     for (int i = tid; i < BD; i += nth) a.out[i] = ring[(T % P1) * BD + i];
     if (tid == 0) {
-        a.st->t = t;
-        a.st->k = k;
-        a.st->f = f;
-        a.st->p_eff = 0;
-        a.st->first_stride = k > 0 ? a.trace[0] : 0;
-        a.st->evals = evals;
-        a.st->status = s_bad ? PD_ERR_NUMERIC : PD_OK;
+        LoopState v;
+        v.t = t;
+        v.k = k;
+        v.f = f;
+        v.p_eff = 0;
+        v.first_stride = first_stride;
+        v.nrows = 0;
+        v.evals = evals;
+        v.status = s_bad ? PD_ERR_NUMERIC : PD_OK;
+        *a.st = v;
+        mirror_state(v, a.st_host);
     }
 }
 

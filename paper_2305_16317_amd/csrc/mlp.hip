@@ -9,17 +9,28 @@
 // permutation of k works as long as A and B agree, so the loads stay
 // contiguous.
 //
-// One block = one 16 x 16 output tile; its 16 waves take every 16th chunk of
-// 16 k and the partial tiles are summed through LDS in a fixed order.  At the
-// policy network's sizes (100 rows in a window, one in the sequential chain)
-// the layer is bound by latency, not by the matrix core: more waves per tile
-// put more loads in flight (16 waves: the sequential chain 3.3 -> 2.2 ms).
+// One block = a 16-row x (16 kNSub)-column output tile.  Its kLinWaves waves
+// split K into contiguous runs of 16-wide chunks; each wave multiplies its x
+// chunk against kNSub column groups of W (the x operand is loaded once for
+// all of them), and the partial tiles are summed through LDS in wave order.
+// At the policy network's sizes (100 rows in a window, one in the
+// sequential chain) the layer is bound by latency and by the cost of
+// dispatching waves, not by the matrix core: few waves with a few dozen
+// MFMAs each beat many waves with a handful.
 #include "pd_internal.h"
 
 namespace pd {
 namespace {
 
-constexpr int kLinWaves = 16;   // waves per block, splitting K
+#ifndef PD_LIN_WAVES
+#define PD_LIN_WAVES 8
+#endif
+#ifndef PD_LIN_NSUB
+#define PD_LIN_NSUB 1
+#endif
+constexpr int kLinWaves = PD_LIN_WAVES;   // waves per block, splitting K
+constexpr int kNSub = PD_LIN_NSUB;        // 16-column groups per block
+constexpr int kBatch = 8;                 // chunks whose loads are in flight together
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
@@ -32,7 +43,7 @@ __global__ __launch_bounds__(kLinWaves * 64) void k_linear(LinearArgs a, const f
                                                 RowSrc src, int64_t D, float* __restrict__ y) {
     const int groups = src.active ? *src.active : src.max_groups;
     const int M = groups * src.group;
-    const int m0 = blockIdx.y * 16, n0 = blockIdx.x * 16;
+    const int m0 = blockIdx.y * 16, n0 = blockIdx.x * (16 * kNSub);
     if (m0 >= M) return;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int li = lane & 15, h = lane >> 4;
@@ -48,64 +59,72 @@ __global__ __launch_bounds__(kLinWaves * 64) void k_linear(LinearArgs a, const f
     } else {
         xrow = xd + (int64_t)mr * K;
     }
-    const int nr = min(n0 + li, N - 1);
-    const float* wrow = a.W + (int64_t)nr * K;
-
-    // the epilogue's bias (or per-timestep shift) of this lane's four outputs,
-    // fetched before the reduction so its latency hides behind the MFMAs
-    const int n_out = min(n0 + li, N - 1);
-    float addv[4];
+    const float* wrow[kNSub];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int m = min(m0 + 4 * h + q, M - 1);
-        addv[q] = a.shift != nullptr ? a.shift[(int64_t)src.n[m / src.group] * N + n_out]
-                                     : a.bias[n_out];
+    for (int s = 0; s < kNSub; ++s) wrow[s] = a.W + (int64_t)min(n0 + 16 * s + li, N - 1) * K;
+
+    // epilogue: thread tid owns output (row m0 + 4 (l / 16) + q, column
+    // n0 + 16 s + l % 16) with l = tid % 64, q = (tid / 64) % 4, s = tid / 256
+    // (threads past 64 * 4 * kNSub own none); its bias or per-timestep shift
+    // is fetched before the products so the latency hides behind them
+    const int el = threadIdx.x & 63, eq = (threadIdx.x >> 6) & 3, es = threadIdx.x >> 8;
+    const bool owner = es < kNSub;
+    const int em = m0 + 4 * (el >> 4) + eq, en = n0 + 16 * es + (el & 15);
+    float addv = 0.f;
+    if (owner) {
+        const int mc = min(em, M - 1), nc = min(en, N - 1);
+        addv = a.shift != nullptr ? a.shift[(int64_t)src.n[mc / src.group] * N + nc] : a.bias[nc];
     }
 
-    // this wave's chunks are c = w, w + 4, ...; kBatch of them are loaded
-    // before any is multiplied, so their loads are in flight together
-    constexpr int kBatch = 4;
-    f4 acc = {0.f, 0.f, 0.f, 0.f};
+    // this wave's chunks: a contiguous run of 16-wide k chunks
     const int nchunks = (K + 15) / 16;
-    for (int c0 = w; c0 < nchunks; c0 += kLinWaves * kBatch) {
-        f4 av[kBatch], bv[kBatch];
+    const int per = (nchunks + kLinWaves - 1) / kLinWaves;
+    const int c_begin = w * per, c_end = min(c_begin + per, nchunks);
+    f4 acc[kNSub];
+#pragma unroll
+    for (int s = 0; s < kNSub; ++s) acc[s] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int c0 = c_begin; c0 < c_end; c0 += kBatch) {
+        f4 av[kBatch], bv[kBatch][kNSub];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-            const int k = (c0 + kLinWaves * u) * 16 + 4 * h;
-            const bool ok = c0 + kLinWaves * u < nchunks && k < K;   // K is a multiple of 4
+            const int k = (c0 + u) * 16 + 4 * h;
+            const bool ok = c0 + u < c_end && k < K;   // K is a multiple of 4
             const int kk = ok ? k : 0;
             const f4 xa = *reinterpret_cast<const f4*>(xrow + kk);
-            const f4 wb = *reinterpret_cast<const f4*>(wrow + kk);
             av[u] = ok ? xa : f4{0.f, 0.f, 0.f, 0.f};
-            bv[u] = ok ? wb : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < kNSub; ++s) {
+                const f4 wb = *reinterpret_cast<const f4*>(wrow[s] + kk);
+                bv[u][s] = ok ? wb : f4{0.f, 0.f, 0.f, 0.f};
+            }
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u)
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u][q], bv[u][q], acc, 0, 0, 0);
+            for (int s = 0; s < kNSub; ++s)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    acc[s] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u][q], bv[u][s][q], acc[s], 0, 0, 0);
     }
 
-    __shared__ f4 s_acc[kLinWaves][64];
-    s_acc[w][lane] = acc;
+    // partial tiles, [wave][column group][register][lane]: conflict-free
+    // writes (one register of 64 lanes at a time) and reads (64 lanes)
+    __shared__ float s_acc[kLinWaves][kNSub][4][64];
+#pragma unroll
+    for (int s = 0; s < kNSub; ++s)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) s_acc[w][s][q][lane] = acc[s][q];
     __syncthreads();
-    if (w != 0) return;
-    f4 sum = s_acc[0][lane];
+    if (!owner || em >= M || en >= N) return;
+    float sum = s_acc[0][es][eq][el];
 #pragma unroll
-    for (int v = 1; v < kLinWaves; ++v) sum += s_acc[v][lane];
-
-    // D[i][j]: row m0 + 4 h + q, column n0 + li
-    const int n = n0 + li;
-    if (n >= N) return;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int m = m0 + 4 * h + q;
-        if (m >= M) continue;
-        float v = sum[q] + addv[q];
-        if (a.act == ACT_GELU) v = gelu_exact(v);
-        y[(int64_t)m * N + n] = v;
-    }
+    for (int v = 1; v < kLinWaves; ++v) sum += s_acc[v][es][eq][el];
+    float v = sum + addv;
+    if (a.act == ACT_GELU) v = gelu_exact(v);
+    y[(int64_t)em * N + en] = v;
 }
+
+static_assert(kLinWaves * 64 >= 256 * kNSub, "every output of the tile needs a thread");
 
 template <bool GATHER>
 void launch(const LinearArgs& a, const float* xd, const RowSrc& src, int64_t D, float* y,
@@ -114,7 +133,7 @@ void launch(const LinearArgs& a, const float* xd, const RowSrc& src, int64_t D, 
     if (Mmax == 0) return;
     if ((a.K % 4) != 0 || (GATHER && (D % 4) != 0))
         fail(PD_ERR_UNSUPPORTED, "mlp layer sizes must be multiples of 4");
-    const dim3 grid((unsigned)((a.N + 15) / 16), (unsigned)((Mmax + 15) / 16));
+    const dim3 grid((unsigned)((a.N + 16 * kNSub - 1) / (16 * kNSub)), (unsigned)((Mmax + 15) / 16));
     hipLaunchKernelGGL(k_linear<GATHER>, grid, dim3(kLinWaves * 64), 0, s, a, xd, src, D, y);
     PD_HIP(hipGetLastError());
 }

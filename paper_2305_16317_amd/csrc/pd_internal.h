@@ -49,6 +49,20 @@ struct LoopState {
                      // row (the point before the window) for the multistep drift
     int64_t evals;   // network evaluations per sample
 };
+// The host reads the loop state from a copy in mapped, coherent pinned host
+// memory that the kernels write as they change it (no copy launch per batch).
+__device__ inline void mirror_state(const LoopState& v, LoopState* host) {
+    if (!host) return;
+    host->t = v.t;
+    host->k = v.k;
+    host->f = v.f;
+    host->p_eff = v.p_eff;
+    host->status = v.status;
+    host->first_stride = v.first_stride;
+    host->nrows = v.nrows;
+    host->evals = v.evals;
+    __threadfence_system();
+}
 
 // ---------------------------------------------------------------- kernels
 // rng.hip
@@ -75,7 +89,8 @@ struct GmmLoopArgs {
     const float* x0;        // [batch][2]
     float* out;             // [batch][2]
     LoopState* st;          // final state (t, k, evals, status)
-    int32_t* trace;         // [T] stride of every iteration
+    LoopState* st_host;     // its host copy (mapped pinned memory), or nullptr
+    int32_t* trace;         // [T] stride of every iteration (mapped pinned memory)
     int32_t T, p, batch, tol_offset;
     float tau2;
 };
@@ -141,6 +156,7 @@ int picard_partial_blocks(int64_t D);
 // Everything the stride rule and the slide need (the finalize step).
 struct FinalizeArgs {
     LoopState* st;
+    LoopState* st_host;         // host copy of *st (mapped pinned memory), or nullptr
     const float* partials;      // [batch][p][picard_partial_blocks(D)]
     int32_t p, batch;
     int64_t D;
@@ -149,7 +165,7 @@ struct FinalizeArgs {
     float tau2;
     int32_t tol_offset;
     const int32_t* model_t;
-    int32_t* trace;
+    int32_t* trace;             // [T] strides (mapped pinned memory)
     int32_t* slot;
     int32_t* nrow;
     const int32_t* model_t_next;   // Heun only, else nullptr

@@ -129,6 +129,57 @@ __global__ __launch_bounds__(256) void k_heun_combine(const LoopState* __restric
         eps[i] = __fmul_rn(__fadd_rn(eps[i], eps2[i]), 0.5f);
 }
 
+// The stride is known: record it, slide the window and write the next
+// iteration's row descriptors.  mt / mt2 (or nullptr: read the tables) hold
+// model_t[t + i] / model_t_next[t + i] for i < 2p, which covers every index
+// read here (the next window starts at t + stride <= t + p_eff).  Thread 0
+// rewrites the loop state; every thread must have read it before.
+__device__ void finalize_apply(const FinalizeArgs& a, int stride, int bad, int t, int k, int pe,
+                               int rows_now, const int* mt, const int* mt2) {
+    LoopState* st = a.st;
+    const int p = a.p, T = a.T;
+    const int fn = t + pe, tn = t + stride;
+    const int pn = bad ? 0 : (p < T - tn ? p : T - tn);
+    auto model_t = [&](int m) { return mt ? mt[m - t] : a.model_t[m]; };
+    auto model_t_next = [&](int m) { return mt2 ? mt2[m - t] : a.model_t_next[m]; };
+    // next batch: [the point before the window, for the multistep drift] then
+    // the window's points
+    const int hn = (a.history && tn >= 1 && pn > 0) ? 1 : 0;
+    if (threadIdx.x == 0) {
+        a.trace[k] = stride;
+        LoopState v = *st;
+        if (k == 0) v.first_stride = stride;
+        v.k = k + 1;
+        // network evaluations: Heun evaluates twice per point but the last
+        // step; with a history row the batch had one row more than the window
+        v.evals += a.nrow2 ? 2 * pe - (t + pe == T ? 1 : 0) : rows_now;
+        v.f = fn;
+        v.t = bad ? T : tn;
+        v.p_eff = pn > 0 ? pn : 0;
+        if (bad) v.status = PD_ERR_NUMERIC;
+        v.nrows = pn > 0 ? pn + hn : 0;
+        *st = v;
+        if (hn) {
+            a.slot[0] = (tn - 1) % a.ring_slots;     // tn - 1 < fn: a computed point
+            a.nrow[0] = model_t(tn - 1);
+        }
+        mirror_state(v, a.st_host);
+    }
+    for (int j = threadIdx.x; j < pn; j += blockDim.x) {
+        const int m = tn + j;
+        a.slot[hn + j] = (m < fn ? m : fn) % a.ring_slots;
+        a.nrow[hn + j] = model_t(m);
+        if (a.nrow2) a.nrow2[j] = model_t_next(m);
+    }
+}
+
+// Tolerance of window offset o >= 1 (Algorithm 1's stride test compares the
+// error with it; sigma^2 = 0 allows no change at all).
+__device__ __forceinline__ float offset_tol(const FinalizeArgs& a, int t, int o) {
+    const float s2 = a.tol_var[t + o + a.tol_offset];
+    return (s2 == 0.f) ? 0.f : a.tau2 * s2;
+}
+
 // One block: reduce the partials of every (offset, sample), apply the stride
 // rule, slide the window and prepare the next iteration's row descriptors.
 // Every thread reads the loop state before the first barrier; thread 0
@@ -137,7 +188,7 @@ __device__ void finalize_body(const FinalizeArgs& a, int nblk) {
     LoopState* st = a.st;
     const int pe = st->p_eff;
     if (pe <= 0) return;
-    const int t = st->t, k = st->k, p = a.p, T = a.T, rows_now = st->nrows;
+    const int t = st->t, k = st->k, p = a.p, rows_now = st->nrows;
     __shared__ int s_stride, s_bad;
     if (threadIdx.x == 0) {
         s_stride = pe;
@@ -168,44 +219,12 @@ __device__ void finalize_body(const FinalizeArgs& a, int nblk) {
             } else {
                 const float err = s / Df;
                 if (!isfinite(err)) atomicOr(&s_bad, 1);
-                const float s2 = a.tol_var[t + o + a.tol_offset];
-                const float tol = (s2 == 0.f) ? 0.f : a.tau2 * s2;
-                if (!(err <= tol)) atomicMin(&s_stride, o);
+                if (!(err <= offset_tol(a, t, o))) atomicMin(&s_stride, o);
             }
         }
     }
     __syncthreads();
-    const int stride = s_stride;
-    const int fn = t + pe, tn = t + stride;
-    const int pn = s_bad ? 0 : (p < T - tn ? p : T - tn);
-    if (threadIdx.x == 0) {
-        a.trace[k] = stride;
-        if (k == 0) st->first_stride = stride;
-        st->k = k + 1;
-        // network evaluations: Heun evaluates twice per point but the last
-        // step; with a history row the batch had one row more than the window
-        st->evals += a.nrow2 ? 2 * pe - (t + pe == T ? 1 : 0) : rows_now;
-        st->f = fn;
-        st->t = s_bad ? T : tn;
-        st->p_eff = pn > 0 ? pn : 0;
-        if (s_bad) st->status = PD_ERR_NUMERIC;
-    }
-    // next batch: [the point before the window, for the multistep drift] then
-    // the window's points
-    const int hn = (a.history && tn >= 1 && pn > 0) ? 1 : 0;
-    if (threadIdx.x == 0) {
-        st->nrows = pn > 0 ? pn + hn : 0;
-        if (hn) {
-            a.slot[0] = (tn - 1) % a.ring_slots;     // tn - 1 < fn: a computed point
-            a.nrow[0] = a.model_t[tn - 1];
-        }
-    }
-    for (int j = threadIdx.x; j < pn; j += blockDim.x) {
-        const int m = tn + j;
-        a.slot[hn + j] = (m < fn ? m : fn) % a.ring_slots;
-        a.nrow[hn + j] = a.model_t[m];
-        if (a.nrow2) a.nrow2[j] = a.model_t_next[m];
-    }
+    finalize_apply(a, s_stride, s_bad, t, k, pe, rows_now, nullptr, nullptr);
 }
 
 __global__ __launch_bounds__(1024) void k_picard_finalize(FinalizeArgs a, int nblk) {
@@ -250,6 +269,26 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     const int ch = (pe + NW - 1) / NW;
     const int j0 = min(w * ch, pe), j1 = min(j0 + ch, pe);
     const int nr = j1 - j0;
+
+    // a single-block grid finalizes the iteration itself, from LDS: its
+    // tolerances and the timesteps of the next window are fetched now, with
+    // the window's data
+    __shared__ int s_mt[2 * kMaxWindow], s_mt2[2 * kMaxWindow];
+    __shared__ float s_err[kMaxWindow];
+    __shared__ int s_stride, s_bad;
+    float ftol = 0.f;
+    if (fuse_finalize) {
+        const int i = threadIdx.x;
+        if (i >= 1 && i < pe) ftol = offset_tol(fin, t, i);
+        if (i < 2 * p && t + i < fin.T) {
+            s_mt[i] = fin.model_t[t + i];
+            if (fin.nrow2) s_mt2[i] = fin.model_t_next[t + i];
+        }
+        if (i == 0) {
+            s_stride = pe;
+            s_bad = 0;
+        }
+    }
 
     // wave totals and first old points, then (after a barrier) the
     // per-row squared differences of every lane
@@ -371,15 +410,34 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     s = group_sum<TPR>(s);
     const int qw = q / R, qr = q % R;
     const int q0 = min(qw * ch, pe), nq = min(q0 + ch, pe) - q0;
+    if (!fuse_finalize) {
+        if (part == 0 && qr < nq) {
+            const int jq = q0 + qr;
+            partials[((int64_t)b * p + (jq + 1 < pe ? jq + 1 : 0)) * nblk + blk] = s;
+        }
+        return;
+    }
+    // one block, one sample: the sums are the errors' numerators; the stride
+    // test and the slide follow here (the same arithmetic as the separate
+    // finalize step, whose sum over one partial is that partial)
     if (part == 0 && qr < nq) {
         const int jq = q0 + qr;
-        partials[((int64_t)b * p + (jq + 1 < pe ? jq + 1 : 0)) * nblk + blk] = s;
+        s_err[jq + 1 < pe ? jq + 1 : 0] = s;
     }
-    // a grid of one block finalizes the iteration itself: one launch fewer
-    if (fuse_finalize) {
-        __syncthreads();
-        finalize_body(fin, nblk);
+    const int k = st->k, rows_now = st->nrows;
+    __syncthreads();
+    {
+        const int o = threadIdx.x;
+        if (o == 0) {
+            if (s_err[0] != 0.f) atomicOr(&s_bad, 1);
+        } else if (o < pe) {
+            const float err = s_err[o] / (float)D;
+            if (!isfinite(err)) atomicOr(&s_bad, 1);
+            if (!(err <= ftol)) atomicMin(&s_stride, o);
+        }
     }
+    __syncthreads();
+    finalize_apply(fin, s_stride, s_bad, t, k, pe, rows_now, s_mt, fin.nrow2 ? s_mt2 : nullptr);
 }
 
 

@@ -526,15 +526,29 @@ struct pd_workspace {
     const pd_denoiser* d = nullptr;
     int p = 0, batch = 0, T = 0;
     int64_t D = 0;
-    DevBuf ring, eps, noise, A, B, zstd, tolv, model_t, state, trace, slot, nrow, partials, scratch;
+    DevBuf ring, eps, noise, A, B, zstd, tolv, model_t, state, slot, nrow, partials, scratch;
     DevBuf xt, eps2, model_t_next, nrow2;   // Heun: predictions, second epsilons, n_{i+1}
     DevBuf Rt, St, xprev, eprev;            // multistep: tables; the sequential loop's last step
     int ring_slots() const { return p + 1 + (s->dpm ? 1 : 0); }
+    // mapped, coherent pinned host memory that the kernels write directly:
+    // the loop state's host copy and the stride of every iteration
     LoopState* h_state = nullptr;
+    LoopState* h_state_dev = nullptr;   // the device's address of h_state
+    int32_t* h_trace = nullptr;
+    int32_t* h_trace_dev = nullptr;
     ~pd_workspace() {
         if (h_state) (void)hipHostFree(h_state);
+        if (h_trace) (void)hipHostFree(h_trace);
     }
 };
+
+template <class T>
+static void host_mapped(T** host, T** dev, size_t count) {
+    PD_HIP(hipHostMalloc(reinterpret_cast<void**>(host), sizeof(T) * count,
+                         hipHostMallocMapped | hipHostMallocCoherent));
+    std::memset(*host, 0, sizeof(T) * count);
+    PD_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(dev), *host, 0));
+}
 
 static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, int batch,
                              pd_workspace& w) {
@@ -559,7 +573,6 @@ static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, 
     w.tolv.upload(s.tol_var.data(), s.T);
     w.model_t.upload(s.model_t.data(), s.T);
     w.state.alloc(sizeof(LoopState));
-    w.trace.alloc(sizeof(int32_t) * (size_t)s.T);
     w.slot.alloc(sizeof(int32_t) * (size_t)(p + hist));
     w.nrow.alloc(sizeof(int32_t) * (size_t)(p + hist));
     w.partials.alloc(sizeof(float) * (size_t)picard_partial_blocks(d.D) * p * batch);
@@ -577,7 +590,8 @@ static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, 
     }
     const size_t sc = d.scratch_floats((int64_t)(p + hist) * batch);
     if (sc) w.scratch.alloc(sc * sizeof(float));
-    PD_HIP(hipHostMalloc(reinterpret_cast<void**>(&w.h_state), sizeof(LoopState), hipHostMallocDefault));
+    host_mapped(&w.h_state, &w.h_state_dev, 1);
+    host_mapped(&w.h_trace, &w.h_trace_dev, (size_t)s.T);
 }
 
 extern "C" pd_status pd_workspace_create(const pd_schedule* s, const pd_denoiser* d, int32_t p,
@@ -633,7 +647,7 @@ static void draw_noise(pd_workspace& w, uint64_t seed, hipStream_t st) {
 }
 
 static void fill_stats(pd_sample_stats* stats, int iters, int64_t evals, int batch, bool guided,
-                       const int32_t* dtrace, const KernelTimer& tm) {
+                       const int32_t* trace, const KernelTimer& tm) {
     if (!stats) return;
     stats->denoiser_launches = tm.count[CAT_DENOISER];
     stats->update_launches = tm.count[CAT_UPDATE];
@@ -644,10 +658,9 @@ static void fill_stats(pd_sample_stats* stats, int iters, int64_t evals, int bat
     stats->iters = iters;
     stats->evals_per_sample = evals;
     stats->network_rows = evals * batch * (guided ? 2 : 1);
-    if (stats->stride_trace && stats->trace_cap > 0 && dtrace) {
+    if (stats->stride_trace && stats->trace_cap > 0 && trace) {   // host memory, loop finished
         const int n = iters < stats->trace_cap ? iters : stats->trace_cap;
-        if (n > 0)
-            PD_HIP(hipMemcpy(stats->stride_trace, dtrace, sizeof(int32_t) * n, hipMemcpyDeviceToHost));
+        if (n > 0) std::memcpy(stats->stride_trace, trace, sizeof(int32_t) * n);
     }
 }
 
@@ -672,7 +685,8 @@ static GmmLoopArgs gmm_loop_args(const pd_schedule& s, const pd_denoiser& d, pd_
     a.x0 = w.ring.as<float>();
     a.out = x_out;
     a.st = w.state.as<LoopState>();
-    a.trace = w.trace.as<int32_t>();
+    a.st_host = w.h_state_dev;
+    a.trace = w.h_trace_dev;
     a.T = s.T;
     a.p = p;
     a.batch = batch;
@@ -771,11 +785,10 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
             launch_gmm_picard_loop(gmm_loop_args(*s, *d, w, pc, batch, tau2, x_out), kFusedLoopLds,
                                    st);
             tm.mark(CAT_UPDATE);
-            PD_HIP(hipMemcpyAsync(w.h_state, dst, sizeof(LoopState), hipMemcpyDeviceToHost, st));
-            PD_HIP(hipStreamSynchronize(st));
+            PD_HIP(hipStreamSynchronize(st));     // the kernel wrote the state's host copy
             if (w.h_state->status != PD_OK) fail(PD_ERR_NUMERIC, "non-finite point or error in the window");
             tm.collect();
-            fill_stats(stats, w.h_state->k, w.h_state->evals, batch, d->guided(), w.trace.as<int32_t>(), tm);
+            fill_stats(stats, w.h_state->k, w.h_state->evals, batch, d->guided(), w.h_trace, tm);
             return;
         }
         const int32_t* mtn = s->heun ? w.model_t_next.as<int32_t>() : nullptr;
@@ -785,10 +798,11 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         const RowSrc src2{w.xt.as<float>(), nullptr, BD, batch, pc, nrow2, &dst->p_eff};
         const int hist = s->dpm ? 1 : 0;     // the multistep drift's row x_{t-1}
         const int slots = pc + 1 + hist;
-        const FinalizeArgs fin{dst, w.partials.as<float>(), pc, batch, d->D, T, w.tolv.as<float>(),
-                               tau2, s->desc.tol_index_offset, w.model_t.as<int32_t>(),
-                               w.trace.as<int32_t>(), w.slot.as<int32_t>(), w.nrow.as<int32_t>(),
-                               mtn, nrow2, slots, hist};
+        const FinalizeArgs fin{dst, w.h_state_dev, w.partials.as<float>(), pc, batch, d->D, T,
+                               w.tolv.as<float>(), tau2, s->desc.tol_index_offset,
+                               w.model_t.as<int32_t>(), w.h_trace_dev, w.slot.as<int32_t>(),
+                               w.nrow.as<int32_t>(), mtn, nrow2, slots, hist};
+        const float* xT = w.ring.as<float>() + (int64_t)(T % slots) * BD;
         const RowSrc src{w.ring.as<float>(), w.slot.as<int32_t>(), BD,     batch,
                          pc + hist,          w.nrow.as<int32_t>(), &dst->nrows};
         int t_host = 0, k_host = 0, issued = 0;
@@ -833,8 +847,10 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                 }
             }
             issued += need;
-            PD_HIP(hipMemcpyAsync(w.h_state, dst, sizeof(LoopState), hipMemcpyDeviceToHost, st));
-            PD_HIP(hipStreamSynchronize(st));
+            // x_T's slot, copied out after every batch so that the last one
+            // needs no further round trip (earlier copies are overwritten)
+            PD_HIP(hipMemcpyAsync(x_out, xT, sizeof(float) * BD, hipMemcpyDeviceToDevice, st));
+            PD_HIP(hipStreamSynchronize(st));     // the finalize steps wrote the state's host copy
             if (w.h_state->status != PD_OK) fail(PD_ERR_NUMERIC, "non-finite point or error in the window");
             t_host = w.h_state->t;
             k_host = w.h_state->k;
@@ -843,10 +859,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         }
         const int iters = w.h_state->k;
         const int64_t evals = w.h_state->evals;
-        const float* xT = w.ring.as<float>() + (int64_t)(T % slots) * BD;
-        PD_HIP(hipMemcpyAsync(x_out, xT, sizeof(float) * BD, hipMemcpyDeviceToDevice, st));
-        PD_HIP(hipStreamSynchronize(st));
         tm.collect();
-        fill_stats(stats, iters, evals, batch, d->guided(), w.trace.as<int32_t>(), tm);
+        fill_stats(stats, iters, evals, batch, d->guided(), w.h_trace, tm);
     });
 }

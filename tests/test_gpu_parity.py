@@ -91,7 +91,7 @@ def test_gmm_forward(M):
 
 
 @pytest.mark.parametrize("shape,width,M", [((4, 3), 32, 3), ((4, 3), 32, 37), ((16, 10), 1024, 100),
-                                           ((16, 10), 1024, 1)])
+                                           ((16, 10), 1024, 1), ((4, 5), 40, 50), ((2, 2), 4, 17)])
 def test_mlp_forward(shape, width, M):
     wl = _wl("mlp", shape, width)
     w = W.make_weights(wl.model)
