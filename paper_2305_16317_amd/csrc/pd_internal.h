@@ -174,7 +174,7 @@ struct FinalizeArgs {
     int32_t history;               // 1: the next batch starts with x_{t-1} (multistep drift)
 };
 // Scan + error partials of one iteration.  Returns true when the grid is a
-// single block, which then also ran the finalize step.
+// single block, which then also ran the finalize step (from LDS).
 // R, S: the multistep (DPM-Solver) coefficients of x_{i-1} and eps_{i-1}, or
 // nullptr; eps then has the history row first when st->nrows > st->p_eff.
 bool launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,

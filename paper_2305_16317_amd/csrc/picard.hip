@@ -129,15 +129,25 @@ __global__ __launch_bounds__(256) void k_heun_combine(const LoopState* __restric
         eps[i] = __fmul_rn(__fadd_rn(eps[i], eps2[i]), 0.5f);
 }
 
+// Barrier for LDS traffic only: global stores issued before it need not have
+// completed (later kernels read them, no wave of this block does).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // The stride is known: record it, slide the window and write the next
-// iteration's row descriptors.  mt / mt2 (or nullptr: read the tables) hold
-// model_t[t + i] / model_t_next[t + i] for i < 2p, which covers every index
-// read here (the next window starts at t + stride <= t + p_eff).  Thread 0
-// rewrites the loop state; every thread must have read it before.
-__device__ void finalize_apply(const FinalizeArgs& a, int stride, int bad, int t, int k, int pe,
-                               int rows_now, const int* mt, const int* mt2) {
+// iteration's row descriptors.  cur is the loop state as the iteration found
+// it.  mt / mt2 (or nullptr: read the tables) hold model_t[t + i] /
+// model_t_next[t + i] for i < 2p, which covers every index read here (the
+// next window starts at t + stride <= t + p_eff).  Thread 0 rewrites the loop
+// state.
+__device__ void finalize_apply(const FinalizeArgs& a, int stride, int bad, const LoopState& cur,
+                               const int* mt, const int* mt2) {
     LoopState* st = a.st;
     const int p = a.p, T = a.T;
+    const int t = cur.t, k = cur.k, pe = cur.p_eff, rows_now = cur.nrows;
     const int fn = t + pe, tn = t + stride;
     const int pn = bad ? 0 : (p < T - tn ? p : T - tn);
     auto model_t = [&](int m) { return mt ? mt[m - t] : a.model_t[m]; };
@@ -147,7 +157,7 @@ __device__ void finalize_apply(const FinalizeArgs& a, int stride, int bad, int t
     const int hn = (a.history && tn >= 1 && pn > 0) ? 1 : 0;
     if (threadIdx.x == 0) {
         a.trace[k] = stride;
-        LoopState v = *st;
+        LoopState v = cur;
         if (k == 0) v.first_stride = stride;
         v.k = k + 1;
         // network evaluations: Heun evaluates twice per point but the last
@@ -182,13 +192,12 @@ __device__ __forceinline__ float offset_tol(const FinalizeArgs& a, int t, int o)
 
 // One block: reduce the partials of every (offset, sample), apply the stride
 // rule, slide the window and prepare the next iteration's row descriptors.
-// Every thread reads the loop state before the first barrier; thread 0
-// rewrites it after the last one.
-__device__ void finalize_body(const FinalizeArgs& a, int nblk) {
-    LoopState* st = a.st;
-    const int pe = st->p_eff;
+// cur is the loop state as the iteration found it; thread 0 rewrites it at
+// the end.
+__device__ void finalize_body(const FinalizeArgs& a, int nblk, const LoopState& cur) {
+    const int pe = cur.p_eff;
     if (pe <= 0) return;
-    const int t = st->t, k = st->k, p = a.p, rows_now = st->nrows;
+    const int t = cur.t, p = a.p;
     __shared__ int s_stride, s_bad;
     if (threadIdx.x == 0) {
         s_stride = pe;
@@ -201,6 +210,7 @@ __device__ void finalize_body(const FinalizeArgs& a, int nblk) {
     const float Df = (float)a.D;
     for (int pair = team; pair < pe * a.batch; pair += nteams) {
         const int o = pair / a.batch, b = pair % a.batch;
+        const float tol = o >= 1 ? offset_tol(a, t, o) : 0.f;    // in flight with the sums
         const float* src = a.partials + ((int64_t)b * p + o) * nblk;
         // 8 independent loads per step keep the team's reads in flight together
         float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -213,23 +223,34 @@ __device__ void finalize_body(const FinalizeArgs& a, int nblk) {
         }
         float s = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
         s = group_sum<kTeam>(s);
+        bool fails = false, bad = false;
         if (tl == 0) {
             if (o == 0) {
-                if (s != 0.f) atomicOr(&s_bad, 1);
+                bad = s != 0.f;
             } else {
                 const float err = s / Df;
-                if (!isfinite(err)) atomicOr(&s_bad, 1);
-                if (!(err <= offset_tol(a, t, o))) atomicMin(&s_stride, o);
+                bad = !isfinite(err);
+                fails = !(err <= tol);
             }
         }
+        // lanes hold pairs in increasing order: the wave's first failing
+        // lane has its smallest failing offset, and one lane per wave votes
+        const uint64_t fm = __ballot(fails), bm = __ballot(bad);
+        const int lane = threadIdx.x & 63;
+        if (fm && lane == __ffsll((unsigned long long)fm) - 1) atomicMin(&s_stride, o);
+        if (bm && lane == __ffsll((unsigned long long)bm) - 1) atomicOr(&s_bad, 1);
     }
     __syncthreads();
-    finalize_apply(a, s_stride, s_bad, t, k, pe, rows_now, nullptr, nullptr);
+    finalize_apply(a, s_stride, s_bad, cur, nullptr, nullptr);
 }
 
+// The finalize step of a multi-block scan (kernel order makes every block's
+// partials visible to it).
 __global__ __launch_bounds__(1024) void k_picard_finalize(FinalizeArgs a, int nblk) {
-    finalize_body(a, nblk);
+    const LoopState cur = *a.st;
+    finalize_body(a, nblk, cur);
 }
+
 
 // One block: 64 * VEC consecutive columns of one sample b, all window rows,
 // split over 16 waves (rows [w*ch, (w+1)*ch) per wave, ch <= R).  Drift and
@@ -252,9 +273,10 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     FinalizeArgs fin, int fuse_finalize) {
     typedef typename Cols<VEC>::type V;
     constexpr int NW = kScanWaves;
-    const int pe = st->p_eff;
+    const LoopState cur = *st;
+    const int pe = cur.p_eff;
     if (pe <= 0) return;
-    const int t = st->t, f = st->f;
+    const int t = cur.t, f = cur.f;
     // the wave index is uniform: keep it (and every row index derived from
     // it) in scalar registers
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -265,7 +287,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     const int64_t col = (int64_t)b * D + (valid ? d : 0);
     const int P1 = fin.ring_slots;
     // DPM-Solver: eps row 0 holds the point before the window (once t >= 1)
-    const int hist = DPM ? st->nrows - pe : 0;
+    const int hist = DPM ? cur.nrows - pe : 0;
     const int ch = (pe + NW - 1) / NW;
     const int j0 = min(w * ch, pe), j1 = min(j0 + ch, pe);
     const int nr = j1 - j0;
@@ -275,18 +297,15 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     // the window's data
     __shared__ int s_mt[2 * kMaxWindow], s_mt2[2 * kMaxWindow];
     __shared__ float s_err[kMaxWindow];
-    __shared__ int s_stride, s_bad;
     float ftol = 0.f;
+    int mt_i = 0, mt2_i = 0;   // stored to LDS once the window's loads have arrived
+    const bool has_mt = fuse_finalize && (int)threadIdx.x < 2 * p && t + (int)threadIdx.x < fin.T;
     if (fuse_finalize) {
         const int i = threadIdx.x;
         if (i >= 1 && i < pe) ftol = offset_tol(fin, t, i);
-        if (i < 2 * p && t + i < fin.T) {
-            s_mt[i] = fin.model_t[t + i];
-            if (fin.nrow2) s_mt2[i] = fin.model_t_next[t + i];
-        }
-        if (i == 0) {
-            s_stride = pe;
-            s_bad = 0;
+        if (has_mt) {
+            mt_i = fin.model_t[t + i];
+            if (fin.nrow2) mt2_i = fin.model_t_next[t + i];
         }
     }
 
@@ -359,7 +378,13 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     sh.x.tot[0][w][lane] = acc_y;
     sh.x.tot[1][w][lane] = acc_z;
     sh.x.first[w][lane] = xo[0];   // x^k_{t+j0}: the previous wave's old point past its range
-    __syncthreads();
+    if (has_mt) {
+        s_mt[threadIdx.x] = mt_i;
+        s_mt2[threadIdx.x] = mt2_i;
+    }
+    // every ring value this wave read has been consumed above, so the ring
+    // writes after the next barrier cannot overtake a read
+    lds_barrier();
     V py = V(0.f), pz = V(0.f);
     for (int v = 0; v < w; ++v) {
         const V a = sh.x.tot[0][v][lane], c2 = sh.x.tot[1][v][lane];
@@ -370,7 +395,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
         }
     }
     const V next_old = (w + 1 < NW) ? sh.x.first[w + 1][lane] : V(0.f);
-    __syncthreads();
+    lds_barrier();
 
     // ---- new points, their squared differences, and the writes
     V sy = V(0.f), sz = V(0.f);
@@ -400,7 +425,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
         if (in && valid) *reinterpret_cast<V*>(ring + (int64_t)((t + j + 1) % P1) * slotsz + col) = xn;
         sh.d2[w * R + r][lane] = (in && valid) ? acc : 0.f;
     }
-    __syncthreads();
+    lds_barrier();
     // row q of the NW * R (wave, row) pairs is summed by 64 / R threads
     constexpr int TPR = 64 / R;
     const int q = threadIdx.x / TPR, part = threadIdx.x % TPR;
@@ -415,7 +440,7 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
             const int jq = q0 + qr;
             partials[((int64_t)b * p + (jq + 1 < pe ? jq + 1 : 0)) * nblk + blk] = s;
         }
-        return;
+        return;     // the finalize step follows as its own launch
     }
     // one block, one sample: the sums are the errors' numerators; the stride
     // test and the slide follow here (the same arithmetic as the separate
@@ -424,20 +449,33 @@ __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
         const int jq = q0 + qr;
         s_err[jq + 1 < pe ? jq + 1 : 0] = s;
     }
-    const int k = st->k, rows_now = st->nrows;
-    __syncthreads();
+    lds_barrier();
+    // thread o tests offset o; each wave records its first failing offset
+    __shared__ int s_wfail[NW], s_wbad[NW];
     {
         const int o = threadIdx.x;
+        bool fails = false, bad = false;
         if (o == 0) {
-            if (s_err[0] != 0.f) atomicOr(&s_bad, 1);
+            bad = s_err[0] != 0.f;
         } else if (o < pe) {
             const float err = s_err[o] / (float)D;
-            if (!isfinite(err)) atomicOr(&s_bad, 1);
-            if (!(err <= ftol)) atomicMin(&s_stride, o);
+            bad = !isfinite(err);
+            fails = !(err <= ftol);
+        }
+        const uint64_t fm = __ballot(fails), bm = __ballot(bad);
+        if (lane == 0) {
+            s_wfail[w] = fm ? w * 64 + __ffsll((unsigned long long)fm) - 1 : pe;
+            s_wbad[w] = bm != 0;
         }
     }
-    __syncthreads();
-    finalize_apply(fin, s_stride, s_bad, t, k, pe, rows_now, s_mt, fin.nrow2 ? s_mt2 : nullptr);
+    lds_barrier();
+    int stride = pe, bad = 0;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) {
+        stride = min(stride, s_wfail[v]);
+        bad |= s_wbad[v];
+    }
+    finalize_apply(fin, stride, bad, cur, s_mt, fin.nrow2 ? s_mt2 : nullptr);
 }
 
 
@@ -551,7 +589,7 @@ static bool launch_scan(const LoopState* st, float* ring, const float* eps, cons
                         int batch, int64_t D, float* partials, const FinalizeArgs& fin,
                         hipStream_t s) {
     const dim3 grid((unsigned)picard_partial_blocks(D), (unsigned)batch);
-    const int fuse = grid.x * grid.y == 1;
+    const int fuse = grid.x * grid.y == 1;   // one block: the finalize works from LDS
     const dim3 block(kScanWaves * 64);
     if (Rt)      // DPM-Solver integrates the noise-free chain
         hipLaunchKernelGGL((k_picard_scan<R, VEC, false, true>), grid, block, 0, s, st, ring, eps,
@@ -590,6 +628,7 @@ void launch_picard_finalize(const FinalizeArgs& fin, hipStream_t s) {
                        picard_partial_blocks(fin.D));
     PD_HIP(hipGetLastError());
 }
+
 
 void launch_seq_step(float* x, const float* eps, const float* z, float A, float B, int64_t n,
                      hipStream_t s) {

@@ -835,11 +835,10 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                     launch_heun_combine(dst, w.eps.as<float>(), w.eps2.as<float>(), pc, T, BD, st);
                 }
                 tm.mark(CAT_DENOISER);
-                const bool fused = launch_picard_scan(dst, w.ring.as<float>(), w.eps.as<float>(),
-                                                      w.noise.as<float>(), w.A.as<float>(),
-                                                      w.B.as<float>(), w.Rt.as<float>(),
-                                                      w.St.as<float>(), pc, batch, d->D,
-                                                      w.partials.as<float>(), fin, st);
+                const bool fused = launch_picard_scan(
+                    dst, w.ring.as<float>(), w.eps.as<float>(), w.noise.as<float>(),
+                    w.A.as<float>(), w.B.as<float>(), w.Rt.as<float>(), w.St.as<float>(), pc, batch,
+                    d->D, w.partials.as<float>(), fin, st);
                 tm.mark(CAT_UPDATE);
                 if (!fused) {
                     launch_picard_finalize(fin, st);
