@@ -322,6 +322,8 @@ def main() -> int:
         "roofline": {"bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK[dtype] / 1e12,
                      "unit": "TFLOP/s", "frac": achieved / PEAK[dtype],
                      "traffic": traffic, "kernel": kname,
+                     # the MLP's four layer launches are timed together, as one call
+                     "kernels_per_call": 4 if wl.model.kind == "mlp" else 1,
                      "flops_per_launch": fl / max(den_n, 1),
                      "mean_launch_ms": den_ms / max(den_n, 1), "launches": den_n},
         "roofline_update": {"bound": "hbm", "achieved": upd_rate / 1e9, "peak": HBM_PEAK / 1e9,

@@ -156,8 +156,9 @@ def test_forward_empty_batch_is_noop():
 
 
 # ------------------------------------------------------------------ samplers
-def _run(wl, weights, sampler="picard", p=None, tau=None, workspace=None, seed=None):
-    sched, den = pd.from_workload(wl, weights)
+def _run(wl, weights, sampler="picard", p=None, tau=None, workspace=None, seed=None,
+         tol_offset=0):
+    sched, den = pd.from_workload(wl, weights, tol_offset)
     x = torch.empty(wl.batch * wl.model.D, device="cuda")
     seed = wl.noise_seed if seed is None else seed
     if sampler == "picard":
@@ -186,6 +187,19 @@ SMALL = {
     "conv_ddim_b3": lambda: W.small_variant("latent_ddim200_b4", T=30, p=8, shape=(4, 6, 7), width=32, batch=3),
     "conv_p128": lambda: W.small_variant("latent_ddpm1000_p64", T=200, p=128, shape=(4, 4, 8), width=32),
     "conv_p_clamped": lambda: W.small_variant("latent_ddpm1000_p64", T=20, p=500, shape=(4, 4, 8), width=32),
+    # degenerate and extreme shapes: one step; the shortest DDPM chain; DDIM
+    # with noise; the largest window with several samples (conv and mlp)
+    "conv_T1": lambda: W.Workload("t1", W.ScheduleSpec("ddim", 10, 1),
+                                  W.ModelSpec("conv1x1", (4, 4, 8), width=32), p=4, tau=0.1),
+    "gmm_T2": lambda: W.Workload("t2", W.ScheduleSpec("ddpm", 2, 2), W.ModelSpec("gmm2d", (2,)),
+                                 p=4, tau=0.1, batch=3),
+    "conv_ddim_eta": lambda: W.Workload("eta", W.ScheduleSpec("ddim", 300, 30, eta=0.7),
+                                        W.ModelSpec("conv1x1", (4, 6, 7), width=32), p=8,
+                                        tau=0.1, batch=2),
+    "conv_p128_b3": lambda: W.small_variant("latent_ddpm1000_p64", T=160, p=128, shape=(4, 4, 8),
+                                            width=32, batch=3),
+    "mlp_p128_b2": lambda: W.small_variant("policy_mlp_ddpm100", T=150, p=128, shape=(4, 3),
+                                           width=32, batch=2),
     "conv_cfg_f32": lambda: W.Workload("cfg", W.ScheduleSpec("ddpm", 50, 50),
                                        W.ModelSpec("conv1x1", (4, 8, 8), width=64, cond_dim=24,
                                                    guidance=7.5), p=16, tau=0.1),
@@ -226,7 +240,7 @@ def test_picard_matches_oracle(name):
 
 
 @pytest.mark.parametrize("name", ["gmm_p7_b3", "gmm_k12", "gmm_k40", "mlp_small", "conv_ddpm",
-                                  "conv_ddim_b3"])
+                                  "conv_ddim_b3", "conv_T1", "gmm_T2", "conv_ddim_eta"])
 def test_sequential_matches_oracle(name):
     wl = SMALL[name]()
     w = W.make_weights(wl.model)
@@ -261,6 +275,19 @@ def test_runs_are_deterministic_and_workspace_reuse():
         torch.cuda.synchronize()
     assert np.array_equal(x.cpu().numpy().reshape(1, -1).view(np.uint32), a.view(np.uint32))
     assert st == sa
+
+
+@pytest.mark.parametrize("name", ["gmm_p7_b3", "gmm_b48_general", "mlp_small", "conv_ddpm",
+                                  "conv_ddim_b3"])
+def test_tolerance_offset_matches_oracle(name):
+    """The sigma_{t+j-1} reading of the stride test's variance index
+    (tol_index_offset = -1): strides and samples as the oracle's."""
+    wl = SMALL[name]()
+    w = W.make_weights(wl.model)
+    got, st = _run(wl, w, tol_offset=-1)
+    ref = Problem(wl, w, np.float32).picard(tol_offset=-1)
+    assert (st.iters, st.trace, st.evals_per_sample) == (ref.iters, ref.trace, ref.evals)
+    assert _rel(got, ref.x) <= REL_F32, _rel(got, ref.x)
 
 
 def test_infinite_tolerance_single_sweeps():
