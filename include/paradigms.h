@@ -222,9 +222,12 @@ typedef struct pd_sample_stats {
 
 typedef struct pd_workspace pd_workspace;
 
-/* Device buffers for sampling with window p and batch size `batch` on the
- * current device: the window ring of p+1 points, the noise of all T steps,
- * the drift batch and the loop state.  Lets repeated calls avoid allocation. */
+/* Buffers for sampling with window p and batch size `batch` on the current
+ * device: the window ring of p+1 points (p+2 for PD_DDIM_DPM2M, which also
+ * keeps x_{t-1}), the noise of all T steps, the drift batch and the loop
+ * state, plus mapped pinned host memory that the kernels write the loop
+ * state and the stride of every iteration into (so the host reads them
+ * without copies).  Lets repeated calls avoid allocation. */
 pd_status pd_workspace_create(const pd_schedule* s, const pd_denoiser* d, int32_t p,
                               int32_t batch, pd_workspace** out);
 void pd_workspace_destroy(pd_workspace* w);
@@ -239,13 +242,15 @@ pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoiser* d, uint6
                                float* x_out, pd_sample_stats* stats, pd_workspace* ws,
                                void* stream);
 
-/* ParaDiGMS sampling, Algorithm 1, with window p (clamped to T) and
- * tolerance tau (>= 0; +inf accepts every point whose sigma^2 > 0).  The
+/* ParaDiGMS sampling, Algorithm 1, with window p (clamped to T, at most 128)
+ * and tolerance tau (>= 0; +inf accepts every point whose sigma^2 > 0).  The
  * stride test fails offset j in [1, p) when, for any sample b of the batch,
  * not ((1/D) |x^{k+1}_{t+j} - x^k_{t+j}|^2 <= tau^2 sigma^2), with the product
  * taken as 0 when sigma^2 = 0.  Returns PD_ERR_NUMERIC (with x_out
  * unspecified) if a point or error becomes non-finite.  x_out: device float
- * [batch][D]; ws as for pd_sample_sequential (its p must be >= the clamped p). */
+ * [batch][D], also written between batches of iterations (only its content
+ * on return is the sample); ws as for pd_sample_sequential (its p must be
+ * >= the clamped p).  PD_ERR_UNSUPPORTED for a clamped p above 128. */
 pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d, int32_t p, float tau,
                            uint64_t noise_seed, int32_t batch, const int64_t* sample_shape,
                            int32_t ndim, float* x_out, pd_sample_stats* stats, pd_workspace* ws,
