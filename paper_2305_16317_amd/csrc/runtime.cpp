@@ -534,11 +534,13 @@ struct pd_workspace {
     // the loop state's host copy and the stride of every iteration
     LoopState* h_state = nullptr;
     LoopState* h_state_dev = nullptr;   // the device's address of h_state
+    hipEvent_t batch_event = nullptr;   // before the last iteration of a batch
     int32_t* h_trace = nullptr;
     int32_t* h_trace_dev = nullptr;
     ~pd_workspace() {
         if (h_state) (void)hipHostFree(h_state);
         if (h_trace) (void)hipHostFree(h_trace);
+        if (batch_event) (void)hipEventDestroy(batch_event);
     }
 };
 
@@ -591,6 +593,7 @@ static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, 
     const size_t sc = d.scratch_floats((int64_t)(p + hist) * batch);
     if (sc) w.scratch.alloc(sc * sizeof(float));
     host_mapped(&w.h_state, &w.h_state_dev, 1);
+    PD_HIP(hipEventCreateWithFlags(&w.batch_event, hipEventDisableTiming));
     host_mapped(&w.h_trace, &w.h_trace_dev, (size_t)s.T);
 }
 
@@ -805,6 +808,15 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         const float* xT = w.ring.as<float>() + (int64_t)(T % slots) * BD;
         const RowSrc src{w.ring.as<float>(), w.slot.as<int32_t>(), BD,     batch,
                          pc + hist,          w.nrow.as<int32_t>(), &dst->nrows};
+        // The kernels write the loop state into host memory as they go, so
+        // the host decides each next batch while the GPU still runs the
+        // previous batch's last iteration (it waits on an event recorded
+        // before that iteration): the GPU never waits idle for the host.
+        volatile LoopState* hs = w.h_state;
+        hs->t = 0;              // the copy still holds the previous call's end
+        hs->k = 0;
+        hs->status = PD_OK;
+        hs->first_stride = 0;
         int t_host = 0, k_host = 0, issued = 0;
         for (;;) {
             // every iteration advances t by at most pc, so at least this many
@@ -814,10 +826,11 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
             // done: strides grow as the trajectory converges, so early means
             // overestimate what is left, and iterations enqueued past the end
             // (they find p_eff = 0 on the device and return at once) still cost
-            // a dispatch each.
+            // a dispatch each.  Iterations still queued count against it.
+            const int in_flight = issued - k_host;
             int need = (T - t_host + pc - 1) / pc;
             if (issued == 0 && T > 1) need = 1 + (T - 1 + pc - 1) / pc;
-            const int first_stride = w.h_state->first_stride;
+            const int first_stride = hs->first_stride;
             if (k_host >= 2 && t_host > first_stride) {
                 const double mean = (double)(t_host - first_stride) / (double)(k_host - 1);
                 int est = (int)std::ceil((double)(T - t_host) / mean);
@@ -825,37 +838,52 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                 need = need > est ? need : est;
             }
             need = need < T - t_host ? need : T - t_host;   // stride >= 1 bounds the rest
-            tm.mark(-1);
-            for (int it = 0; it < need; ++it) {
-                d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
-                if (s->heun) {   // second evaluation at every row's Euler prediction
-                    launch_heun_predict(dst, w.ring.as<float>(), w.eps.as<float>(), w.A.as<float>(),
-                                        w.B.as<float>(), pc, BD, w.xt.as<float>(), st);
-                    d->forward(src2, w.eps2.as<float>(), w.scratch.as<float>(), st);
-                    launch_heun_combine(dst, w.eps.as<float>(), w.eps2.as<float>(), pc, T, BD, st);
+            need -= in_flight;
+            if (issued + need > T) need = T - issued;
+            if (need > 0) {
+                tm.mark(-1);
+                for (int it = 0; it < need; ++it) {
+                    if (it == need - 1) PD_HIP(hipEventRecord(w.batch_event, st));
+                    d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
+                    if (s->heun) {   // second evaluation at every row's Euler prediction
+                        launch_heun_predict(dst, w.ring.as<float>(), w.eps.as<float>(),
+                                            w.A.as<float>(), w.B.as<float>(), pc, BD,
+                                            w.xt.as<float>(), st);
+                        d->forward(src2, w.eps2.as<float>(), w.scratch.as<float>(), st);
+                        launch_heun_combine(dst, w.eps.as<float>(), w.eps2.as<float>(), pc, T, BD,
+                                            st);
+                    }
+                    tm.mark(CAT_DENOISER);
+                    const bool fused = launch_picard_scan(
+                        dst, w.ring.as<float>(), w.eps.as<float>(), w.noise.as<float>(),
+                        w.A.as<float>(), w.B.as<float>(), w.Rt.as<float>(), w.St.as<float>(), pc,
+                        batch, d->D, w.partials.as<float>(), fin, st);
+                    tm.mark(CAT_UPDATE);
+                    if (!fused) {
+                        launch_picard_finalize(fin, st);
+                        tm.mark(CAT_FINALIZE);
+                    }
                 }
-                tm.mark(CAT_DENOISER);
-                const bool fused = launch_picard_scan(
-                    dst, w.ring.as<float>(), w.eps.as<float>(), w.noise.as<float>(),
-                    w.A.as<float>(), w.B.as<float>(), w.Rt.as<float>(), w.St.as<float>(), pc, batch,
-                    d->D, w.partials.as<float>(), fin, st);
-                tm.mark(CAT_UPDATE);
-                if (!fused) {
-                    launch_picard_finalize(fin, st);
-                    tm.mark(CAT_FINALIZE);
-                }
+                issued += need;
+                // x_T's slot, copied out after every batch so that the last
+                // one needs no further round trip (earlier copies are
+                // overwritten)
+                PD_HIP(hipMemcpyAsync(x_out, xT, sizeof(float) * BD, hipMemcpyDeviceToDevice, st));
+                // every iteration but the batch's last has run: decide the
+                // next batch while that one runs
+                PD_HIP(hipEventSynchronize(w.batch_event));
+            } else if (in_flight > 0) {
+                PD_HIP(hipStreamSynchronize(st));   // the queued ones may finish the loop
+            } else {
+                fail(PD_ERR_DEVICE, "Picard loop did not terminate within T iterations");
             }
-            issued += need;
-            // x_T's slot, copied out after every batch so that the last one
-            // needs no further round trip (earlier copies are overwritten)
-            PD_HIP(hipMemcpyAsync(x_out, xT, sizeof(float) * BD, hipMemcpyDeviceToDevice, st));
-            PD_HIP(hipStreamSynchronize(st));     // the finalize steps wrote the state's host copy
-            if (w.h_state->status != PD_OK) fail(PD_ERR_NUMERIC, "non-finite point or error in the window");
-            t_host = w.h_state->t;
-            k_host = w.h_state->k;
-            if (t_host >= T) break;
-            if (issued >= T) fail(PD_ERR_DEVICE, "Picard loop did not terminate within T iterations");
+            k_host = hs->k;
+            t_host = hs->t;
+            if (t_host >= T || hs->status != PD_OK) break;
         }
+        PD_HIP(hipStreamSynchronize(st));     // every queued launch and the copy of x_T
+        if (w.h_state->status != PD_OK) fail(PD_ERR_NUMERIC, "non-finite point or error in the window");
+        if (w.h_state->t < T) fail(PD_ERR_DEVICE, "Picard loop did not reach T");
         const int iters = w.h_state->k;
         const int64_t evals = w.h_state->evals;
         tm.collect();
