@@ -74,7 +74,7 @@ const char* pd_version(void);
  *     corresponding DDPM SDE, footnote in Sec. 3.1).
  *   PD_DDIM_HEUN: the PD_DDIM chain with eta = 0 (required), integrated with
  *     Heun's method instead of its Euler step (Sec. 3.3: any solver can supply
- *     the drift of Algorithm 1's lines 5-6).  With the DDIM step as the Euler
+ *     the drift of Algorithm 1).  With the DDIM step as the Euler
  *     prediction x~ = x + (A_i x + B_i eps(x, n_i)), the drift of every step
  *     but the last is y_i = A_i x + (B_i / 2) (eps(x, n_i) + eps(x~, n_{i+1}));
  *     the last step (to abar = 1, no network timestep) keeps the DDIM drift.
@@ -130,7 +130,7 @@ pd_status pd_schedule_tables(const pd_schedule* s, int32_t* T, float* A, float* 
 pd_status pd_schedule_multistep_tables(const pd_schedule* s, float* R, float* S);
 
 /* ------------------------------------------------------------------ denoiser
- * The network of Algorithm 1's drift line, as an epsilon predictor
+ * The network behind Algorithm 1's drift, as an epsilon predictor
  * eps(x, n).  The paper's trained networks are replaced by three synthetic
  * families with the shapes of its workloads:
  *  PD_MODEL_GMM2D   exact epsilon of an equal-weight mixture of isotropic

@@ -9,9 +9,9 @@ up-front noise.
 sequential()  -- the chain x_{i+1} = h_i(x_i) = x_i + y_i + z_i (Sec. 3, the
                  nested-function view of sequential sampling), drift form.
 drifts()      -- y_i of a batch of steps: Euler (the DDPM/DDIM step), Heun's
-                 step on the DDIM ODE (Sec. 3.3: any solver can supply the
-                 drift of lines 5-6; two network evaluations per step, one for
-                 the last), or DPM-Solver++(2M), whose drift also reads the
+                 step on the DDIM ODE (Sec. 3.3: any solver can supply
+                 Algorithm 1's drift; two network evaluations per step, one
+                 for the last), or DPM-Solver++(2M), whose drift also reads the
                  previous step's point and epsilon (Picard evaluates the point
                  before the window once per iteration for it).
 sequential_mean_form() -- the same chain through the textbook step means
@@ -25,7 +25,7 @@ picard()      -- Algorithm 1, step for step, on the whole trajectory array:
                  tau^2 sigma^2 (else p), new points initialised to the window's
                  last point, t += stride, p = min(p, T - t).
 
-Readings of the text that Algorithm 1 leaves open (each repeated in the design doc):
+Readings of the text that Algorithm 1 leaves open:
 * the sigma in the stride test is that of the point's own absolute step,
   sigma^2_{t+j} (``tol_offset=0``); ``tol_offset=-1`` selects sigma^2_{t+j-1};
 * "error > tol" fails, equality passes, and a NaN error fails;
