@@ -1,13 +1,15 @@
 // Picard update, error check and window slide of Algorithm 1 on the device.
 //
 // The window x_t .. x_{t+p} lives in a ring of p+1 trajectory slots,
-// slot(m) = m mod (p+1).  The frontier f is the highest index that holds a
-// computed point; every point past f equals x_f (the new points of Algorithm
-// 1 are copies of the window's last point), so they are read from slot(f)
-// and never copied.  The loop state (t, k, f, p_eff) stays on the device: the
-// finalize kernel of one iteration writes the row descriptors (ring slot and
+// slot(m) = m mod (p+1) (p+2 for the multistep drift, which also keeps
+// x_{t-1}).  The frontier f is the highest index that holds a computed
+// point; every point past f equals x_f (the new points of Algorithm 1 are
+// copies of the window's last point), so they are read from slot(f) and
+// never copied.  The loop state (t, k, f, p_eff) stays on the device: the
+// finalize step of one iteration writes the row descriptors (ring slot and
 // network timestep of every window point) that the next iteration's denoiser
-// and scan read, so no host round trip is needed between iterations.
+// and scan read, so no host round trip is needed between iterations; it also
+// copies the state into mapped host memory for the host's batch decisions.
 #include <type_traits>
 
 #include "pd_internal.h"
@@ -263,7 +265,11 @@ __global__ __launch_bounds__(1024) void k_picard_finalize(FinalizeArgs a, int nb
 // per lane over its columns, transposed through LDS and reduced per window
 // offset into per-block partial sums partials[b][o][blk]; offset 0 (never
 // tested) carries the count of non-finite points in the window's last row
-// (a non-finite point in any other row makes its error non-finite).
+// (a non-finite point in any other row makes its error non-finite).  With
+// DPM, a second-order step's drift also adds R x_{i-1} + S eps_{i-1}: the
+// previous row's point and epsilon, or for a wave's first row the ones
+// before it (for the window's first row, the history row x_{t-1} that the
+// batch evaluated first).
 template <int R, int VEC, bool NOISE, bool DPM>
 __global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
     const LoopState* __restrict__ st, float* ring, const float* __restrict__ eps,
