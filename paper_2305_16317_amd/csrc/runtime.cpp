@@ -626,6 +626,14 @@ static void check_sample_args(const pd_schedule* s, const pd_denoiser* d, int32_
     require(x_out != nullptr, "x_out must not be NULL");
 }
 
+// Waits for the sampling stream when a sampler leaves, also by an error:
+// declared after the workspace it uses, it runs before a workspace made for
+// the call is freed, so no queued kernel or copy outlives its buffers.
+struct StreamDrain {
+    hipStream_t s;
+    ~StreamDrain() { (void)hipStreamSynchronize(s); }
+};
+
 static pd_workspace* use_workspace(pd_workspace* ws, std::unique_ptr<pd_workspace>& own,
                                    const pd_schedule* s, const pd_denoiser* d, int p, int batch) {
     if (ws) {
@@ -708,6 +716,7 @@ extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoise
         const hipStream_t st = static_cast<hipStream_t>(stream);
         std::unique_ptr<pd_workspace> own;
         pd_workspace& w = *use_workspace(ws, own, s, d, 1, batch);
+        const StreamDrain drain{st};
         const int64_t BD = (int64_t)batch * d->D;
         float* x = w.ring.as<float>();
         KernelTimer tm;
@@ -775,6 +784,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         const hipStream_t st = static_cast<hipStream_t>(stream);
         std::unique_ptr<pd_workspace> own;
         pd_workspace& w = *use_workspace(ws, own, s, d, pc, batch);
+        const StreamDrain drain{st};
         const int64_t BD = (int64_t)batch * d->D;
         const float tau2 = tau * tau;
         LoopState* dst = w.state.as<LoopState>();
