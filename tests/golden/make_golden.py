@@ -9,7 +9,8 @@ For every workload it stores, as JSON: the iteration count K, the stride of
 every iteration, the model evaluations, the squared norm of the sample (float64
 sum of the float32 values) and the sample's values at 4096 fixed indices
 (every index for samples smaller than that), for the Picard sampler and, where
-listed, for the sequential sampler.  Runs in float32 (the device path's
+listed, for the sequential sampler and for Picard with the sigma^2_{t+j-1}
+reading of the stride test.  Runs in float32 (the device path's
 precision, which also decides the strides); the bf16 workload uses the
 oracle's bf16-operand mode.
 """
@@ -29,6 +30,8 @@ from oracle import Problem  # noqa: E402
 N_SAMPLE = 4096
 SEQUENTIAL = {"gmm2d_ddpm100", "policy_mlp_ddpm100", "latent_ddpm1000_p64",
               "policy_mlp_dpm15", "latent_dpm200_p64"}
+# also run with the sigma^2_{t+j-1} reading of the stride test
+TOL_OFFSET_M1 = {"latent_ddpm1000_p64", "policy_mlp_ddpm100"}
 
 
 def sample_indices(n: int) -> np.ndarray:
@@ -56,6 +59,12 @@ def run(name: str) -> dict:
            "picard": {"iters": r.iters, "evals": r.evals, "trace": r.trace, **summarize(r.x)},
            "picard_seconds": time.time() - t0}
     print(name, "picard K", r.iters, "evals", r.evals, "%.1fs" % (time.time() - t0), flush=True)
+    if name in TOL_OFFSET_M1:
+        t0 = time.time()
+        r1 = pr.picard(tol_offset=-1)
+        out["picard_tol_offset_m1"] = {"iters": r1.iters, "evals": r1.evals, "trace": r1.trace,
+                                       **summarize(r1.x)}
+        print(name, "picard (tol_offset -1) K", r1.iters, "%.1fs" % (time.time() - t0), flush=True)
     if name in SEQUENTIAL:
         t0 = time.time()
         xs = pr.sequential()

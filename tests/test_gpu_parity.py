@@ -357,6 +357,16 @@ def test_full_size_sequential_matches_oracle(name):
     _check_summary(got, g["sequential"], REL_F32)
 
 
+@pytest.mark.parametrize("name", ["latent_ddpm1000_p64", "policy_mlp_ddpm100"])
+def test_full_size_tolerance_offset_matches_oracle(name):
+    """The sigma^2_{t+j-1} reading of the stride test at full size."""
+    g = _golden(name)["picard_tol_offset_m1"]
+    wl = W.WORKLOADS[name]
+    got, st = _run(wl, W.make_weights(wl.model), tol_offset=-1)
+    assert (st.iters, st.trace, st.evals_per_sample) == (g["iters"], g["trace"], g["evals"])
+    _check_summary(got, g, REL_F32)
+
+
 def test_full_size_bf16_picard_matches_oracle():
     """Guided bf16 workload at full size (4x96x96, width 320, T=1000, p=128):
     sampled outputs and the norm within 2e-2 of the oracle run with the same
@@ -462,3 +472,28 @@ def test_dpm_sequential_matches_oracle_and_window_of_one(name):
     one, st1 = _run(wl, w, "picard", p=1)
     assert st1.iters == T and st1.evals_per_sample == 2 * T - 1
     assert np.array_equal(one.view(np.uint32), seq.view(np.uint32))
+
+
+@pytest.mark.parametrize("name,table", [("dpm_conv", "DPM"), ("dpm_mlp", "DPM"),
+                                        ("heun_conv", "HEUN")])
+def test_multistep_and_heun_workspace_reuse(name, table):
+    """A workspace reused across calls (its ring and state hold the previous
+    call's end) gives each call's fresh-workspace result bit for bit."""
+    wl = (DPM if table == "DPM" else HEUN)[name]()
+    w = W.make_weights(wl.model)
+    sched, den = pd.from_workload(wl, w)
+    ws = pd.pd_workspace_create(sched, den, wl.p, wl.batch)
+    x = torch.empty(wl.batch * wl.model.D, device="cuda")
+    for seed in (0, 3, 0):
+        ref, sr = _run(wl, w, seed=seed)
+        st = pd.pd_sample_picard(sched, den, wl.p, wl.tau, seed, wl.batch, wl.model.sample_shape, x,
+                                 workspace=ws)
+        torch.cuda.synchronize()
+        got = x.cpu().numpy().reshape(wl.batch, -1)
+        assert np.array_equal(got.view(np.uint32), ref.view(np.uint32)), seed
+        assert (st.iters, st.trace, st.evals_per_sample) == (sr.iters, sr.trace, sr.evals_per_sample)
+        seq_ref, _ = _run(wl, w, "sequential", seed=seed)
+        pd.pd_sample_sequential(sched, den, seed, wl.batch, wl.model.sample_shape, x, workspace=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(x.cpu().numpy().reshape(wl.batch, -1).view(np.uint32),
+                              seq_ref.view(np.uint32)), seed
