@@ -213,7 +213,15 @@ def sweep(a) -> int:
             got = x.double().cpu().numpy()
             dist.append(float(np.linalg.norm(got - seq[s]) / max(np.linalg.norm(seq[s]), 1e-300)))
         med = float(np.median(lat))
+        # the decomposition of the paper's window plots: evaluations per step
+        # (algorithm inefficiency) against evaluations per unit time relative
+        # to the sequential sampler (hardware efficiency); their ratio is the
+        # speed-up
+        ev = float(np.mean(evals))
+        alg = ev / T
+        hw = (ev / med) / (T / seq_med)
         print(json.dumps({"sweep": a.sweep, "workload": wl.name, "value": v, "p": p, "tau": tau,
+                          "algorithm_inefficiency": alg, "hardware_efficiency": hw,
                           "tol_index_offset": a.tol_offset, "seeds": len(seeds),
                           "K_mean": float(np.mean(ks)), "K_range": [min(ks), max(ks)],
                           "evals_mean": float(np.mean(evals)), "latency_ms_median": med,
