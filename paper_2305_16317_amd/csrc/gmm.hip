@@ -121,8 +121,6 @@ __device__ __forceinline__ float* gmm_stage(const GmmLoopArgs& g, float* sm, Gmm
     return t.means + 2 * K;
 }
 
-__device__ __forceinline__ size_t gmm_stage_floats(int T, int K) { return 6 * (size_t)T + 2 * K; }
-
 // Algorithm 1 for the 2-D mixture in one workgroup, start to finish: the
 // step tables, the window ring, the drift batch, the new points and the
 // noise live in LDS, the loop state in registers, and one launch runs every
