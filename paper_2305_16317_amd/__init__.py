@@ -11,7 +11,6 @@ from __future__ import annotations
 
 import ctypes
 import dataclasses
-import math
 import os
 from typing import Dict, List, Optional, Sequence
 
