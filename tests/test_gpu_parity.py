@@ -367,6 +367,27 @@ def test_full_size_tolerance_offset_matches_oracle(name):
     _check_summary(got, g, REL_F32)
 
 
+def test_full_size_headline_in_bench_configuration():
+    """The 4x96x96 DDPM T=1000, p=64 sample run as bench.py times it: a workspace
+    made once, the current torch stream, per-kernel events on, then a second
+    call on the same workspace with events off; both match the oracle's
+    golden (K, strides, evaluations, sampled values)."""
+    name = "latent_ddpm1000_p64"
+    g = _golden(name)["picard"]
+    wl = W.WORKLOADS[name]
+    sched, den = pd.from_workload(wl, W.make_weights(wl.model))
+    ws = pd.pd_workspace_create(sched, den, wl.p, wl.batch)
+    x = torch.empty(wl.batch * wl.model.D, device="cuda")
+    stream = torch.cuda.current_stream()
+    for timed in (True, False):
+        st = pd.pd_sample_picard(sched, den, wl.p, wl.tau, wl.noise_seed, wl.batch,
+                                 wl.model.sample_shape, x, workspace=ws, stream=stream,
+                                 time_kernels=timed)
+        torch.cuda.synchronize()
+        assert (st.iters, st.trace, st.evals_per_sample) == (g["iters"], g["trace"], g["evals"])
+        _check_summary(x.cpu().numpy().reshape(wl.batch, -1), g, REL_F32)
+
+
 def test_full_size_bf16_picard_matches_oracle():
     """Guided bf16 workload at full size (4x96x96, width 320, T=1000, p=128):
     sampled outputs and the norm within 2e-2 of the oracle run with the same
