@@ -227,6 +227,20 @@ def test_picard_bf16_matches_oracle(name):
     assert abs(st.iters - ref.iters) <= max(1, ref.iters // 10), (st.iters, ref.iters)
 
 
+@pytest.mark.parametrize("name", list(BF16))
+def test_sequential_bf16_matches_oracle(name):
+    """bf16 denoiser, sequential chain: within 2e-2 of the oracle run with the
+    same bf16 operand rounding, and Picard with p = 1 gives it bit for bit."""
+    wl = BF16[name]()
+    w = W.make_weights(wl.model)
+    got, st = _run(wl, w, "sequential")
+    ref = Problem(wl, w, np.float32).sequential()
+    assert st.evals_per_sample == wl.schedule.T and st.network_rows == 2 * wl.schedule.T
+    assert _rel(got, ref) <= 2e-2, _rel(got, ref)
+    one, _ = _run(wl, w, "picard", p=1)
+    assert np.array_equal(one.view(np.uint32), got.view(np.uint32))
+
+
 @pytest.mark.parametrize("name", list(SMALL))
 def test_picard_matches_oracle(name):
     wl = SMALL[name]()
