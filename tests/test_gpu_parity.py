@@ -182,6 +182,8 @@ SMALL = {
     "gmm_k40": lambda: W.small_variant("gmm2d_ddpm100", p=33, batch=5, n_components=40),
     "mlp_full": lambda: W.WORKLOADS["policy_mlp_ddpm100"],
     "mlp_small": lambda: W.small_variant("policy_mlp_ddpm100", T=30, p=9, shape=(4, 3), width=32, batch=2),
+    # eight samples sharing the window: 40-row layer launches, any-of-batch strides
+    "mlp_b8": lambda: W.small_variant("policy_mlp_ddpm100", T=40, p=5, shape=(8, 6), width=64, batch=8),
     "conv_ddpm": lambda: W.small_variant("latent_ddpm1000_p64", T=40, p=16, shape=(4, 16, 16), width=64),
     "conv_ddpm_w320": lambda: W.small_variant("latent_ddpm1000_p64", T=60, p=32, shape=(4, 8, 12), width=320),
     "conv_ddim_b3": lambda: W.small_variant("latent_ddim200_b4", T=30, p=8, shape=(4, 6, 7), width=32, batch=3),
