@@ -140,3 +140,48 @@ def test_denoiser_argument_validation_precedes_device():
     with pytest.raises(pd.PdError) as e:
         pd.pd_denoiser_create(pd.PD_MODEL_CONV1X1, (4, 8, 8), conv, s, width=96)
     assert e.value.code == pd.PD_ERR_UNSUPPORTED
+
+
+C_PROGRAM = r"""
+#include <stdio.h>
+#include "paradigms.h"
+
+int main(void) {
+    pd_schedule_desc d = {PD_DDPM, 1000, 1000, 0, 1e-4, 0.02, 0.0};
+    pd_schedule* s = NULL;
+    if (pd_init_schedule(&d, &s) != PD_OK) { printf("init: %s\n", pd_last_error()); return 1; }
+    int32_t T = 0;
+    float A[1000], B[1000];
+    if (pd_schedule_tables(s, &T, A, B, NULL, NULL, NULL) != PD_OK) return 2;
+    d.T = 0;                              /* invalid: reported, no abort */
+    pd_schedule* bad = NULL;
+    const pd_status st = pd_init_schedule(&d, &bad);
+    printf("%d %.9g %.9g %d %s\n", T, A[0], B[0], st, st == PD_ERR_INVALID_ARG ? "ok" : "no");
+    pd_destroy_schedule(s);
+    return 0;
+}
+"""
+
+
+def test_plain_c_program_builds_and_runs(tmp_path):
+    """The header is plain C and the library links into a C program: the
+    schedule calls need no GPU, and an invalid argument comes back as a status."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use.c"
+    src.write_text(C_PROGRAM)
+    exe = tmp_path / "use"
+    libdir = os.path.dirname(pd.lib_path())
+    r = subprocess.run([cc, "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"),
+                        str(src), "-L", libdir, "-lparadigms", f"-Wl,-rpath,{libdir}",
+                        "-o", str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stdout + r.stderr
+    T, A0, B0, status, ok = r.stdout.split()
+    tb = pd.pd_init_schedule(pd.PD_DDPM, 1000, 1000).tables()
+    assert int(T) == 1000 and ok == "ok" and int(status) == pd.PD_ERR_INVALID_ARG
+    assert np.float32(float(A0)) == tb["A"][0] and np.float32(float(B0)) == tb["B"][0]
