@@ -1,30 +1,28 @@
 // Per-pixel 4-layer stack (a stack of 1x1 convolutions) of the latent
-// denoiser, fused into one kernel on fp32 MFMA (v_mfma_f32_32x32x2f32).
+// denoiser, fused into one kernel: k_conv_f32x6 for the fp32 network,
+// k_conv_bf16 for the network with bf16 matmul operands.
 //
-// Each wave owns a tile of 32 pixels of one sample and runs all four layers
-// on it with the activations held in registers.  Layers are computed
-// transposed, out^T = W h^T: the MFMA's M dimension is the output feature
-// and its N dimension the pixel, so the 32x32 accumulator of output block nb
-// holds, in lane l and register r, feature 32 nb + 8 (r/4) + 4 (l/32) + r%4
-// of pixel l%32.  The B operand of the next layer needs, in lane l, one
-// input feature of pixel l%32 per lane half -- exactly what a single
-// accumulator register already holds.  So register r of block b is used
-// unchanged as the B operand of k-step (b, r), and the weights are packed on
-// the host with the same permutation of the reduction index: k-step (b, r)
-// pairs input feature 32 b + 8 (r/4) + 4 h + r%4 with lane half h.  No
+// Both share one design.  Each wave owns a tile of 32 pixels of one sample
+// and runs all four layers on it with the activations held in registers.
+// Layers are computed transposed, out^T = W h^T: the MFMA's M dimension is the
+// output feature and its N dimension the pixel.  Every 32x32 MFMA leaves
+// D[i][j] in lane j + 32 ((i/4) % 2), register (i%4) + 4 (i/8), so the
+// accumulator of output block nb holds, in lane l and register r, feature
+// 32 nb + 8 (r/4) + 4 (l/32) + r%4 of pixel l%32.  On
+// v_mfma_f32_32x32x16_bf16 (A[i][k] in lane i + 32 (k/8), B[k][j] in lane
+// j + 32 (k/8), element k%8 of 8 packed bf16) accumulator registers
+// 8 g2 .. 8 g2 + 7 of block b, converted to bf16 and packed, are exactly the
+// B operand of k-step (b, g2) of the next layer: lane half h then carries
+// input features 32 b + 16 g2 + 8 (u/4) + 4 h + u%4, u = 0..7, and the host
+// packs the weights with the same permutation of the reduction index.  No
 // activation ever leaves the registers.
 //
-// v_mfma_f32_32x32x2f32 (wave64): A[i][k] in lane i + 32 k, B[k][j] in lane
-// j + 32 k, D[i][j] in lane j + 32 ((i/4) % 2), register (i%4) + 4 (i/8).
-//
-// Weights stream through LDS in slabs shared by the block's 4 waves, double
+// Weights stream through LDS in slabs shared by a block's waves, double
 // buffered: the next slab is copied global -> LDS by the gfx950 LDS-DMA path
 // (global_load_lds_dwordx4, no registers involved) while the current one
-// feeds the MFMAs.  Slab order: layer 1 (all of it), layer 2 one input block
-// at a time, layer 3 likewise, layer 4 (all of it, output rows padded to 32).
-// Inside a mid-layer slab for input block b, fragment (g, nb) of lane l holds
-// float4 {W[32 nb + l%32][32 b + 8 g + 4 (l/32) + q] : q = 0..3}, so one
-// ds_read_b128 feeds four MFMAs.
+// feeds the MFMAs.  The two buffers are separate LDS variables: with one
+// array of two buffers the compiler cannot tell a read of one buffer from a
+// copy into the other, and waits for every copy to land before the next read.
 #include <cstring>
 #include <utility>
 
@@ -48,17 +46,6 @@ __device__ __forceinline__ void static_for(F&& f) {
     static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-template <int NB, int C>
-struct ConvLayout {
-    static constexpr int KS1 = C / 2;                 // layer-1 k-steps
-    static constexpr int SL1 = (NB * 64 * KS1 + 255) / 256 * 256;  // layer-1 slab, 1 KB multiple
-    static constexpr int SLM = 16 * NB * 64;          // floats in every other slab
-    static constexpr int NSLAB = 2 + 2 * NB;
-    static constexpr int TOTAL = SL1 + (2 * NB + 1) * SLM;
-    static constexpr __host__ __device__ int off(int i) { return i == 0 ? 0 : SL1 + (i - 1) * SLM; }
-    static constexpr __host__ __device__ int size(int i) { return i == 0 ? SL1 : SLM; }
-};
-
 __device__ __forceinline__ float silu(float v) {
     return v * __builtin_amdgcn_rcpf(1.0f + __expf(-v));
 }
@@ -78,257 +65,10 @@ struct ActVecs {
     static constexpr int F4 = ROWS * STRIDE / 4;
 };
 
-// Blocks are persistent: each loops over groups of 4 tiles (one per wave),
-// and the next pass's first weight slab is copied during the current pass's
-// last layer, so a tile starts without waiting for weights.
-//
-// Activations at a layer transition: only block 0 of the new activations is
-// computed up front; the next layer's first slab consumes block 0 alone, so
-// the SiLU of blocks 1..NB-1 is spread over that slab's MFMAs (the old
-// accumulators of those blocks stay live instead of their activations, which
-// costs no extra registers).  fp32 MFMAs do not co-issue with VALU work on
-// this GPU, so this spreads the SiLU between the MFMAs rather than hiding it;
-// it keeps the matrix core fed without a burst of dependent VALU work.
-template <int S, int NB>
-struct Spread {   // block k in [lo(s), hi(s)) is activated after MFMA slot s of S
-    static constexpr __device__ int lo(int s) { return 1 + (s * (NB - 1)) / S; }
-    static constexpr __device__ int hi(int s) { return 1 + ((s + 1) * (NB - 1)) / S; }
-};
-
-template <int NB, int C>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void k_conv_f32(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
-    using L = ConvLayout<NB, C>;
-    constexpr int NBP = (NB + 1) / 2;                        // output-block pairs
-    constexpr int SLOTS = 4 * NBP;                           // MFMA slots of a mid slab
-    using SP = Spread<SLOTS, NB>;
-    using AV = ActVecs<NB, 4>;
-    __shared__ f4 lds[2][L::SLM / 4];
-    __shared__ f4 vec4[AV::F4];
-
-    const int groups = src.active ? *src.active : src.max_groups;
-    const int64_t ntiles = (int64_t)groups * src.group * tiles_per_row;
-    const int64_t ngroups = (ntiles + 3) / 4;
-    if ((int64_t)blockIdx.x >= ngroups) return;              // uniform over the block
-
-    // the wave index is uniform: tile bookkeeping stays in scalar registers
-    const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int64_t P = a.P;
-
-    // slab i -> LDS buffer `buf`: 1 KB per wave instruction, 16 B per lane
-    auto dma = [&](int i, int buf) {
-        const int nch = L::size(i) / 256;
-        // base and lane offset are made opaque at every call so the addresses
-        // are formed here as SGPR base + 32-bit lane offset (the saddr form)
-        // instead of being hoisted out of the loops into 64-bit VGPRs
-        const char* gb = reinterpret_cast<const char*>(a.frags);
-        uint32_t lo = (uint32_t)lane * 16u;
-        asm volatile("" : "+s"(gb), "+v"(lo));
-        float* ls = reinterpret_cast<float*>(lds[buf]);
-        for (int c = wave; c < nch; c += 4) {
-            const uint32_t ob = (uint32_t)(L::off(i) + c * 256) * 4u + lo;
-            __builtin_amdgcn_global_load_lds(
-                (const __attribute__((address_space(1))) void*)(gb + (size_t)ob),
-                (__attribute__((address_space(3))) void*)(ls + c * 256), 16, 0, 0);
-        }
-    };
-    auto land = [&]() {          // this wave's copies are in LDS, then all waves sync
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-    };
-    // first-layer shift of the next pass (tile row n, branch br) -> this wave's row
-    auto dma_shift = [&](int n, int br) {
-        const float* row = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * AV::W;
-        float* dst = reinterpret_cast<float*>(vec4) + wave * AV::STRIDE;
-        for (int c = 0; c < AV::STRIDE / 256; ++c) {
-            int off = c * 256 + lane * 4;
-            off = off <= AV::W - 4 ? off : AV::W - 4;      // lanes past the row re-read its end
-            __builtin_amdgcn_global_load_lds(
-                (const __attribute__((address_space(1))) void*)(row + off),
-                (__attribute__((address_space(3))) void*)(dst + c * 256), 16, 0, 0);
-        }
-    };
-    // SiLU(acc + v) for block nb, v = LDS vector row `vrow`: the 4 features of
-    // register group q4 are contiguous
-    auto act = [&](const f16v& c, int vrow, int nb) -> f16v {
-        // opaque per call: keeps these reads next to their use instead of
-        // hoisted out of the tile loop (the bias rows do not change)
-        int o = vrow * (AV::STRIDE / 4);
-        asm volatile("" : "+s"(o));
-        f16v h;
-        static_for<4>([&](auto q4c) {
-            constexpr int q4 = decltype(q4c)::value;
-            const f4 sh = vec4[o + 8 * nb + 2 * q4 + half];
-            static_for<4>([&](auto qc) {
-                constexpr int q = decltype(qc)::value;
-                h[4 * q4 + q] = silu(c[4 * q4 + q] + sh[q]);
-            });
-        });
-        return h;
-    };
-    struct Tile {
-        int64_t row, px;
-        bool active, pxok;
-        const float* x;
-        int n;
-    };
-    auto locate = [&](int64_t tg) -> Tile {
-        Tile T;
-        const int64_t tile = tg * 4 + wave;
-        T.active = tile < ntiles;
-        const int64_t tt = T.active ? tile : ntiles - 1;     // idle waves redo the last tile
-        T.row = tt / tiles_per_row;
-        const int pt = (int)(tt % tiles_per_row);
-        const int g = (int)(T.row / src.group), bb = (int)(T.row % src.group);
-        // per-wave values loaded from memory: uniform by construction
-        const int64_t sl = src.slot ? __builtin_amdgcn_readfirstlane(src.slot[g]) : g;
-        T.x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
-        T.n = __builtin_amdgcn_readfirstlane(src.n[g]);
-        T.px = (int64_t)pt * 32 + (lane & 31);
-        T.pxok = T.px < P;
-        return T;
-    };
-    const int nbranch = a.shift_c ? 2 : 1;
-
-    Tile cur = locate(blockIdx.x);
-    dma(0, 0);
-    dma_shift(cur.n, 0);
-    for (int i = tid; i < AV::W; i += 256) {
-        reinterpret_cast<float*>(vec4)[AV::B2 * AV::STRIDE + i] = a.b2[i];
-        reinterpret_cast<float*>(vec4)[AV::B3 * AV::STRIDE + i] = a.b3[i];
-    }
-    land();
-    float xin[L::KS1];
-#pragma unroll
-    for (int s = 0; s < L::KS1; ++s) xin[s] = cur.pxok ? cur.x[(2 * s + half) * P + cur.px] : 0.f;
-
-    for (int64_t tg = blockIdx.x; tg < ngroups; tg += gridDim.x) {
-        const bool last_group = tg + gridDim.x >= ngroups;
-        // the next group's input, fetched while this one computes
-        Tile nxt = locate(last_group ? tg : tg + gridDim.x);
-        float xnx[L::KS1];
-#pragma unroll
-        for (int s = 0; s < L::KS1; ++s) xnx[s] = nxt.pxok ? nxt.x[(2 * s + half) * P + nxt.px] : 0.f;
-
-        float eu[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int br = 0; br < nbranch; ++br) {
-            f16v acc[NB], H[NB];
-
-            // ---- layer 1 (slab 0, buffer 0): K = C
-            dma(1, 1);
-            static_for<NB>([&](auto nbc) {
-                constexpr int nb = decltype(nbc)::value;
-                acc[nb] = f16v{};
-                const float* f1 = reinterpret_cast<const float*>(lds[0]) + (nb * 64 + lane) * L::KS1;
-                static_for<L::KS1>([&](auto sc) {
-                    constexpr int s = decltype(sc)::value;
-                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(f1[s], xin[s], acc[nb], 0, 0, 0);
-                });
-            });
-
-            // ---- layers 2 and 3: one slab per input block
-            static_for<2>([&](auto lc) {
-                constexpr int layer = decltype(lc)::value;
-                const int vin = layer == 0 ? wave : AV::B2;   // shift of the activation
-                H[0] = act(acc[0], vin, 0);
-                f16v nacc[NB];
-                static_for<NB>([&](auto nbc) { nacc[decltype(nbc)::value] = f16v{}; });
-                static_for<NB>([&](auto bc) {
-                    constexpr int b = decltype(bc)::value;
-                    constexpr int slab = 1 + layer * NB + b;
-                    constexpr int buf = slab & 1;
-                    if (b == 0) land();                          // slab 1 / NB+1 has landed
-                    dma(slab + 1, buf ^ 1);
-                    static_for<4>([&](auto gc) {
-                        constexpr int g4 = decltype(gc)::value;
-                        static_for<NBP>([&](auto pc) {
-                            constexpr int nb = 2 * decltype(pc)::value;
-                            const f4 w0 = lds[buf][(g4 * NB + nb) * 64 + lane];
-                            const f4 w1 = nb + 1 < NB ? lds[buf][(g4 * NB + nb + 1) * 64 + lane] : f4{};
-                            static_for<4>([&](auto qc) {
-                                constexpr int q = decltype(qc)::value;
-                                nacc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                                    w0[q], H[b][4 * g4 + q], nacc[nb], 0, 0, 0);
-                                if constexpr (nb + 1 < NB)
-                                    nacc[nb + 1] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                                        w1[q], H[b][4 * g4 + q], nacc[nb + 1], 0, 0, 0);
-                            });
-                            if constexpr (b == 0) {              // deferred activations
-                                constexpr int slot = g4 * NBP + nb / 2;
-                                static_for<NB>([&](auto kc) {
-                                    constexpr int k = decltype(kc)::value;
-                                    if constexpr (k >= SP::lo(slot) && k < SP::hi(slot))
-                                        H[k] = act(acc[k], vin, k);
-                                });
-                            }
-                        });
-                    });
-                    if (b + 1 < NB) land();
-                });
-                static_for<NB>([&](auto nbc) { acc[decltype(nbc)::value] = nacc[decltype(nbc)::value]; });
-            });
-
-            // ---- layer 4 (slab 2NB+1, buffer 1): C outputs, 4 chains of MFMAs
-            {
-                constexpr int slab = 1 + 2 * NB;
-                constexpr int buf = slab & 1;
-                land();
-                const bool more = br + 1 < nbranch || !last_group;
-                if (more) {                                      // next pass's layer 1
-                    dma(0, 0);
-                    if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
-                    else dma_shift(nxt.n, 0);
-                }
-                H[0] = act(acc[0], AV::B3, 0);
-                f16v o4[4] = {f16v{}, f16v{}, f16v{}, f16v{}};
-                static_for<NB>([&](auto bc) {
-                    constexpr int b = decltype(bc)::value;
-                    static_for<4>([&](auto gc) {
-                        constexpr int g4 = decltype(gc)::value;
-                        const f4 w = lds[buf][(b * 4 + g4) * 64 + lane];
-                        static_for<4>([&](auto qc) {
-                            constexpr int q = decltype(qc)::value;
-                            o4[g4] = __builtin_amdgcn_mfma_f32_32x32x2f32(w[q], H[b][4 * g4 + q],
-                                                                          o4[g4], 0, 0, 0);
-                        });
-                    });
-                    if constexpr (b + 1 < NB) H[b + 1] = act(acc[b + 1], AV::B3, b + 1);
-                });
-                const f16v o = (o4[0] + o4[1]) + (o4[2] + o4[3]);
-                float* out = eps + cur.row * (int64_t)C * P;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int c = 4 * half + r;
-                    if (c < C) {
-                        const float v = o[r] + a.b4[c];
-                        if (br == 0) {
-                            eu[r] = v;
-                            if (nbranch == 1 && cur.active && cur.pxok) out[c * P + cur.px] = v;
-                        } else if (cur.active && cur.pxok) {
-                            out[c * P + cur.px] = eu[r] + a.guidance * (v - eu[r]);
-                        }
-                    }
-                }
-                land();                                          // slab 0 is in buffer 0 again
-            }
-        }
-        cur = nxt;
-#pragma unroll
-        for (int s = 0; s < L::KS1; ++s) xin[s] = xnx[s];
-    }
-}
-
 // ---------------------------------------------------------------- bf16
-// Same transposed design on v_mfma_f32_32x32x16_bf16: A[i][k] holds
-// k = 8 (l/32) + u (u = 0..7) in lane i + 32 (l/32) as 8 packed bf16, B[k][j]
-// likewise in lane j + 32 (k/8), D as for the fp32 instruction.  Accumulator
-// registers 8 g2 .. 8 g2 + 7 of block b, rounded to bf16 and packed, are the
-// B operand of k-step (b, g2): lane half h then carries input features
-// 32 b + 16 g2 + 8 (u/4) + 4 h + u%4, and the packed weights use the same
-// order.  Layer 1 pads K = C to 16 with zeros, layer 4 pads its C output rows
-// to 32.  Every matmul operand is bf16 (round to nearest even); accumulation,
-// bias, shift, SiLU and the guidance combination stay in fp32.
+// k_conv_bf16: every matmul operand is bf16 (round to nearest even);
+// accumulation, bias, shift, SiLU and the guidance combination stay in fp32.
+// Layer 1 pads K = C to 16 with zeros, layer 4 pads its C output rows to 32.
 //
 // A 32x32x16 bf16 MFMA and the SiLU of one accumulator register cost about
 // the same issue time, so the work is arranged for the hardware to overlap
@@ -362,7 +102,9 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
     constexpr int NW = kBf16Waves;
     using AV = ActVecs<NB, NW>;
     static_assert(C <= 8, "layer 1 holds at most 8 channels in one lane half");
-    __shared__ bf8 lds[2][L::BUF];
+    __shared__ bf8 lds_0[L::BUF];
+    __shared__ bf8 lds_1[L::BUF];
+    auto ldsb = [&](int buf) -> bf8* { return buf ? lds_1 : lds_0; };
     __shared__ f4 vec4[AV::F4];
 
     const int groups = src.active ? *src.active : src.max_groups;
@@ -380,7 +122,7 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
         const char* gb = reinterpret_cast<const char*>(a.frags);
         uint32_t lo = (uint32_t)lane * 16u;
         asm volatile("" : "+s"(gb), "+v"(lo));
-        bf8* ls = lds[buf];
+        bf8* ls = ldsb(buf);
         for (int c = wave; c < nch; c += NW) {
             const uint32_t ob = (uint32_t)(L::off(i) + c * 64) * 16u + lo;
             __builtin_amdgcn_global_load_lds(
@@ -476,7 +218,7 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
             dma(1, 1);
             static_for<NB>([&](auto jc) {
                 constexpr int j = decltype(jc)::value;
-                const f16v acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[0][j * 64 + lane], xb, f16v{},
+                const f16v acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_0[j * 64 + lane], xb, f16v{},
                                                                          0, 0, 0);
                 act(acc, wave, j, H[j]);
             });
@@ -496,7 +238,7 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                         constexpr int b = decltype(bc)::value;
                         static_for<2>([&](auto g2c) {
                             constexpr int g2 = decltype(g2c)::value;
-                            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[buf][(b * 2 + g2) * 64 + lane],
+                            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ldsb(buf)[(b * 2 + g2) * 64 + lane],
                                                                           H[b][g2], acc, 0, 0, 0);
                         });
                     });
@@ -525,7 +267,7 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                     constexpr int b = decltype(bc)::value;
                     static_for<2>([&](auto gc) {
                         constexpr int g2 = decltype(gc)::value;
-                        o2[g2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds[buf][(b * 2 + g2) * 64 + lane],
+                        o2[g2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ldsb(buf)[(b * 2 + g2) * 64 + lane],
                                                                          H[b][g2], o2[g2], 0, 0, 0);
                     });
                 });
@@ -549,6 +291,304 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
         }
         cur = nxt;
         xb = xnx;
+    }
+}
+
+// ---------------------------------------------------------------- fp32
+// k_conv_f32x6: the fp32 network with fp32-accurate products on
+// v_mfma_f32_32x32x16_bf16.  Every fp32 operand is split exactly into three
+// bf16 parts, x = x0 + x1 + x2 (x0 the nearest bf16 to x, x1 the nearest to
+// x - x0, x2 = x - x0 - x1, which has at most 8 significant bits), so
+// |x1| <= 2^-8 |x| and |x2| <= 2^-16 |x|.  w x is formed from the six part
+// products down to 2^-16 |w x| (w0x0, w0x1, w1x0, w0x2, w2x0, w1x1); the three
+// left out add up to about 2^-23 |w| |x|, the size of one fp32 rounding.  Each
+// part product is exact in fp32 and the sums are fp32.  A bf16 MFMA does 16
+// times the multiply-adds of an fp32 one in the same time, so the six take
+// 6/16 of the fp32 matrix-core time.
+//
+// Persistent blocks of 4 waves, one per SIMD: a tile's activations and the
+// accumulators of a whole layer fill the register file.  Layer 1 (K = C) runs
+// on fp32 MFMA (v_mfma_f32_32x32x2f32: A[i][k] in lane i + 32 k, B[k][j] in
+// lane j + 32 k, the same accumulator layout); its slab holds, for output
+// block nb and lane l, the C/2 values W1[32 nb + l%32][2 s + l/32].  Layers
+// 2-4 run on the split products: the weights are split on the host, the
+// activations of input block b + 1 are computed and split during the MFMAs of
+// block b.  Mid-layer slab b holds input block b for every output block nb,
+// fragment ((g2 NB + nb) 3 + part), one 16-B unit per lane; layer 4's slab
+// holds fragment ((b 2 + g2) 3 + part) with the C output rows padded to 32.
+typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+typedef float fl2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ fl2 widen(bf2 v) {              // bf16 pair -> fp32 pair, exact
+    const uint32_t w = __builtin_bit_cast(uint32_t, v);
+    return fl2{__builtin_bit_cast(float, w << 16), __builtin_bit_cast(float, w & 0xffff0000u)};
+}
+
+template <int NB, int C>
+struct ConvLayoutX6 {                            // units of 16 B
+    static constexpr int KS1 = C / 2;            // layer-1 fp32 k-steps
+    static constexpr int SL1 = (NB * 64 * KS1 / 4 + 63) / 64 * 64;
+    static constexpr int SLM = 2 * NB * 3 * 64;
+    static constexpr int BUF = SL1 > SLM ? SL1 : SLM;
+    static constexpr int TOTAL = SL1 + (2 * NB + 1) * SLM;
+    // slab 0: layer 1; 1 + layer * NB + b: input block b of layer 2 or 3;
+    // 1 + 2 NB: layer 4
+    static constexpr __host__ __device__ int off(int i) { return i == 0 ? 0 : SL1 + (i - 1) * SLM; }
+    static constexpr __host__ __device__ int size(int i) { return i == 0 ? SL1 : SLM; }
+};
+
+template <int NB, int C>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
+    using L = ConvLayoutX6<NB, C>;
+    using AV = ActVecs<NB, 4>;
+    static_assert(C % 2 == 0 && C <= 8, "layer 1 pairs channels; layer 4 fills one lane half");
+    __shared__ bf8 lds_0[L::BUF];
+    __shared__ bf8 lds_1[L::BUF];
+    auto ldsb = [&](int buf) -> bf8* { return buf ? lds_1 : lds_0; };
+    __shared__ f4 vec4[AV::F4];
+
+    const int groups = src.active ? *src.active : src.max_groups;
+    const int64_t ntiles = (int64_t)groups * src.group * tiles_per_row;
+    const int64_t ngroups = (ntiles + 3) / 4;
+    if ((int64_t)blockIdx.x >= ngroups) return;              // uniform over the block
+
+    const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t P = a.P;
+
+    auto dma = [&](int i, int buf) {                         // slab i -> buffer, 1 KB per wave op
+        const int nch = L::size(i) / 64;
+        const char* gb = reinterpret_cast<const char*>(a.frags);
+        uint32_t lo = (uint32_t)lane * 16u;
+        asm volatile("" : "+s"(gb), "+v"(lo));
+        bf8* ls = ldsb(buf);
+        for (int c = wave; c < nch; c += 4) {
+            const uint32_t ob = (uint32_t)(L::off(i) + c * 64) * 16u + lo;
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(gb + (size_t)ob),
+                (__attribute__((address_space(3))) void*)(ls + c * 64), 16, 0, 0);
+        }
+    };
+    auto land = [&]() {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    };
+    auto dma_shift = [&](int n, int br) {
+        const float* row = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * AV::W;
+        float* dst = reinterpret_cast<float*>(vec4) + wave * AV::STRIDE;
+        for (int c = 0; c < AV::STRIDE / 256; ++c) {
+            int off = c * 256 + lane * 4;
+            off = off <= AV::W - 4 ? off : AV::W - 4;
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(row + off),
+                (__attribute__((address_space(3))) void*)(dst + c * 256), 16, 0, 0);
+        }
+    };
+    // SiLU(acc + v) of block nb (v = LDS vector row vrow) in fp32, split into
+    // the three bf16 parts of the block's two B operands: p[g2][part]
+    auto act_split = [&](const f16v& c, int vrow, int nb, bf8 (&p)[2][3]) {
+        int o = vrow * (AV::STRIDE / 4);
+        asm volatile("" : "+s"(o));
+        static_for<4>([&](auto q4c) {
+            constexpr int q4 = decltype(q4c)::value;
+            const f4 sh = vec4[o + 8 * nb + 2 * q4 + half];
+            static_for<2>([&](auto qc) {
+                constexpr int q = 2 * decltype(qc)::value;
+                constexpr int g2 = q4 / 2, u = 4 * (q4 % 2) + q;
+                const fl2 h = {silu(c[4 * q4 + q] + sh[q]), silu(c[4 * q4 + q + 1] + sh[q + 1])};
+                const bf2 h0 = __builtin_convertvector(h, bf2);
+                const fl2 r1 = h - widen(h0);                    // exact
+                const bf2 h1 = __builtin_convertvector(r1, bf2);
+                const fl2 r2 = r1 - widen(h1);                   // exact, at most 8 bits
+                const bf2 h2 = __builtin_convertvector(r2, bf2);
+                p[g2][0][u] = h0[0]; p[g2][0][u + 1] = h0[1];
+                p[g2][1][u] = h1[0]; p[g2][1][u + 1] = h1[1];
+                p[g2][2][u] = h2[0]; p[g2][2][u + 1] = h2[1];
+            });
+        });
+        // pinned here, so the work overlaps the MFMAs it is placed between
+        // instead of being sunk past the next barrier
+        asm volatile("" : "+v"(p[0][0]), "+v"(p[0][1]), "+v"(p[0][2]),
+                          "+v"(p[1][0]), "+v"(p[1][1]), "+v"(p[1][2]));
+    };
+    // acc += w x over one k-step from the parts: six bf16 products
+    auto mac6 = [&](const bf8* fr, const bf8 (&x)[3], f16v& acc0, f16v& acc1) {
+        const bf8 w0 = fr[0], w1 = fr[64], w2 = fr[128];
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, x[0], acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, x[1], acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, x[0], acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, x[2], acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w2, x[0], acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, x[1], acc1, 0, 0, 0);
+    };
+    // the same for two output blocks, their MFMAs interleaved
+    auto mac6x2 = [&](const bf8* fa, const bf8* fb, const bf8 (&x)[3], f16v& A, f16v& B) {
+        const bf8 a0 = fa[0], a1 = fa[64], a2 = fa[128];
+        const bf8 b0 = fb[0], b1 = fb[64], b2 = fb[128];
+        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, x[0], A, 0, 0, 0);
+        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, x[0], B, 0, 0, 0);
+        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, x[1], A, 0, 0, 0);
+        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, x[1], B, 0, 0, 0);
+        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, x[0], A, 0, 0, 0);
+        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, x[0], B, 0, 0, 0);
+        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, x[2], A, 0, 0, 0);
+        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, x[2], B, 0, 0, 0);
+        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, x[0], A, 0, 0, 0);
+        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b2, x[0], B, 0, 0, 0);
+        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, x[1], A, 0, 0, 0);
+        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, x[1], B, 0, 0, 0);
+    };
+    struct Tile {
+        int64_t row, px;
+        bool active, pxok;
+        const float* x;
+        int n;
+    };
+    auto locate = [&](int64_t tg) -> Tile {
+        Tile T;
+        const int64_t tile = tg * 4 + wave;
+        T.active = tile < ntiles;
+        const int64_t tt = T.active ? tile : ntiles - 1;     // idle waves redo the last tile
+        T.row = tt / tiles_per_row;
+        const int pt = (int)(tt % tiles_per_row);
+        const int g = (int)(T.row / src.group), bb = (int)(T.row % src.group);
+        const int64_t sl = src.slot ? __builtin_amdgcn_readfirstlane(src.slot[g]) : g;
+        T.x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
+        T.n = __builtin_amdgcn_readfirstlane(src.n[g]);
+        T.px = (int64_t)pt * 32 + (lane & 31);
+        T.pxok = T.px < P;
+        return T;
+    };
+    const int nbranch = a.shift_c ? 2 : 1;
+
+    Tile cur = locate(blockIdx.x);
+    dma(0, 0);
+    dma_shift(cur.n, 0);
+    for (int i = tid; i < AV::W; i += 256) {
+        reinterpret_cast<float*>(vec4)[AV::B2 * AV::STRIDE + i] = a.b2[i];
+        reinterpret_cast<float*>(vec4)[AV::B3 * AV::STRIDE + i] = a.b3[i];
+    }
+    land();
+    float xin[L::KS1];
+#pragma unroll
+    for (int s = 0; s < L::KS1; ++s) xin[s] = cur.pxok ? cur.x[(2 * s + half) * P + cur.px] : 0.f;
+
+    for (int64_t tg = blockIdx.x; tg < ngroups; tg += gridDim.x) {
+        const bool last_group = tg + gridDim.x >= ngroups;
+        Tile nxt = locate(last_group ? tg : tg + gridDim.x);
+        float xnx[L::KS1];
+#pragma unroll
+        for (int s = 0; s < L::KS1; ++s) xnx[s] = nxt.pxok ? nxt.x[(2 * s + half) * P + nxt.px] : 0.f;
+
+        float eu[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int br = 0; br < nbranch; ++br) {
+            f16v acc[NB];
+
+            // ---- layer 1 (slab 0, buffer 0): K = C on fp32 MFMA
+            dma(1, 1);
+            static_for<NB>([&](auto nbc) {
+                constexpr int nb = decltype(nbc)::value;
+                acc[nb] = f16v{};
+                const float* f1 = reinterpret_cast<const float*>(lds_0) + (nb * 64 + lane) * L::KS1;
+                static_for<L::KS1>([&](auto sc) {
+                    constexpr int s = decltype(sc)::value;
+                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(f1[s], xin[s], acc[nb], 0, 0, 0);
+                });
+            });
+
+            // ---- layers 2 and 3: one slab per input block
+            static_for<2>([&](auto lc) {
+                constexpr int layer = decltype(lc)::value;
+                const int vin = layer == 0 ? wave : AV::B2;
+                bf8 X[2][3];
+                act_split(acc[0], vin, 0, X);
+                constexpr int NBP = (NB + 1) / 2;               // output-block pairs
+                f16v nacc[NB];
+                static_for<NB>([&](auto nbc) { nacc[decltype(nbc)::value] = f16v{}; });
+                static_for<NB>([&](auto bc) {
+                    constexpr int b = decltype(bc)::value;
+                    constexpr int slab = 1 + layer * NB + b;
+                    constexpr int buf = slab & 1;
+                    land();                                      // slab b has landed
+                    dma(slab + 1, buf ^ 1);                      // the next one, or layer 4
+                    bf8 Y[2][3];
+                    static_for<2>([&](auto g2c) {
+                        constexpr int g2 = decltype(g2c)::value;
+                        static_for<NBP>([&](auto pc) {
+                            constexpr int nb = 2 * decltype(pc)::value;
+                            const bf8* fr = ldsb(buf) + ((g2 * NB + nb) * 3) * 64 + lane;
+                            if constexpr (nb + 1 < NB)
+                                mac6x2(fr, fr + 3 * 64, X[g2], nacc[nb], nacc[nb + 1]);
+                            else
+                                mac6(fr, X[g2], nacc[nb], nacc[nb]);
+                            if constexpr (b + 1 < NB && g2 == 0 && nb + 2 >= NB)
+                                act_split(acc[b + 1], vin, b + 1, Y);
+                        });
+                    });
+                    if constexpr (b + 1 < NB) {
+                        static_for<2>([&](auto g2c) {
+                            constexpr int g2 = decltype(g2c)::value;
+                            X[g2][0] = Y[g2][0];
+                            X[g2][1] = Y[g2][1];
+                            X[g2][2] = Y[g2][2];
+                        });
+                    }
+                });
+                static_for<NB>([&](auto nbc) { acc[decltype(nbc)::value] = nacc[decltype(nbc)::value]; });
+            });
+
+            // ---- layer 4 (slab 2NB+1, buffer 1): C outputs
+            {
+                constexpr int slab = 1 + 2 * NB;
+                constexpr int buf = slab & 1;
+                land();
+                const bool more = br + 1 < nbranch || !last_group;
+                if (more) {                                      // next pass's layer 1
+                    dma(0, 0);
+                    if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
+                    else dma_shift(nxt.n, 0);
+                }
+                bf8 X[2][3];
+                act_split(acc[0], AV::B3, 0, X);
+                f16v o4[4] = {f16v{}, f16v{}, f16v{}, f16v{}};
+                static_for<NB>([&](auto bc) {
+                    constexpr int b = decltype(bc)::value;
+                    bf8 Y[2][3];
+                    static_for<2>([&](auto g2c) {
+                        constexpr int g2 = decltype(g2c)::value;
+                        mac6(ldsb(buf) + ((b * 2 + g2) * 3) * 64 + lane, X[g2], o4[2 * g2], o4[2 * g2 + 1]);
+                    });
+                    if constexpr (b + 1 < NB) {
+                        act_split(acc[b + 1], AV::B3, b + 1, Y);
+                        static_for<2>([&](auto g2c) {
+                            constexpr int g2 = decltype(g2c)::value;
+                            X[g2][0] = Y[g2][0];
+                            X[g2][1] = Y[g2][1];
+                            X[g2][2] = Y[g2][2];
+                        });
+                    }
+                });
+                const f16v o = (o4[0] + o4[1]) + (o4[2] + o4[3]);
+                float* out = eps + cur.row * (int64_t)C * P;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int c = 4 * half + r;
+                    if (c < C) {
+                        const float v = o[r] + a.b4[c];
+                        if (br == 0) {
+                            eu[r] = v;
+                            if (nbranch == 1 && cur.active && cur.pxok) out[c * P + cur.px] = v;
+                        } else if (cur.active && cur.pxok) {
+                            out[c * P + cur.px] = eu[r] + a.guidance * (v - eu[r]);
+                        }
+                    }
+                }
+                land();                                          // slab 0 is in buffer 0 again
+            }
+        }
+        cur = nxt;
+#pragma unroll
+        for (int s = 0; s < L::KS1; ++s) xin[s] = xnx[s];
     }
 }
 
@@ -594,6 +634,60 @@ void pack_bf16_t(const float* W1, const float* W2, const float* W3, const float*
                         (l % 32 < C) ? to_bf16(W4[(l % 32) * W + fin(b, g2, l, u)]) : (uint16_t)0;
 }
 
+float from_bf16(uint16_t h) {
+    const uint32_t u = (uint32_t)h << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    return f;
+}
+
+// w = p[0] + p[1] + p[2] exactly (for finite w away from the overflow edge):
+// each part is the nearest bf16 to what the previous parts leave, and the
+// differences are exact in fp32
+void split_bf16(float w, uint16_t (&p)[3]) {
+    p[0] = to_bf16(w);
+    const float r1 = w - from_bf16(p[0]);
+    p[1] = to_bf16(r1);
+    const float r2 = r1 - from_bf16(p[1]);
+    p[2] = to_bf16(r2);
+}
+
+template <int NB, int C>
+void pack_x6_t(const float* W1, const float* W2, const float* W3, const float* W4,
+               std::vector<uint8_t>& out) {
+    using L = ConvLayoutX6<NB, C>;
+    constexpr int W = 32 * NB;
+    out.assign((size_t)L::TOTAL * 16, 0);
+    float* f = reinterpret_cast<float*>(out.data());            // layer 1: fp32 fragments
+    for (int nb = 0; nb < NB; ++nb)
+        for (int l = 0; l < 64; ++l)
+            for (int s = 0; s < L::KS1; ++s)
+                f[L::off(0) * 4 + (nb * 64 + l) * L::KS1 + s] = W1[(32 * nb + l % 32) * C + 2 * s + l / 32];
+    uint16_t* h = reinterpret_cast<uint16_t*>(out.data());
+    auto put = [&](int unit, int u, float w) {                  // part k -> k fragments on
+        uint16_t p[3];
+        split_bf16(w, p);
+        for (int k = 0; k < 3; ++k) h[((size_t)unit + (size_t)k * 64) * 8 + u] = p[k];
+    };
+    auto fin = [](int b, int g2, int l, int u) { return 32 * b + 16 * g2 + 8 * (u / 4) + 4 * (l / 32) + u % 4; };
+    for (int layer = 0; layer < 2; ++layer) {
+        const float* Wm = layer == 0 ? W2 : W3;
+        for (int b = 0; b < NB; ++b)
+            for (int g2 = 0; g2 < 2; ++g2)
+                for (int nb = 0; nb < NB; ++nb)
+                    for (int l = 0; l < 64; ++l)
+                        for (int u = 0; u < 8; ++u)
+                            put(L::off(1 + layer * NB + b) + ((g2 * NB + nb) * 3) * 64 + l, u,
+                                Wm[(32 * nb + l % 32) * W + fin(b, g2, l, u)]);
+    }
+    for (int b = 0; b < NB; ++b)
+        for (int g2 = 0; g2 < 2; ++g2)
+            for (int l = 0; l < 64; ++l)
+                for (int u = 0; u < 8; ++u)
+                    put(L::off(1 + 2 * NB) + ((b * 2 + g2) * 3) * 64 + l, u,
+                        (l % 32 < C) ? W4[(l % 32) * W + fin(b, g2, l, u)] : 0.f);
+}
+
 int device_cus();
 
 template <int NB, int C>
@@ -620,47 +714,15 @@ int device_cus() {
 }
 
 template <int NB, int C>
-void launch_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
+void launch_x6_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
     const int tiles_per_row = (int)((a.P + 31) / 32);
     const int64_t ntiles = (int64_t)src.max_groups * src.group * tiles_per_row;
     if (ntiles == 0) return;
     int64_t blocks = (ntiles + 3) / 4;                       // persistent: one block per CU
     if (blocks > device_cus()) blocks = device_cus();
-    hipLaunchKernelGGL((k_conv_f32<NB, C>), dim3((unsigned)blocks), dim3(256), 0, s, a, src, eps,
+    hipLaunchKernelGGL((k_conv_f32x6<NB, C>), dim3((unsigned)blocks), dim3(256), 0, s, a, src, eps,
                        tiles_per_row);
     PD_HIP(hipGetLastError());
-}
-
-template <int NB, int C>
-void pack_t(const float* W1, const float* W2, const float* W3, const float* W4,
-            std::vector<uint8_t>& out) {
-    using L = ConvLayout<NB, C>;
-    constexpr int W = 32 * NB;
-    out.assign((size_t)L::TOTAL * sizeof(float), 0);
-    float* f = reinterpret_cast<float*>(out.data());
-    for (int nb = 0; nb < NB; ++nb)
-        for (int l = 0; l < 64; ++l)
-            for (int s = 0; s < L::KS1; ++s)
-                f[L::off(0) + (nb * 64 + l) * L::KS1 + s] = W1[(32 * nb + l % 32) * C + 2 * s + l / 32];
-    for (int layer = 0; layer < 2; ++layer) {
-        const float* Wm = layer == 0 ? W2 : W3;
-        for (int b = 0; b < NB; ++b) {
-            float* sl = f + L::off(1 + layer * NB + b);
-            for (int g4 = 0; g4 < 4; ++g4)
-                for (int nb = 0; nb < NB; ++nb)
-                    for (int l = 0; l < 64; ++l)
-                        for (int q = 0; q < 4; ++q)
-                            sl[((g4 * NB + nb) * 64 + l) * 4 + q] =
-                                Wm[(32 * nb + l % 32) * W + 32 * b + 8 * g4 + 4 * (l / 32) + q];
-        }
-    }
-    float* sl = f + L::off(1 + 2 * NB);
-    for (int b = 0; b < NB; ++b)
-        for (int g4 = 0; g4 < 4; ++g4)
-            for (int l = 0; l < 64; ++l)
-                for (int q = 0; q < 4; ++q)
-                    sl[((b * 4 + g4) * 64 + l) * 4 + q] =
-                        (l % 32 < C) ? W4[(l % 32) * W + 32 * b + 8 * g4 + 4 * (l / 32) + q] : 0.f;
 }
 
 #define PD_CONV_SHAPES(X) X(1, 4) X(2, 4) X(4, 4) X(10, 4)
@@ -678,7 +740,7 @@ bool conv_supported(int C, int width, bool bf16) {
 size_t conv_frag_bytes(int C, int width, bool bf16) {
 #define X(nb, c)                                                                      \
     if (C == c && width == 32 * nb)                                                   \
-        return bf16 ? (size_t)ConvLayoutBf16<nb, c>::TOTAL * 16 : (size_t)ConvLayout<nb, c>::TOTAL * 4;
+        return bf16 ? (size_t)ConvLayoutBf16<nb, c>::TOTAL * 16 : (size_t)ConvLayoutX6<nb, c>::TOTAL * 16;
     PD_CONV_SHAPES(X)
 #undef X
     return 0;
@@ -691,7 +753,7 @@ void conv_pack_weights(int C, int width, bool bf16, const float* W1, const float
         if (bf16)                                                 \
             pack_bf16_t<nb, c>(W1, W2, W3, W4, out);              \
         else                                                      \
-            pack_t<nb, c>(W1, W2, W3, W4, out);                   \
+            pack_x6_t<nb, c>(W1, W2, W3, W4, out);                \
         return;                                                   \
     }
     PD_CONV_SHAPES(X)
@@ -705,7 +767,7 @@ void launch_conv1x1(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_
         if (a.bf16)                                                \
             launch_bf16_t<nb, c>(a, src, eps, s);                  \
         else                                                       \
-            launch_t<nb, c>(a, src, eps, s);                       \
+            launch_x6_t<nb, c>(a, src, eps, s);                    \
         return;                                                    \
     }
     PD_CONV_SHAPES(X)

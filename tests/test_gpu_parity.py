@@ -122,6 +122,25 @@ def test_conv1x1_forward(shape, width, M, cond):
     assert _rel(got, ref) <= REL_F32
 
 
+@pytest.mark.parametrize("scale", [1.0, 1e3, 1e-3])
+def test_conv1x1_forward_is_fp32_accurate(scale):
+    """The fp32 network runs on bf16 matrix cores with each operand split into
+    three bf16 parts: against a float64 evaluation it must be at least as
+    accurate as a plain float32 one, at any input scale."""
+    wl = _wl("conv1x1", (4, 16, 16), 320, T=1000)
+    w = W.make_weights(wl.model)
+    rng = np.random.default_rng(7)
+    x = (rng.standard_normal((3, 4, 16, 16)) * scale).astype(np.float32)
+    n = rng.integers(0, 1000, 3).astype(np.int32)
+    got = _forward(wl, w, x, n)
+    tb = schedule.from_spec(wl.schedule)
+    ref64 = denoisers.Denoiser(wl.model, w, tb.alphabar, np.float64, False)(x.astype(np.float64), n)
+    ref64 = ref64.reshape(3, -1)
+    ref32 = _oracle_eps(wl, w, x, n)
+    e_dev, e_32 = _rel(got, ref64), _rel(ref32, ref64)
+    assert e_dev <= max(2 * e_32, 1e-7), (e_dev, e_32)
+
+
 @pytest.mark.parametrize("shape,width,M,cond", [
     ((4, 8, 8), 32, 3, 0),
     ((4, 6, 7), 64, 5, 0),        # ragged last tile
