@@ -156,6 +156,12 @@ pd_status pd_schedule_multistep_tables(const pd_schedule* s, float* R, float* S)
  *  MLP / CONV1X1: W1 [W][Din], b1 [W], W2 [W][W], b2, W3 [W][W], b3,
  *                 W4 [Dout][W], b4 [Dout]  (+ Wc [W][cond_dim], c [cond_dim])
  *  with Din = Dout = D (MLP) or C (CONV1X1).
+ * dtype PD_F32 computes the network to float32 accuracy: for conv1x1 the
+ * matmuls of layers 2-4 run on the bf16 matrix cores with each operand split
+ * exactly into three bfloat16 parts and six part products per multiply-add,
+ * whose error is about one float32 rounding (a value within about 2^-8 of
+ * the float32 overflow threshold splits into a non-finite part, and the
+ * result is NaN where float32 arithmetic would give an infinity).
  * dtype PD_BF16 (conv1x1 only) rounds every matmul operand to bfloat16
  * (round to nearest even) and accumulates in float32.
  * The training schedule `train` supplies abar (GMM) and T_train (the range
