@@ -306,16 +306,25 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 // times the multiply-adds of an fp32 one in the same time, so the six take
 // 6/16 of the fp32 matrix-core time.
 //
-// Persistent blocks of 4 waves, one per SIMD: a tile's activations and the
-// accumulators of a whole layer fill the register file.  Layer 1 (K = C) runs
-// on fp32 MFMA (v_mfma_f32_32x32x2f32: A[i][k] in lane i + 32 k, B[k][j] in
-// lane j + 32 k, the same accumulator layout); its slab holds, for output
-// block nb and lane l, the C/2 values W1[32 nb + l%32][2 s + l/32].  Layers
-// 2-4 run on the split products: the weights are split on the host, the
-// activations of input block b + 1 are computed and split during the MFMAs of
-// block b.  Mid-layer slab b holds input block b for every output block nb,
-// fragment ((g2 NB + nb) 3 + part), one 16-B unit per lane; layer 4's slab
-// holds fragment ((b 2 + g2) 3 + part) with the C output rows padded to 32.
+// Persistent blocks of 8 waves on 4 tiles: the two waves of a tile share a
+// SIMD and split the output blocks of every layer between them (half 0 the
+// first ceil(NB/2), half 1 the rest), so that one wave's SiLU and splitting
+// run beside the other's MFMAs.  A tile's activations and a layer's
+// accumulators would not fit one wave's 256 registers at two waves per SIMD;
+// halved they do.  The owner of an input block activates it (fp32 SiLU) into
+// an LDS exchange buffer one slab ahead, and both waves split it from there;
+// at layer 4 each wave sums over its own input blocks and half 1 passes its
+// partial sums to half 0 through the same buffer.
+//
+// Layer 1 (K = C) runs on fp32 MFMA (v_mfma_f32_32x32x2f32: A[i][k] in lane
+// i + 32 k, B[k][j] in lane j + 32 k, the same accumulator layout); its slab
+// holds, for output block nb and lane l, the C/2 values
+// W1[32 nb + l%32][2 s + l/32].  Layers 2-4 run on the split products, with
+// the weights split on the host.  Mid-layer slab b holds input block b for
+// every output block nb, fragment ((g2 NB + nb) 3 + part), one 16-B unit per
+// lane; layer 4's slab holds fragment ((b 2 + g2) 3 + part) with the C output
+// rows padded to 32.  LDS: two 60 KB slabs, two 16 KB exchange buffers and
+// the activation vectors, 163,328 bytes at width 320.
 typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
 typedef float fl2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ fl2 widen(bf2 v) {              // bf16 pair -> fp32 pair, exact
@@ -337,32 +346,42 @@ struct ConvLayoutX6 {                            // units of 16 B
 };
 
 template <int NB, int C>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
     using L = ConvLayoutX6<NB, C>;
-    using AV = ActVecs<NB, 4>;
+    constexpr int NT = 4;                            // tiles per block, two waves each
+    constexpr int NBH = (NB + 1) / 2;                // output blocks of half 0 (half 1: NB - NBH)
+    constexpr int NPR = (NBH + 1) / 2;               // pairs of them
+    constexpr int W = 32 * NB;
     static_assert(C % 2 == 0 && C <= 8, "layer 1 pairs channels; layer 4 fills one lane half");
     __shared__ bf8 lds_0[L::BUF];
     __shared__ bf8 lds_1[L::BUF];
-    auto ldsb = [&](int buf) -> bf8* { return buf ? lds_1 : lds_0; };
-    __shared__ f4 vec4[AV::F4];
+    __shared__ f4 xch_0[NT * 4 * 64];                // one input block's activations per tile
+    __shared__ f4 xch_1[NT * 4 * 64];
+    __shared__ __attribute__((aligned(16))) float vec[(NT + 2) * W];   // shifts of the tiles, b2, b3
 
     const int groups = src.active ? *src.active : src.max_groups;
     const int64_t ntiles = (int64_t)groups * src.group * tiles_per_row;
-    const int64_t ngroups = (ntiles + 3) / 4;
+    const int64_t ngroups = (ntiles + NT - 1) / NT;
     if ((int64_t)blockIdx.x >= ngroups) return;              // uniform over the block
 
     const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int tile = wave & (NT - 1);                // waves tile and tile + NT share a SIMD
+    const int oh = wave >> 2;                        // output half
     const int64_t P = a.P;
+    // does this wave own its j-th output block (half 1 has one fewer when NB is odd)
+    auto own = [&](int j) { return NB % 2 == 0 || oh == 0 || j < NB - NBH; };
 
+    auto ldsb = [&](int buf) -> bf8* { return buf ? lds_1 : lds_0; };
+    auto xchb = [&](int buf) -> f4* { return (buf ? xch_1 : xch_0) + tile * 4 * 64; };
     auto dma = [&](int i, int buf) {                         // slab i -> buffer, 1 KB per wave op
         const int nch = L::size(i) / 64;
         const char* gb = reinterpret_cast<const char*>(a.frags);
         uint32_t lo = (uint32_t)lane * 16u;
         asm volatile("" : "+s"(gb), "+v"(lo));
         bf8* ls = ldsb(buf);
-        for (int c = wave; c < nch; c += 4) {
+        for (int c = wave; c < nch; c += 2 * NT) {
             const uint32_t ob = (uint32_t)(L::off(i) + c * 64) * 16u + lo;
             __builtin_amdgcn_global_load_lds(
                 (const __attribute__((address_space(1))) void*)(gb + (size_t)ob),
@@ -373,31 +392,41 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     };
+    // first-layer shift of this tile for the next pass (row n, branch br), by the tile's half-0 wave
     auto dma_shift = [&](int n, int br) {
-        const float* row = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * AV::W;
-        float* dst = reinterpret_cast<float*>(vec4) + wave * AV::STRIDE;
-        for (int c = 0; c < AV::STRIDE / 256; ++c) {
-            int off = c * 256 + lane * 4;
-            off = off <= AV::W - 4 ? off : AV::W - 4;
-            __builtin_amdgcn_global_load_lds(
-                (const __attribute__((address_space(1))) void*)(row + off),
-                (__attribute__((address_space(3))) void*)(dst + c * 256), 16, 0, 0);
+        if (oh != 0) return;
+        const float* row = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * W;
+        float* dst = vec + tile * W;
+        for (int c = 0; c * 256 < W; ++c) {
+            const int off = c * 256 + lane * 4;
+            if (off < W)                                     // W is a multiple of 32
+                __builtin_amdgcn_global_load_lds(
+                    (const __attribute__((address_space(1))) void*)(row + off),
+                    (__attribute__((address_space(3))) void*)(dst + c * 256), 16, 0, 0);
         }
     };
-    // SiLU(acc + v) of block nb (v = LDS vector row vrow) in fp32, split into
-    // the three bf16 parts of the block's two B operands: p[g2][part]
-    auto act_split = [&](const f16v& c, int vrow, int nb, bf8 (&p)[2][3]) {
-        int o = vrow * (AV::STRIDE / 4);
-        asm volatile("" : "+s"(o));
+    // SiLU(acc + v) of output block nb, v = LDS vector row vrow, in fp32
+    auto act = [&](const f16v& c, int vrow, int nb, f4 (&h)[4]) {
+        const float* v = vec + vrow * W + 32 * nb + 4 * half;
         static_for<4>([&](auto q4c) {
             constexpr int q4 = decltype(q4c)::value;
-            const f4 sh = vec4[o + 8 * nb + 2 * q4 + half];
+            const f4 sh = *reinterpret_cast<const f4*>(v + 8 * q4);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) h[q4][q] = silu(c[4 * q4 + q] + sh[q]);
+        });
+    };
+    // the three bf16 parts of half g2 of a block's activations: the B operands of
+    // its k-step g2
+    auto split_g2 = [&](auto g2c, const f4 (&h)[4], bf8 (&p)[2][3]) {
+        constexpr int g2 = decltype(g2c)::value;
+        static_for<2>([&](auto q4h) {
+            constexpr int q4 = 2 * g2 + decltype(q4h)::value;
             static_for<2>([&](auto qc) {
                 constexpr int q = 2 * decltype(qc)::value;
-                constexpr int g2 = q4 / 2, u = 4 * (q4 % 2) + q;
-                const fl2 h = {silu(c[4 * q4 + q] + sh[q]), silu(c[4 * q4 + q + 1] + sh[q + 1])};
-                const bf2 h0 = __builtin_convertvector(h, bf2);
-                const fl2 r1 = h - widen(h0);                    // exact
+                constexpr int u = 4 * (q4 % 2) + q;
+                const fl2 hv = {h[q4][q], h[q4][q + 1]};
+                const bf2 h0 = __builtin_convertvector(hv, bf2);
+                const fl2 r1 = hv - widen(h0);                   // exact
                 const bf2 h1 = __builtin_convertvector(r1, bf2);
                 const fl2 r2 = r1 - widen(h1);                   // exact, at most 8 bits
                 const bf2 h2 = __builtin_convertvector(r2, bf2);
@@ -406,12 +435,7 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                 p[g2][2][u] = h2[0]; p[g2][2][u + 1] = h2[1];
             });
         });
-        // pinned here, so the work overlaps the MFMAs it is placed between
-        // instead of being sunk past the next barrier
-        asm volatile("" : "+v"(p[0][0]), "+v"(p[0][1]), "+v"(p[0][2]),
-                          "+v"(p[1][0]), "+v"(p[1][1]), "+v"(p[1][2]));
     };
-    // acc += w x over one k-step from the parts: six bf16 products
     auto mac6 = [&](const bf8* fr, const bf8 (&x)[3], f16v& acc0, f16v& acc1) {
         const bf8 w0 = fr[0], w1 = fr[64], w2 = fr[128];
         acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, x[0], acc0, 0, 0, 0);
@@ -421,7 +445,6 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
         acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w2, x[0], acc0, 0, 0, 0);
         acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, x[1], acc1, 0, 0, 0);
     };
-    // the same for two output blocks, their MFMAs interleaved
     auto mac6x2 = [&](const bf8* fa, const bf8* fb, const bf8 (&x)[3], f16v& A, f16v& B) {
         const bf8 a0 = fa[0], a1 = fa[64], a2 = fa[128];
         const bf8 b0 = fb[0], b1 = fb[64], b2 = fb[128];
@@ -446,9 +469,9 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
     };
     auto locate = [&](int64_t tg) -> Tile {
         Tile T;
-        const int64_t tile = tg * 4 + wave;
-        T.active = tile < ntiles;
-        const int64_t tt = T.active ? tile : ntiles - 1;     // idle waves redo the last tile
+        const int64_t t = tg * NT + tile;
+        T.active = t < ntiles;
+        const int64_t tt = T.active ? t : ntiles - 1;       // idle waves redo the last tile
         T.row = tt / tiles_per_row;
         const int pt = (int)(tt % tiles_per_row);
         const int g = (int)(T.row / src.group), bb = (int)(T.row % src.group);
@@ -464,9 +487,9 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
     Tile cur = locate(blockIdx.x);
     dma(0, 0);
     dma_shift(cur.n, 0);
-    for (int i = tid; i < AV::W; i += 256) {
-        reinterpret_cast<float*>(vec4)[AV::B2 * AV::STRIDE + i] = a.b2[i];
-        reinterpret_cast<float*>(vec4)[AV::B3 * AV::STRIDE + i] = a.b3[i];
+    for (int i = tid; i < W; i += 2 * NT * 64) {
+        vec[NT * W + i] = a.b2[i];
+        vec[(NT + 1) * W + i] = a.b3[i];
     }
     land();
     float xin[L::KS1];
@@ -482,62 +505,77 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
 
         float eu[4] = {0.f, 0.f, 0.f, 0.f};
         for (int br = 0; br < nbranch; ++br) {
-            f16v acc[NB];
+            f16v acc[NBH];
 
-            // ---- layer 1 (slab 0, buffer 0): K = C on fp32 MFMA
+            // ---- layer 1 (slab 0, buffer 0): this wave's output blocks on fp32 MFMA
             dma(1, 1);
-            static_for<NB>([&](auto nbc) {
-                constexpr int nb = decltype(nbc)::value;
-                acc[nb] = f16v{};
-                const float* f1 = reinterpret_cast<const float*>(lds_0) + (nb * 64 + lane) * L::KS1;
-                static_for<L::KS1>([&](auto sc) {
-                    constexpr int s = decltype(sc)::value;
-                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(f1[s], xin[s], acc[nb], 0, 0, 0);
-                });
+            static_for<NBH>([&](auto jc) {
+                constexpr int j = decltype(jc)::value;
+                acc[j] = f16v{};
+                if (own(j)) {
+                    const float* f1 = reinterpret_cast<const float*>(lds_0) + ((oh * NBH + j) * 64 + lane) * L::KS1;
+                    static_for<L::KS1>([&](auto sc) {
+                        constexpr int s = decltype(sc)::value;
+                        acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(f1[s], xin[s], acc[j], 0, 0, 0);
+                    });
+                }
             });
 
-            // ---- layers 2 and 3: one slab per input block
+            // ---- layers 2 and 3: one slab per input block; the block's owner
+            // activates it into an exchange buffer one slab ahead
             static_for<2>([&](auto lc) {
                 constexpr int layer = decltype(lc)::value;
-                const int vin = layer == 0 ? wave : AV::B2;
-                bf8 X[2][3];
-                act_split(acc[0], vin, 0, X);
-                constexpr int NBP = (NB + 1) / 2;               // output-block pairs
-                f16v nacc[NB];
-                static_for<NB>([&](auto nbc) { nacc[decltype(nbc)::value] = f16v{}; });
+                const int vin = layer == 0 ? tile : NT;
+                if (oh == 0) {
+                    f4 h[4];
+                    act(acc[0], vin, 0, h);
+                    f4* xd = xchb(0);
+                    static_for<4>([&](auto q4c) { xd[decltype(q4c)::value * 64 + lane] = h[decltype(q4c)::value]; });
+                }
+                f16v nacc[NBH];
+                static_for<NBH>([&](auto jc) { nacc[decltype(jc)::value] = f16v{}; });
                 static_for<NB>([&](auto bc) {
                     constexpr int b = decltype(bc)::value;
                     constexpr int slab = 1 + layer * NB + b;
                     constexpr int buf = slab & 1;
-                    land();                                      // slab b has landed
-                    dma(slab + 1, buf ^ 1);                      // the next one, or layer 4
-                    bf8 Y[2][3];
+                    land();                                      // slab b and block b's activations are in
+                    dma(slab + 1, buf ^ 1);
+                    if constexpr (b + 1 < NB) {
+                        constexpr int o = (b + 1) < NBH ? 0 : 1, jl = (b + 1) - o * NBH;
+                        if (oh == o) {
+                            f4 h[4];
+                            act(acc[jl], vin, b + 1, h);
+                            f4* xd = xchb((b + 1) & 1);
+                            static_for<4>([&](auto q4c) { xd[decltype(q4c)::value * 64 + lane] = h[decltype(q4c)::value]; });
+                        }
+                    }
+                    const f4* xs = xchb(b & 1);
                     static_for<2>([&](auto g2c) {
                         constexpr int g2 = decltype(g2c)::value;
-                        static_for<NBP>([&](auto pc) {
-                            constexpr int nb = 2 * decltype(pc)::value;
-                            const bf8* fr = ldsb(buf) + ((g2 * NB + nb) * 3) * 64 + lane;
-                            if constexpr (nb + 1 < NB)
-                                mac6x2(fr, fr + 3 * 64, X[g2], nacc[nb], nacc[nb + 1]);
-                            else
-                                mac6(fr, X[g2], nacc[nb], nacc[nb]);
-                            if constexpr (b + 1 < NB && g2 == 0 && nb + 2 >= NB)
-                                act_split(acc[b + 1], vin, b + 1, Y);
+                        bf8 X[2][3];
+                        {
+                            f4 h[4];
+                            h[2 * g2] = xs[(2 * g2) * 64 + lane];
+                            h[2 * g2 + 1] = xs[(2 * g2 + 1) * 64 + lane];
+                            split_g2(g2c, h, X);
+                        }
+                        static_for<NPR>([&](auto pc) {
+                            constexpr int j = 2 * decltype(pc)::value;
+                            const bf8* fr = ldsb(buf) + ((g2 * NB + oh * NBH + j) * 3) * 64 + lane;
+                            if constexpr (j + 1 < NBH) {
+                                if (own(j + 1)) mac6x2(fr, fr + 3 * 64, X[g2], nacc[j], nacc[j + 1]);
+                                else mac6(fr, X[g2], nacc[j], nacc[j]);
+                            } else {
+                                if (own(j)) mac6(fr, X[g2], nacc[j], nacc[j]);
+                            }
                         });
                     });
-                    if constexpr (b + 1 < NB) {
-                        static_for<2>([&](auto g2c) {
-                            constexpr int g2 = decltype(g2c)::value;
-                            X[g2][0] = Y[g2][0];
-                            X[g2][1] = Y[g2][1];
-                            X[g2][2] = Y[g2][2];
-                        });
-                    }
                 });
-                static_for<NB>([&](auto nbc) { acc[decltype(nbc)::value] = nacc[decltype(nbc)::value]; });
+                static_for<NBH>([&](auto jc) { acc[decltype(jc)::value] = nacc[decltype(jc)::value]; });
             });
 
-            // ---- layer 4 (slab 2NB+1, buffer 1): C outputs
+            // ---- layer 4 (slab 2NB+1, buffer 1): each half sums over its own input
+            // blocks; half 1 hands its partial sums to half 0
             {
                 constexpr int slab = 1 + 2 * NB;
                 constexpr int buf = slab & 1;
@@ -548,38 +586,40 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                     if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
                     else dma_shift(nxt.n, 0);
                 }
-                bf8 X[2][3];
-                act_split(acc[0], AV::B3, 0, X);
                 f16v o4[4] = {f16v{}, f16v{}, f16v{}, f16v{}};
-                static_for<NB>([&](auto bc) {
-                    constexpr int b = decltype(bc)::value;
-                    bf8 Y[2][3];
-                    static_for<2>([&](auto g2c) {
-                        constexpr int g2 = decltype(g2c)::value;
-                        mac6(ldsb(buf) + ((b * 2 + g2) * 3) * 64 + lane, X[g2], o4[2 * g2], o4[2 * g2 + 1]);
-                    });
-                    if constexpr (b + 1 < NB) {
-                        act_split(acc[b + 1], AV::B3, b + 1, Y);
+                static_for<NBH>([&](auto jc) {
+                    constexpr int j = decltype(jc)::value;
+                    if (own(j)) {
+                        f4 h[4];
+                        bf8 X[2][3];
+                        act(acc[j], NT + 1, oh * NBH + j, h);
+                        split_g2(std::integral_constant<int, 0>{}, h, X);
+                        split_g2(std::integral_constant<int, 1>{}, h, X);
                         static_for<2>([&](auto g2c) {
                             constexpr int g2 = decltype(g2c)::value;
-                            X[g2][0] = Y[g2][0];
-                            X[g2][1] = Y[g2][1];
-                            X[g2][2] = Y[g2][2];
+                            mac6(ldsb(buf) + (((oh * NBH + j) * 2 + g2) * 3) * 64 + lane, X[g2], o4[2 * g2],
+                                 o4[2 * g2 + 1]);
                         });
                     }
                 });
                 const f16v o = (o4[0] + o4[1]) + (o4[2] + o4[3]);
-                float* out = eps + cur.row * (int64_t)C * P;
+                f4* xp = xchb(0);
+                if (oh == 1) xp[lane] = f4{o[0], o[1], o[2], o[3]};
+                __syncthreads();
+                if (oh == 0) {
+                    const f4 o1 = xp[lane];
+                    float* out = eps + cur.row * (int64_t)C * P;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int c = 4 * half + r;
-                    if (c < C) {
-                        const float v = o[r] + a.b4[c];
-                        if (br == 0) {
-                            eu[r] = v;
-                            if (nbranch == 1 && cur.active && cur.pxok) out[c * P + cur.px] = v;
-                        } else if (cur.active && cur.pxok) {
-                            out[c * P + cur.px] = eu[r] + a.guidance * (v - eu[r]);
+                    for (int r = 0; r < 4; ++r) {
+                        const int c = 4 * half + r;
+                        if (c < C) {
+                            const float v = (o[r] + o1[r]) + a.b4[c];
+                            if (br == 0) {
+                                eu[r] = v;
+                                if (nbranch == 1 && cur.active && cur.pxok) out[c * P + cur.px] = v;
+                            } else if (cur.active && cur.pxok) {
+                                out[c * P + cur.px] = eu[r] + a.guidance * (v - eu[r]);
+                            }
                         }
                     }
                 }
@@ -720,7 +760,7 @@ void launch_x6_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s
     if (ntiles == 0) return;
     int64_t blocks = (ntiles + 3) / 4;                       // persistent: one block per CU
     if (blocks > device_cus()) blocks = device_cus();
-    hipLaunchKernelGGL((k_conv_f32x6<NB, C>), dim3((unsigned)blocks), dim3(256), 0, s, a, src, eps,
+    hipLaunchKernelGGL((k_conv_f32x6<NB, C>), dim3((unsigned)blocks), dim3(512), 0, s, a, src, eps,
                        tiles_per_row);
     PD_HIP(hipGetLastError());
 }
