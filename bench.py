@@ -105,8 +105,9 @@ def denoiser_roofline(wl, dtype: str, fl: float, seconds: float) -> dict:
     the peak of the instruction that runs them."""
     rate = fl / seconds if seconds > 0 else 0.0
     if wl.model.kind == "conv1x1" and dtype == "f32":
-        # layer 1 (K = C, 0.6% of the FLOPs at C = 4, width 320) runs on fp32
-        # MFMA; counting it as split products too keeps the figure simple
+        # layers 1 and 4 (K = C and C outputs, 1.2% of the FLOPs at C = 4,
+        # width 320) run on fp32 MFMA and the VALU; counting them as split
+        # products too keeps the figure simple
         ach = SPLIT_PRODUCTS * rate
         return {"bound": "mfma", "achieved": ach / 1e12, "peak": PEAK["bf16"] / 1e12,
                 "unit": "TFLOP/s", "frac": ach / PEAK["bf16"], "peak_dtype": "bf16",

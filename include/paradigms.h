@@ -157,9 +157,9 @@ pd_status pd_schedule_multistep_tables(const pd_schedule* s, float* R, float* S)
  *                 W4 [Dout][W], b4 [Dout]  (+ Wc [W][cond_dim], c [cond_dim])
  *  with Din = Dout = D (MLP) or C (CONV1X1).
  * dtype PD_F32 computes the network to float32 accuracy: for conv1x1 the
- * matmuls of layers 2-4 run on the bf16 matrix cores with each operand split
- * exactly into three bfloat16 parts and six part products per multiply-add,
- * whose error is about one float32 rounding (a value within about 2^-8 of
+ * matmuls of layers 2 and 3 run on the bf16 matrix cores with each operand
+ * split exactly into three bfloat16 parts and six part products per
+ * multiply-add, whose error is about one float32 rounding (a value within about 2^-8 of
  * the float32 overflow threshold splits into a non-finite part, and the
  * result is NaN where float32 arithmetic would give an infinity).
  * dtype PD_BF16 (conv1x1 only) rounds every matmul operand to bfloat16

@@ -296,9 +296,10 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 
 // ---------------------------------------------------------------- fp32
 // k_conv_f32x6: the fp32 network with fp32-accurate products on
-// v_mfma_f32_32x32x16_bf16.  Every fp32 operand is split exactly into three
-// bf16 parts, x = x0 + x1 + x2 (x0 the nearest bf16 to x, x1 the nearest to
-// x - x0, x2 = x - x0 - x1, which has at most 8 significant bits), so
+// v_mfma_f32_32x32x16_bf16 for its two W x W layers.  Every fp32 operand is
+// split exactly into three bf16 parts, x = x0 + x1 + x2 (x0 the nearest bf16
+// to x, x1 the nearest to x - x0, x2 = x - x0 - x1, which has at most 8
+// significant bits), so
 // |x1| <= 2^-8 |x| and |x2| <= 2^-16 |x|.  w x is formed from the six part
 // products down to 2^-16 |w x| (w0x0, w0x1, w1x0, w0x2, w2x0, w1x1); the three
 // left out add up to about 2^-23 |w| |x|, the size of one fp32 rounding.  Each
@@ -319,11 +320,12 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 // Layer 1 (K = C) runs on fp32 MFMA (v_mfma_f32_32x32x2f32: A[i][k] in lane
 // i + 32 k, B[k][j] in lane j + 32 k, the same accumulator layout); its slab
 // holds, for output block nb and lane l, the C/2 values
-// W1[32 nb + l%32][2 s + l/32].  Layers 2-4 run on the split products, with
-// the weights split on the host.  Mid-layer slab b holds input block b for
-// every output block nb, fragment ((g2 NB + nb) 3 + part), one 16-B unit per
-// lane; layer 4's slab holds fragment ((b 2 + g2) 3 + part) with the C output
-// rows padded to 32.  LDS: two 60 KB slabs, two 16 KB exchange buffers and
+// W1[32 nb + l%32][2 s + l/32].  Layers 2 and 3 run on the split products,
+// with the weights split on the host: slab b holds input block b for every
+// output block nb, fragment ((g2 NB + nb) 3 + part), one 16-B unit per lane.
+// Layer 4 (C outputs) runs as fp32 fused multiply-adds on the VALU from W4
+// in fp32 ([C][W], 5 KB at width 320): on the matrix core its C rows would be
+// padded to 32.  LDS: two 60 KB slabs, two 16 KB exchange buffers and
 // the activation vectors, 163,328 bytes at width 320.
 typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
 typedef float fl2 __attribute__((ext_vector_type(2)));
@@ -337,12 +339,15 @@ struct ConvLayoutX6 {                            // units of 16 B
     static constexpr int KS1 = C / 2;            // layer-1 fp32 k-steps
     static constexpr int SL1 = (NB * 64 * KS1 / 4 + 63) / 64 * 64;
     static constexpr int SLM = 2 * NB * 3 * 64;
+    static constexpr int SL4 = (C * 32 * NB / 4 + 63) / 64 * 64;   // layer 4: W4 in fp32, [C][W]
     static constexpr int BUF = SL1 > SLM ? SL1 : SLM;
-    static constexpr int TOTAL = SL1 + (2 * NB + 1) * SLM;
+    static constexpr int TOTAL = SL1 + 2 * NB * SLM + SL4;
     // slab 0: layer 1; 1 + layer * NB + b: input block b of layer 2 or 3;
     // 1 + 2 NB: layer 4
     static constexpr __host__ __device__ int off(int i) { return i == 0 ? 0 : SL1 + (i - 1) * SLM; }
-    static constexpr __host__ __device__ int size(int i) { return i == 0 ? SL1 : SLM; }
+    static constexpr __host__ __device__ int size(int i) {
+        return i == 0 ? SL1 : i == 1 + 2 * NB ? SL4 : SLM;
+    }
 };
 
 template <int NB, int C>
@@ -353,7 +358,7 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
     constexpr int NBH = (NB + 1) / 2;                // output blocks of half 0 (half 1: NB - NBH)
     constexpr int NPR = (NBH + 1) / 2;               // pairs of them
     constexpr int W = 32 * NB;
-    static_assert(C % 2 == 0 && C <= 8, "layer 1 pairs channels; layer 4 fills one lane half");
+    static_assert(C % 2 == 0 && C <= 8, "layer 1 pairs channels; at most 8 channels");
     __shared__ bf8 lds_0[L::BUF];
     __shared__ bf8 lds_1[L::BUF];
     __shared__ f4 xch_0[NT * 4 * 64];                // one input block's activations per tile
@@ -503,7 +508,9 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
 #pragma unroll
         for (int s = 0; s < L::KS1; ++s) xnx[s] = nxt.pxok ? nxt.x[(2 * s + half) * P + nxt.px] : 0.f;
 
-        float eu[4] = {0.f, 0.f, 0.f, 0.f};
+        float eu[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) eu[c] = 0.f;
         for (int br = 0; br < nbranch; ++br) {
             f16v acc[NBH];
 
@@ -574,11 +581,14 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                 static_for<NBH>([&](auto jc) { acc[decltype(jc)::value] = nacc[decltype(jc)::value]; });
             });
 
-            // ---- layer 4 (slab 2NB+1, buffer 1): each half sums over its own input
-            // blocks; half 1 hands its partial sums to half 0
+            // ---- layer 4 (slab 2NB+1, buffer 1: W4 in fp32): C outputs as fp32
+            // dot products on the VALU, each half over its own input blocks, the
+            // lane halves (the same pixel) added by a lane swap; half 1 hands its
+            // sums to half 0
             {
                 constexpr int slab = 1 + 2 * NB;
                 constexpr int buf = slab & 1;
+                constexpr int C4 = (C + 3) / 4;
                 land();
                 const bool more = br + 1 < nbranch || !last_group;
                 if (more) {                                      // next pass's layer 1
@@ -586,39 +596,52 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                     if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
                     else dma_shift(nxt.n, 0);
                 }
-                f16v o4[4] = {f16v{}, f16v{}, f16v{}, f16v{}};
+                const float* w4 = reinterpret_cast<const float*>(ldsb(buf));
+                float part[4 * C4];
+#pragma unroll
+                for (int c = 0; c < 4 * C4; ++c) part[c] = 0.f;
                 static_for<NBH>([&](auto jc) {
                     constexpr int j = decltype(jc)::value;
                     if (own(j)) {
                         f4 h[4];
-                        bf8 X[2][3];
                         act(acc[j], NT + 1, oh * NBH + j, h);
-                        split_g2(std::integral_constant<int, 0>{}, h, X);
-                        split_g2(std::integral_constant<int, 1>{}, h, X);
-                        static_for<2>([&](auto g2c) {
-                            constexpr int g2 = decltype(g2c)::value;
-                            mac6(ldsb(buf) + (((oh * NBH + j) * 2 + g2) * 3) * 64 + lane, X[g2], o4[2 * g2],
-                                 o4[2 * g2 + 1]);
+                        static_for<4>([&](auto q4c) {
+                            constexpr int q4 = decltype(q4c)::value;
+                            const int f = 32 * (oh * NBH + j) + 8 * q4 + 4 * half;   // features f..f+3
+                            static_for<C>([&](auto cc) {
+                                constexpr int c = decltype(cc)::value;
+                                const f4 w = *reinterpret_cast<const f4*>(w4 + c * W + f);
+#pragma unroll
+                                for (int q = 0; q < 4; ++q) part[c] = __builtin_fmaf(w[q], h[q4][q], part[c]);
+                            });
                         });
                     }
                 });
-                const f16v o = (o4[0] + o4[1]) + (o4[2] + o4[3]);
+#pragma unroll
+                for (int c = 0; c < C; ++c) part[c] += __shfl_xor(part[c], 32);
                 f4* xp = xchb(0);
-                if (oh == 1) xp[lane] = f4{o[0], o[1], o[2], o[3]};
+                if (oh == 1) {
+#pragma unroll
+                    for (int k = 0; k < C4; ++k)
+                        xp[k * 64 + lane] = f4{part[4 * k], part[4 * k + 1], part[4 * k + 2], part[4 * k + 3]};
+                }
                 __syncthreads();
-                if (oh == 0) {
-                    const f4 o1 = xp[lane];
+                if (oh == 0 && half == 0) {
                     float* out = eps + cur.row * (int64_t)C * P;
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int c = 4 * half + r;
-                        if (c < C) {
-                            const float v = (o[r] + o1[r]) + a.b4[c];
-                            if (br == 0) {
-                                eu[r] = v;
-                                if (nbranch == 1 && cur.active && cur.pxok) out[c * P + cur.px] = v;
-                            } else if (cur.active && cur.pxok) {
-                                out[c * P + cur.px] = eu[r] + a.guidance * (v - eu[r]);
+                    for (int k = 0; k < C4; ++k) {
+                        const f4 o1 = xp[k * 64 + lane];
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int c = 4 * k + r;
+                            if (c < C) {
+                                const float v = (part[c] + o1[r]) + a.b4[c];
+                                if (br == 0) {
+                                    eu[c] = v;
+                                    if (nbranch == 1 && cur.active && cur.pxok) out[c * P + cur.px] = v;
+                                } else if (cur.active && cur.pxok) {
+                                    out[c * P + cur.px] = eu[c] + a.guidance * (v - eu[c]);
+                                }
                             }
                         }
                     }
@@ -720,12 +743,9 @@ void pack_x6_t(const float* W1, const float* W2, const float* W3, const float* W
                             put(L::off(1 + layer * NB + b) + ((g2 * NB + nb) * 3) * 64 + l, u,
                                 Wm[(32 * nb + l % 32) * W + fin(b, g2, l, u)]);
     }
-    for (int b = 0; b < NB; ++b)
-        for (int g2 = 0; g2 < 2; ++g2)
-            for (int l = 0; l < 64; ++l)
-                for (int u = 0; u < 8; ++u)
-                    put(L::off(1 + 2 * NB) + ((b * 2 + g2) * 3) * 64 + l, u,
-                        (l % 32 < C) ? W4[(l % 32) * W + fin(b, g2, l, u)] : 0.f);
+    float* f4w = f + (size_t)L::off(1 + 2 * NB) * 4;              // layer 4: fp32 [C][W]
+    for (int c = 0; c < C; ++c)
+        for (int k = 0; k < W; ++k) f4w[c * W + k] = W4[(size_t)c * W + k];
 }
 
 int device_cus();
