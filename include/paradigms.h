@@ -144,7 +144,9 @@ pd_status pd_schedule_multistep_tables(const pd_schedule* s, float* R, float* S)
  *                   h3 = GELU(W3 h2 + b3), eps = W4 h3 + b4.
  *  PD_MODEL_CONV1X1 the same four layers applied to every pixel's channel
  *                   vector of a [C][H][W] sample, with SiLU activations
- *                   (a stack of 1x1 convolutions).
+ *                   (a stack of 1x1 convolutions).  Built for C = 4 and
+ *                   W in {32, 64, 96, 128, 320}; other shapes return
+ *                   PD_ERR_UNSUPPORTED.
  *  e_n: sinusoidal embedding of width W, sin(n f_k) for k < W/2 and
  *  cos(n f_{k-W/2}) after, f_k = exp(-ln(1e4) k/(W/2)).
  *  Classifier-free guidance (cond_dim > 0, conv1x1 only): the conditional

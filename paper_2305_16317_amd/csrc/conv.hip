@@ -785,7 +785,8 @@ void launch_x6_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s
     PD_HIP(hipGetLastError());
 }
 
-#define PD_CONV_SHAPES(X) X(1, 4) X(2, 4) X(4, 4) X(10, 4)
+// (blocks of 32 features, channels): widths 32, 64, 96, 128 and 320 over 4 channels
+#define PD_CONV_SHAPES(X) X(1, 4) X(2, 4) X(3, 4) X(4, 4) X(10, 4)
 
 }  // namespace
 

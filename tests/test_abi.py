@@ -138,7 +138,7 @@ def test_denoiser_argument_validation_precedes_device():
     assert e.value.code == pd.PD_ERR_INVALID_ARG
     conv = {k: np.zeros((4, 4), np.float32) for k in pd.WEIGHT_ORDER[pd.PD_MODEL_CONV1X1]}
     with pytest.raises(pd.PdError) as e:
-        pd.pd_denoiser_create(pd.PD_MODEL_CONV1X1, (4, 8, 8), conv, s, width=96)
+        pd.pd_denoiser_create(pd.PD_MODEL_CONV1X1, (4, 8, 8), conv, s, width=160)
     assert e.value.code == pd.PD_ERR_UNSUPPORTED
 
 

@@ -107,6 +107,7 @@ def test_mlp_forward(shape, width, M):
     ((4, 8, 8), 32, 3, 0),        # two full pixel tiles per row
     ((4, 6, 7), 64, 5, 0),        # ragged last tile (42 pixels)
     ((4, 5, 5), 128, 2, 0),
+    ((4, 7, 9), 96, 3, 0),        # odd number of 32-feature blocks: the halves own 2 and 1
     ((4, 16, 16), 320, 7, 0),     # production width, 8 tiles per row, idle waves
     ((4, 96, 96), 320, 2, 0),     # production shape
     ((4, 6, 6), 64, 3, 24),       # classifier-free guidance, w = 7.5
@@ -147,6 +148,7 @@ def test_conv1x1_forward_is_fp32_accurate(scale):
     ((4, 16, 16), 320, 3, 0),     # production width
     ((4, 96, 96), 320, 2, 768),   # production shape with guidance, 768-d condition
     ((4, 6, 6), 128, 3, 24),
+    ((4, 7, 9), 96, 3, 0),
 ])
 def test_conv1x1_bf16_forward(shape, width, M, cond):
     """bf16 operands, fp32 accumulation: against the oracle's bf16-operand mode
@@ -204,6 +206,7 @@ SMALL = {
     # eight samples sharing the window: 40-row layer launches, any-of-batch strides
     "mlp_b8": lambda: W.small_variant("policy_mlp_ddpm100", T=40, p=5, shape=(8, 6), width=64, batch=8),
     "conv_ddpm": lambda: W.small_variant("latent_ddpm1000_p64", T=40, p=16, shape=(4, 16, 16), width=64),
+    "conv_w96": lambda: W.small_variant("latent_ddpm1000_p64", T=30, p=12, shape=(4, 9, 10), width=96),
     "conv_ddpm_w320": lambda: W.small_variant("latent_ddpm1000_p64", T=60, p=32, shape=(4, 8, 12), width=320),
     "conv_ddim_b3": lambda: W.small_variant("latent_ddim200_b4", T=30, p=8, shape=(4, 6, 7), width=32, batch=3),
     "conv_p128": lambda: W.small_variant("latent_ddpm1000_p64", T=200, p=128, shape=(4, 4, 8), width=32),
