@@ -108,6 +108,7 @@ def test_mlp_forward(shape, width, M):
     ((4, 6, 7), 64, 5, 0),        # ragged last tile (42 pixels)
     ((4, 5, 5), 128, 2, 0),
     ((4, 7, 9), 96, 3, 0),        # odd number of 32-feature blocks: the halves own 2 and 1
+    ((4, 1, 3), 64, 9, 0),        # three pixels: one tile per row, 29 idle lanes
     ((4, 16, 16), 320, 7, 0),     # production width, 8 tiles per row, idle waves
     ((4, 96, 96), 320, 2, 0),     # production shape
     ((4, 6, 6), 64, 3, 24),       # classifier-free guidance, w = 7.5
