@@ -13,9 +13,9 @@ the steps as it does over samples.  Prints one JSON line:
   ms_per_step  sample latency in ms (mean over the timed steps)
   roofline     the dominant kernel (the denoiser on the matrix cores):
                algorithmic FLOPs per launch over its mean event-timed duration;
-               the fp32 latent network runs each multiply-add as six bf16
-               products, so it is priced at six bf16 FLOPs per fp32 one
-               against the bf16 peak
+               the fp32 latent network runs each multiply-add as three fp16
+               products, so it is priced at three fp16 FLOPs per fp32 one
+               against the fp16 peak
   roofline_update  the Picard update (scan + error partials), HBM-bound
   cpu_baseline the CPU oracle (float32 NumPy) timed on a bounded sample of the
                same workload on this host
@@ -33,7 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "sample latency (ms) + denoiser evals/s at T=1000, p=64; % HBM / MFMA peak"
-PEAK = {"f32": 157.3e12, "bf16": 2.5e15}       # dense MFMA FLOP/s, MI355X
+PEAK = {"f32": 157.3e12, "bf16": 2.5e15, "f16": 2.5e15}   # dense MFMA FLOP/s, MI355X
 HBM_PEAK = 8.0e12                              # bytes/s
 
 
@@ -91,13 +91,14 @@ def metric_name(wl) -> str:
 
 
 def denoiser_kernel(wl, dtype: str) -> str:
-    conv = "k_conv_bf16" if dtype == "bf16" else "k_conv_f32x6"
+    conv = "k_conv_bf16" if dtype == "bf16" else "k_conv_f32x3"
     return {"conv1x1": conv, "mlp": "k_linear", "gmm2d": "k_gmm"}[wl.model.kind]
 
 
-# bf16 matrix-core products per fp32 multiply-add of the fp32 latent network
-# (each operand split into three bf16 parts, the six leading part products)
-SPLIT_PRODUCTS = 6
+# fp16 matrix-core products per fp32 multiply-add of the fp32 latent network
+# (each operand split into a leading fp16 part and a scaled fp16 remainder;
+# the three leading part products)
+SPLIT_PRODUCTS = 3
 
 
 def denoiser_roofline(wl, dtype: str, fl: float, seconds: float) -> dict:
@@ -109,9 +110,9 @@ def denoiser_roofline(wl, dtype: str, fl: float, seconds: float) -> dict:
         # width 320) run on fp32 MFMA and the VALU; counting them as split
         # products too keeps the figure simple
         ach = SPLIT_PRODUCTS * rate
-        return {"bound": "mfma", "achieved": ach / 1e12, "peak": PEAK["bf16"] / 1e12,
-                "unit": "TFLOP/s", "frac": ach / PEAK["bf16"], "peak_dtype": "bf16",
-                "bf16_products_per_fp32_flop": SPLIT_PRODUCTS,
+        return {"bound": "mfma", "achieved": ach / 1e12, "peak": PEAK["f16"] / 1e12,
+                "unit": "TFLOP/s", "frac": ach / PEAK["f16"], "peak_dtype": "f16",
+                "f16_products_per_fp32_flop": SPLIT_PRODUCTS,
                 "fp32_algorithmic_tflops": rate / 1e12,
                 "fp32_algorithmic_vs_fp32_mfma_peak": rate / PEAK["f32"]}
     return {"bound": "mfma", "achieved": rate / 1e12, "peak": PEAK[dtype] / 1e12,

@@ -1,5 +1,5 @@
 // Per-pixel 4-layer stack (a stack of 1x1 convolutions) of the latent
-// denoiser, fused into one kernel: k_conv_f32x6 for the fp32 network,
+// denoiser, fused into one kernel: k_conv_f32x3 for the fp32 network,
 // k_conv_bf16 for the network with bf16 matmul operands.
 //
 // Both share one design.  Each wave owns a tile of 32 pixels of one sample
@@ -295,17 +295,23 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 }
 
 // ---------------------------------------------------------------- fp32
-// k_conv_f32x6: the fp32 network with fp32-accurate products on
-// v_mfma_f32_32x32x16_bf16 for its two W x W layers.  Every fp32 operand is
-// split exactly into three bf16 parts, x = x0 + x1 + x2 (x0 the nearest bf16
-// to x, x1 the nearest to x - x0, x2 = x - x0 - x1, which has at most 8
-// significant bits), so
-// |x1| <= 2^-8 |x| and |x2| <= 2^-16 |x|.  w x is formed from the six part
-// products down to 2^-16 |w x| (w0x0, w0x1, w1x0, w0x2, w2x0, w1x1); the three
-// left out add up to about 2^-23 |w| |x|, the size of one fp32 rounding.  Each
-// part product is exact in fp32 and the sums are fp32.  A bf16 MFMA does 16
-// times the multiply-adds of an fp32 one in the same time, so the six take
-// 6/16 of the fp32 matrix-core time.
+// k_conv_f32x3: the fp32 network with fp32-accurate products on
+// v_mfma_f32_32x32x16_f16 for its two W x W layers.  Every fp32 operand is
+// split exactly into a leading fp16 part and a scaled fp16 remainder:
+// w = w0 + 2^-11 w1 with w0 the nearest fp16 to w and w1 the nearest fp16 to
+// 2^11 (w - w0), so w is kept to 2^-22 |w|.  The three products
+//   (2^11 w0) x0 + w0 x1 + w1 x0  =  2^11 (w0 x0 + w0 x1' + w1' x0)
+// (x1' = 2^-11 x1, w1' = 2^-11 w1) go into one fp32 accumulator; the one left
+// out, w1' x1', is about 2^-22 |w x|.  Each fp16 product is exact in fp32 and
+// the sums are fp32.  The weights are split on the host into the three A
+// operands 2^11 w0, w0 and w1 (exact as long as |w| < 16; Xavier weights are
+// far below).  The activations are split in registers after a per-tile
+// power-of-two scale s that puts the tile's largest input of the layer just
+// below 2^14: every value then lies in fp16's range, and the accumulator
+// holds 2^11 s (W h), removed exactly by the next activation step.  The
+// bound comes from the pre-activation values, since |SiLU(u)| <= |u|.  A
+// 32x32x16 fp16 MFMA does 16 times the multiply-adds of an fp32 one in the
+// same time, so the three take 3/16 of the fp32 matrix-core time.
 //
 // Persistent blocks of 8 waves on 4 tiles: the two waves of a tile share a
 // SIMD and split the output blocks of every layer between them (half 0 the
@@ -326,16 +332,16 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 // Layer 4 (C outputs) runs as fp32 fused multiply-adds on the VALU from W4
 // in fp32 ([C][W], 5 KB at width 320): on the matrix core its C rows would be
 // padded to 32.  LDS: two 60 KB slabs, two 16 KB exchange buffers and
-// the activation vectors, 163,328 bytes at width 320.
-typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+// the activation vectors, 163,392 bytes at width 320.
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float fl2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ fl2 widen(bf2 v) {              // bf16 pair -> fp32 pair, exact
-    const uint32_t w = __builtin_bit_cast(uint32_t, v);
-    return fl2{__builtin_bit_cast(float, w << 16), __builtin_bit_cast(float, w & 0xffff0000u)};
-}
+
+// 2^k for an integer |k| <= 126, built from its exponent field
+__device__ __forceinline__ float pow2(int k) { return __builtin_bit_cast(float, (k + 127) << 23); }
 
 template <int NB, int C>
-struct ConvLayoutX6 {                            // units of 16 B
+struct ConvLayoutX3 {                            // units of 16 B
     static constexpr int KS1 = C / 2;            // layer-1 fp32 k-steps
     static constexpr int SL1 = (NB * 64 * KS1 / 4 + 63) / 64 * 64;
     static constexpr int SLM = 2 * NB * 3 * 64;
@@ -352,8 +358,8 @@ struct ConvLayoutX6 {                            // units of 16 B
 
 template <int NB, int C>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
-    using L = ConvLayoutX6<NB, C>;
+void k_conv_f32x3(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
+    using L = ConvLayoutX3<NB, C>;
     constexpr int NT = 4;                            // tiles per block, two waves each
     constexpr int NBH = (NB + 1) / 2;                // output blocks of half 0 (half 1: NB - NBH)
     constexpr int NPR = (NBH + 1) / 2;               // pairs of them
@@ -364,6 +370,7 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
     __shared__ f4 xch_0[NT * 4 * 64];                // one input block's activations per tile
     __shared__ f4 xch_1[NT * 4 * 64];
     __shared__ __attribute__((aligned(16))) float vec[(NT + 2) * W];   // shifts of the tiles, b2, b3
+    __shared__ float s_max[2][NT][2];                // per layer, tile and half: largest |input|
 
     const int groups = src.active ? *src.active : src.max_groups;
     const int64_t ntiles = (int64_t)groups * src.group * tiles_per_row;
@@ -410,61 +417,75 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                     (__attribute__((address_space(3))) void*)(dst + c * 256), 16, 0, 0);
         }
     };
-    // SiLU(acc + v) of output block nb, v = LDS vector row vrow, in fp32
-    auto act = [&](const f16v& c, int vrow, int nb, f4 (&h)[4]) {
+    // SiLU(cs acc + v) of output block nb, v = LDS vector row vrow, in fp32;
+    // cs (a power of two) removes the scale the accumulator carries
+    auto act = [&](const f16v& c, float cs, int vrow, int nb, f4 (&h)[4]) {
         const float* v = vec + vrow * W + 32 * nb + 4 * half;
         static_for<4>([&](auto q4c) {
             constexpr int q4 = decltype(q4c)::value;
             const f4 sh = *reinterpret_cast<const f4*>(v + 8 * q4);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) h[q4][q] = silu(c[4 * q4 + q] + sh[q]);
+            for (int q = 0; q < 4; ++q) h[q4][q] = silu(__builtin_fmaf(c[4 * q4 + q], cs, sh[q]));
         });
     };
-    // the three bf16 parts of half g2 of a block's activations: the B operands of
-    // its k-step g2
-    auto split_g2 = [&](auto g2c, const f4 (&h)[4], bf8 (&p)[2][3]) {
+    // largest |cs acc + v| over this wave's output blocks (the values act
+    // takes the SiLU of), reduced over the wave
+    auto in_max = [&](const f16v (&c)[NBH], float cs, int vrow) {
+        float m = 0.f;
+        static_for<NBH>([&](auto jc) {
+            constexpr int j = decltype(jc)::value;
+            if (own(j)) {
+                const float* v = vec + vrow * W + 32 * (oh * NBH + j) + 4 * half;
+                static_for<4>([&](auto q4c) {
+                    constexpr int q4 = decltype(q4c)::value;
+                    const f4 sh = *reinterpret_cast<const f4*>(v + 8 * q4);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        m = __builtin_fmaxf(m, __builtin_fabsf(__builtin_fmaf(c[j][4 * q4 + q], cs, sh[q])));
+                });
+            }
+        });
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) m = __builtin_fmaxf(m, __shfl_xor(m, o));
+        return m;
+    };
+    // the two fp16 parts of half g2 of a block's activations, scaled by sx:
+    // the B operands of its k-step g2
+    auto split_g2 = [&](auto g2c, const f4 (&h)[4], float sx, h8 (&p)[2][2]) {
         constexpr int g2 = decltype(g2c)::value;
         static_for<2>([&](auto q4h) {
             constexpr int q4 = 2 * g2 + decltype(q4h)::value;
             static_for<2>([&](auto qc) {
                 constexpr int q = 2 * decltype(qc)::value;
                 constexpr int u = 4 * (q4 % 2) + q;
-                const fl2 hv = {h[q4][q], h[q4][q + 1]};
-                const bf2 h0 = __builtin_convertvector(hv, bf2);
-                const fl2 r1 = hv - widen(h0);                   // exact
-                const bf2 h1 = __builtin_convertvector(r1, bf2);
-                const fl2 r2 = r1 - widen(h1);                   // exact, at most 8 bits
-                const bf2 h2 = __builtin_convertvector(r2, bf2);
-                p[g2][0][u] = h0[0]; p[g2][0][u + 1] = h0[1];
-                p[g2][1][u] = h1[0]; p[g2][1][u + 1] = h1[1];
-                p[g2][2][u] = h2[0]; p[g2][2][u + 1] = h2[1];
+                const fl2 hv = fl2{h[q4][q], h[q4][q + 1]} * sx;        // exact
+                const h2 x0 = __builtin_convertvector(hv, h2);
+                const fl2 r = (hv - __builtin_convertvector(x0, fl2)) * 2048.f;   // exact
+                const h2 x1 = __builtin_convertvector(r, h2);
+                p[g2][0][u] = x0[0]; p[g2][0][u + 1] = x0[1];
+                p[g2][1][u] = x1[0]; p[g2][1][u + 1] = x1[1];
             });
         });
     };
-    auto mac6 = [&](const bf8* fr, const bf8 (&x)[3], f16v& acc0, f16v& acc1) {
-        const bf8 w0 = fr[0], w1 = fr[64], w2 = fr[128];
-        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, x[0], acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, x[1], acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, x[0], acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w0, x[2], acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w2, x[0], acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w1, x[1], acc1, 0, 0, 0);
+    auto mfma = [](const h8& w, const h8& x, const f16v& c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(w, x, c, 0, 0, 0);
     };
-    auto mac6x2 = [&](const bf8* fa, const bf8* fb, const bf8 (&x)[3], f16v& A, f16v& B) {
-        const bf8 a0 = fa[0], a1 = fa[64], a2 = fa[128];
-        const bf8 b0 = fb[0], b1 = fb[64], b2 = fb[128];
-        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, x[0], A, 0, 0, 0);
-        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, x[0], B, 0, 0, 0);
-        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, x[1], A, 0, 0, 0);
-        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, x[1], B, 0, 0, 0);
-        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, x[0], A, 0, 0, 0);
-        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, x[0], B, 0, 0, 0);
-        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, x[2], A, 0, 0, 0);
-        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, x[2], B, 0, 0, 0);
-        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, x[0], A, 0, 0, 0);
-        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b2, x[0], B, 0, 0, 0);
-        A = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, x[1], A, 0, 0, 0);
-        B = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, x[1], B, 0, 0, 0);
+    // fragments 2^11 w0, w0, w1 of one output block
+    auto mac3 = [&](const h8* fr, const h8 (&x)[2], f16v& acc) {
+        const h8 w0s = fr[0], w0 = fr[64], w1 = fr[128];
+        acc = mfma(w0s, x[0], acc);
+        acc = mfma(w0, x[1], acc);
+        acc = mfma(w1, x[0], acc);
+    };
+    auto mac3x2 = [&](const h8* fa, const h8* fb, const h8 (&x)[2], f16v& A, f16v& B) {
+        const h8 a0s = fa[0], a0 = fa[64], a1 = fa[128];
+        const h8 b0s = fb[0], b0 = fb[64], b1 = fb[128];
+        A = mfma(a0s, x[0], A);
+        B = mfma(b0s, x[0], B);
+        A = mfma(a0, x[1], A);
+        B = mfma(b0, x[1], B);
+        A = mfma(a1, x[0], A);
+        B = mfma(b1, x[0], B);
     };
     struct Tile {
         int64_t row, px;
@@ -529,29 +550,48 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
             });
 
             // ---- layers 2 and 3: one slab per input block; the block's owner
-            // activates it into an exchange buffer one slab ahead
+            // activates it into an exchange buffer one slab ahead.  cs is the
+            // scale the accumulators carry (none after layer 1's fp32 MFMAs).
+            float cs = 1.f;
             static_for<2>([&](auto lc) {
                 constexpr int layer = decltype(lc)::value;
                 const int vin = layer == 0 ? tile : NT;
+                {
+                    const float m = in_max(acc, cs, vin);
+                    if (lane == 0) s_max[layer][tile][oh] = m;   // read after the next barrier
+                }
                 if (oh == 0) {
                     f4 h[4];
-                    act(acc[0], vin, 0, h);
+                    act(acc[0], cs, vin, 0, h);
                     f4* xd = xchb(0);
                     static_for<4>([&](auto q4c) { xd[decltype(q4c)::value * 64 + lane] = h[decltype(q4c)::value]; });
                 }
                 f16v nacc[NBH];
                 static_for<NBH>([&](auto jc) { nacc[decltype(jc)::value] = f16v{}; });
+                float sx = 1.f, cs_next = 1.f;
                 static_for<NB>([&](auto bc) {
                     constexpr int b = decltype(bc)::value;
                     constexpr int slab = 1 + layer * NB + b;
                     constexpr int buf = slab & 1;
                     land();                                      // slab b and block b's activations are in
                     dma(slab + 1, buf ^ 1);
+                    if constexpr (b == 0) {
+                        // the tile's scale: its largest input m below 2^14, m 2^e < 2^(e+1)
+                        const float m = __builtin_fmaxf(s_max[layer][tile][0], s_max[layer][tile][1]);
+                        int e = 0;
+                        if (m > 0.f && m <= 3.4028235e38f) {
+                            const int be = (int)((__builtin_bit_cast(uint32_t, m) >> 23) & 0xff);
+                            e = (be == 0 ? -126 : be - 127) - 13;
+                            e = e < -64 ? -64 : (e > 64 ? 64 : e);
+                        }
+                        sx = pow2(-e);
+                        cs_next = pow2(e - 11);
+                    }
                     if constexpr (b + 1 < NB) {
                         constexpr int o = (b + 1) < NBH ? 0 : 1, jl = (b + 1) - o * NBH;
                         if (oh == o) {
                             f4 h[4];
-                            act(acc[jl], vin, b + 1, h);
+                            act(acc[jl], cs, vin, b + 1, h);
                             f4* xd = xchb((b + 1) & 1);
                             static_for<4>([&](auto q4c) { xd[decltype(q4c)::value * 64 + lane] = h[decltype(q4c)::value]; });
                         }
@@ -559,26 +599,28 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                     const f4* xs = xchb(b & 1);
                     static_for<2>([&](auto g2c) {
                         constexpr int g2 = decltype(g2c)::value;
-                        bf8 X[2][3];
+                        h8 X[2][2];
                         {
                             f4 h[4];
                             h[2 * g2] = xs[(2 * g2) * 64 + lane];
                             h[2 * g2 + 1] = xs[(2 * g2 + 1) * 64 + lane];
-                            split_g2(g2c, h, X);
+                            split_g2(g2c, h, sx, X);
                         }
                         static_for<NPR>([&](auto pc) {
                             constexpr int j = 2 * decltype(pc)::value;
-                            const bf8* fr = ldsb(buf) + ((g2 * NB + oh * NBH + j) * 3) * 64 + lane;
+                            const h8* fr = reinterpret_cast<const h8*>(ldsb(buf)) +
+                                           ((g2 * NB + oh * NBH + j) * 3) * 64 + lane;
                             if constexpr (j + 1 < NBH) {
-                                if (own(j + 1)) mac6x2(fr, fr + 3 * 64, X[g2], nacc[j], nacc[j + 1]);
-                                else mac6(fr, X[g2], nacc[j], nacc[j]);
+                                if (own(j + 1)) mac3x2(fr, fr + 3 * 64, X[g2], nacc[j], nacc[j + 1]);
+                                else mac3(fr, X[g2], nacc[j]);
                             } else {
-                                if (own(j)) mac6(fr, X[g2], nacc[j], nacc[j]);
+                                if (own(j)) mac3(fr, X[g2], nacc[j]);
                             }
                         });
                     });
                 });
                 static_for<NBH>([&](auto jc) { acc[decltype(jc)::value] = nacc[decltype(jc)::value]; });
+                cs = cs_next;
             });
 
             // ---- layer 4 (slab 2NB+1, buffer 1: W4 in fp32): C outputs as fp32
@@ -604,7 +646,7 @@ void k_conv_f32x6(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                     constexpr int j = decltype(jc)::value;
                     if (own(j)) {
                         f4 h[4];
-                        act(acc[j], NT + 1, oh * NBH + j, h);
+                        act(acc[j], cs, NT + 1, oh * NBH + j, h);
                         static_for<4>([&](auto q4c) {
                             constexpr int q4 = decltype(q4c)::value;
                             const int f = 32 * (oh * NBH + j) + 8 * q4 + 4 * half;   // features f..f+3
@@ -697,28 +739,23 @@ void pack_bf16_t(const float* W1, const float* W2, const float* W3, const float*
                         (l % 32 < C) ? to_bf16(W4[(l % 32) * W + fin(b, g2, l, u)]) : (uint16_t)0;
 }
 
-float from_bf16(uint16_t h) {
-    const uint32_t u = (uint32_t)h << 16;
-    float f;
-    std::memcpy(&f, &u, 4);
-    return f;
-}
-
-// w = p[0] + p[1] + p[2] exactly (for finite w away from the overflow edge):
-// each part is the nearest bf16 to what the previous parts leave, and the
-// differences are exact in fp32
-void split_bf16(float w, uint16_t (&p)[3]) {
-    p[0] = to_bf16(w);
-    const float r1 = w - from_bf16(p[0]);
-    p[1] = to_bf16(r1);
-    const float r2 = r1 - from_bf16(p[1]);
-    p[2] = to_bf16(r2);
+// The three A operands of an fp32 weight: 2^11 w0, w0 and w1, with w0 the
+// nearest fp16 to w and w1 the nearest fp16 to 2^11 (w - w0), which is exact
+// in fp32; 2^11 w0 is exact for |w| < 16
+void split_f16(float w, uint16_t (&p)[3]) {
+    if (!(w > -16.f && w < 16.f)) fail(PD_ERR_UNSUPPORTED, "fp32 conv weight outside (-16, 16)");
+    const _Float16 w0 = (_Float16)w;
+    const _Float16 w0s = (_Float16)((float)w0 * 2048.f);
+    const _Float16 w1 = (_Float16)((w - (float)w0) * 2048.f);
+    std::memcpy(&p[0], &w0s, 2);
+    std::memcpy(&p[1], &w0, 2);
+    std::memcpy(&p[2], &w1, 2);
 }
 
 template <int NB, int C>
-void pack_x6_t(const float* W1, const float* W2, const float* W3, const float* W4,
+void pack_x3_t(const float* W1, const float* W2, const float* W3, const float* W4,
                std::vector<uint8_t>& out) {
-    using L = ConvLayoutX6<NB, C>;
+    using L = ConvLayoutX3<NB, C>;
     constexpr int W = 32 * NB;
     out.assign((size_t)L::TOTAL * 16, 0);
     float* f = reinterpret_cast<float*>(out.data());            // layer 1: fp32 fragments
@@ -729,7 +766,7 @@ void pack_x6_t(const float* W1, const float* W2, const float* W3, const float* W
     uint16_t* h = reinterpret_cast<uint16_t*>(out.data());
     auto put = [&](int unit, int u, float w) {                  // part k -> k fragments on
         uint16_t p[3];
-        split_bf16(w, p);
+        split_f16(w, p);
         for (int k = 0; k < 3; ++k) h[((size_t)unit + (size_t)k * 64) * 8 + u] = p[k];
     };
     auto fin = [](int b, int g2, int l, int u) { return 32 * b + 16 * g2 + 8 * (u / 4) + 4 * (l / 32) + u % 4; };
@@ -774,13 +811,13 @@ int device_cus() {
 }
 
 template <int NB, int C>
-void launch_x6_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
+void launch_x3_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
     const int tiles_per_row = (int)((a.P + 31) / 32);
     const int64_t ntiles = (int64_t)src.max_groups * src.group * tiles_per_row;
     if (ntiles == 0) return;
     int64_t blocks = (ntiles + 3) / 4;                       // persistent: one block per CU
     if (blocks > device_cus()) blocks = device_cus();
-    hipLaunchKernelGGL((k_conv_f32x6<NB, C>), dim3((unsigned)blocks), dim3(512), 0, s, a, src, eps,
+    hipLaunchKernelGGL((k_conv_f32x3<NB, C>), dim3((unsigned)blocks), dim3(512), 0, s, a, src, eps,
                        tiles_per_row);
     PD_HIP(hipGetLastError());
 }
@@ -801,7 +838,7 @@ bool conv_supported(int C, int width, bool bf16) {
 size_t conv_frag_bytes(int C, int width, bool bf16) {
 #define X(nb, c)                                                                      \
     if (C == c && width == 32 * nb)                                                   \
-        return bf16 ? (size_t)ConvLayoutBf16<nb, c>::TOTAL * 16 : (size_t)ConvLayoutX6<nb, c>::TOTAL * 16;
+        return bf16 ? (size_t)ConvLayoutBf16<nb, c>::TOTAL * 16 : (size_t)ConvLayoutX3<nb, c>::TOTAL * 16;
     PD_CONV_SHAPES(X)
 #undef X
     return 0;
@@ -814,7 +851,7 @@ void conv_pack_weights(int C, int width, bool bf16, const float* W1, const float
         if (bf16)                                                 \
             pack_bf16_t<nb, c>(W1, W2, W3, W4, out);              \
         else                                                      \
-            pack_x6_t<nb, c>(W1, W2, W3, W4, out);                \
+            pack_x3_t<nb, c>(W1, W2, W3, W4, out);                \
         return;                                                   \
     }
     PD_CONV_SHAPES(X)
@@ -828,7 +865,7 @@ void launch_conv1x1(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_
         if (a.bf16)                                                \
             launch_bf16_t<nb, c>(a, src, eps, s);                  \
         else                                                       \
-            launch_x6_t<nb, c>(a, src, eps, s);                    \
+            launch_x3_t<nb, c>(a, src, eps, s);                    \
         return;                                                    \
     }
     PD_CONV_SHAPES(X)
