@@ -300,16 +300,17 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 // split exactly into a leading fp16 part and a scaled fp16 remainder:
 // w = w0 + 2^-11 w1 with w0 the nearest fp16 to w and w1 the nearest fp16 to
 // 2^11 (w - w0), so w is kept to 2^-22 |w|.  The three products
-//   (2^11 w0) x0 + w0 x1 + w1 x0  =  2^11 (w0 x0 + w0 x1' + w1' x0)
+//   w0 (2^11 x0) + w0 x1 + w1 x0  =  2^11 (w0 x0 + w0 x1' + w1' x0)
 // (x1' = 2^-11 x1, w1' = 2^-11 w1) go into one fp32 accumulator; the one left
 // out, w1' x1', is about 2^-22 |w x|.  Each fp16 product is exact in fp32 and
-// the sums are fp32.  The weights are split on the host into the three A
-// operands 2^11 w0, w0 and w1 (exact as long as |w| < 16; Xavier weights are
-// far below).  The activations are split in registers after a per-tile
-// power-of-two scale s that puts the tile's largest input of the layer just
-// below 2^14: every value then lies in fp16's range, and the accumulator
-// holds 2^11 s (W h), removed exactly by the next activation step.  The
-// bound comes from the pre-activation values, since |SiLU(u)| <= |u|.  A
+// the sums are fp32.  The weights are split on the host into the two A
+// operands w0 and w1.  The activations are split in registers into the three
+// B operands 2^11 x0, x1 and x0, after a per-tile power-of-two scale s that
+// puts the tile's largest input of the layer just below 2^4: 2^11 x0 then
+// stays below 2^15, inside fp16's range, and values down to 2^-28 of the
+// largest keep full precision.  The accumulator holds 2^11 s (W h), removed
+// exactly by the next activation step.  The bound on the inputs comes from
+// the pre-activation values, since |SiLU(u)| <= |u|.  A
 // 32x32x16 fp16 MFMA does 16 times the multiply-adds of an fp32 one in the
 // same time, so the three take 3/16 of the fp32 matrix-core time.
 //
@@ -328,11 +329,11 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 // holds, for output block nb and lane l, the C/2 values
 // W1[32 nb + l%32][2 s + l/32].  Layers 2 and 3 run on the split products,
 // with the weights split on the host: slab b holds input block b for every
-// output block nb, fragment ((g2 NB + nb) 3 + part), one 16-B unit per lane.
+// output block nb, fragment ((g2 NB + nb) 2 + part), one 16-B unit per lane.
 // Layer 4 (C outputs) runs as fp32 fused multiply-adds on the VALU from W4
 // in fp32 ([C][W], 5 KB at width 320): on the matrix core its C rows would be
-// padded to 32.  LDS: two 60 KB slabs, two 16 KB exchange buffers and
-// the activation vectors, 163,392 bytes at width 320.
+// padded to 32.  LDS: two 40 KB slabs, two 16 KB exchange buffers and
+// the activation vectors, 122,432 bytes at width 320.
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float fl2 __attribute__((ext_vector_type(2)));
@@ -344,7 +345,7 @@ template <int NB, int C>
 struct ConvLayoutX3 {                            // units of 16 B
     static constexpr int KS1 = C / 2;            // layer-1 fp32 k-steps
     static constexpr int SL1 = (NB * 64 * KS1 / 4 + 63) / 64 * 64;
-    static constexpr int SLM = 2 * NB * 3 * 64;
+    static constexpr int SLM = 2 * NB * 2 * 64;
     static constexpr int SL4 = (C * 32 * NB / 4 + 63) / 64 * 64;   // layer 4: W4 in fp32, [C][W]
     static constexpr int BUF = SL1 > SLM ? SL1 : SLM;
     static constexpr int TOTAL = SL1 + 2 * NB * SLM + SL4;
@@ -449,9 +450,9 @@ void k_conv_f32x3(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
         for (int o = 32; o >= 1; o >>= 1) m = __builtin_fmaxf(m, __shfl_xor(m, o));
         return m;
     };
-    // the two fp16 parts of half g2 of a block's activations, scaled by sx:
-    // the B operands of its k-step g2
-    auto split_g2 = [&](auto g2c, const f4 (&h)[4], float sx, h8 (&p)[2][2]) {
+    // the fp16 parts 2^11 x0, x1 and x0 of half g2 of a block's activations,
+    // scaled by sx: the B operands of its k-step g2
+    auto split_g2 = [&](auto g2c, const f4 (&h)[4], float sx, h8 (&p)[2][3]) {
         constexpr int g2 = decltype(g2c)::value;
         static_for<2>([&](auto q4h) {
             constexpr int q4 = 2 * g2 + decltype(q4h)::value;
@@ -462,30 +463,32 @@ void k_conv_f32x3(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                 const h2 x0 = __builtin_convertvector(hv, h2);
                 const fl2 r = (hv - __builtin_convertvector(x0, fl2)) * 2048.f;   // exact
                 const h2 x1 = __builtin_convertvector(r, h2);
-                p[g2][0][u] = x0[0]; p[g2][0][u + 1] = x0[1];
+                const h2 x0s = x0 * (_Float16)2048.f;                    // exact
+                p[g2][0][u] = x0s[0]; p[g2][0][u + 1] = x0s[1];
                 p[g2][1][u] = x1[0]; p[g2][1][u + 1] = x1[1];
+                p[g2][2][u] = x0[0]; p[g2][2][u + 1] = x0[1];
             });
         });
     };
     auto mfma = [](const h8& w, const h8& x, const f16v& c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_f16(w, x, c, 0, 0, 0);
     };
-    // fragments 2^11 w0, w0, w1 of one output block
-    auto mac3 = [&](const h8* fr, const h8 (&x)[2], f16v& acc) {
-        const h8 w0s = fr[0], w0 = fr[64], w1 = fr[128];
-        acc = mfma(w0s, x[0], acc);
+    // fragments w0, w1 of one output block against 2^11 x0, x1, x0
+    auto mac3 = [&](const h8* fr, const h8 (&x)[3], f16v& acc) {
+        const h8 w0 = fr[0], w1 = fr[64];
+        acc = mfma(w0, x[0], acc);
         acc = mfma(w0, x[1], acc);
-        acc = mfma(w1, x[0], acc);
+        acc = mfma(w1, x[2], acc);
     };
-    auto mac3x2 = [&](const h8* fa, const h8* fb, const h8 (&x)[2], f16v& A, f16v& B) {
-        const h8 a0s = fa[0], a0 = fa[64], a1 = fa[128];
-        const h8 b0s = fb[0], b0 = fb[64], b1 = fb[128];
-        A = mfma(a0s, x[0], A);
-        B = mfma(b0s, x[0], B);
+    auto mac3x2 = [&](const h8* fa, const h8* fb, const h8 (&x)[3], f16v& A, f16v& B) {
+        const h8 a0 = fa[0], a1 = fa[64];
+        const h8 b0 = fb[0], b1 = fb[64];
+        A = mfma(a0, x[0], A);
+        B = mfma(b0, x[0], B);
         A = mfma(a0, x[1], A);
         B = mfma(b0, x[1], B);
-        A = mfma(a1, x[0], A);
-        B = mfma(b1, x[0], B);
+        A = mfma(a1, x[2], A);
+        B = mfma(b1, x[2], B);
     };
     struct Tile {
         int64_t row, px;
@@ -576,12 +579,12 @@ void k_conv_f32x3(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                     land();                                      // slab b and block b's activations are in
                     dma(slab + 1, buf ^ 1);
                     if constexpr (b == 0) {
-                        // the tile's scale: its largest input m below 2^14, m 2^e < 2^(e+1)
+                        // the tile's scale: its largest input m below 2^4, m 2^e < 2^(e+1)
                         const float m = __builtin_fmaxf(s_max[layer][tile][0], s_max[layer][tile][1]);
                         int e = 0;
                         if (m > 0.f && m <= 3.4028235e38f) {
                             const int be = (int)((__builtin_bit_cast(uint32_t, m) >> 23) & 0xff);
-                            e = (be == 0 ? -126 : be - 127) - 13;
+                            e = (be == 0 ? -126 : be - 127) - 3;
                             e = e < -64 ? -64 : (e > 64 ? 64 : e);
                         }
                         sx = pow2(-e);
@@ -599,7 +602,7 @@ void k_conv_f32x3(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                     const f4* xs = xchb(b & 1);
                     static_for<2>([&](auto g2c) {
                         constexpr int g2 = decltype(g2c)::value;
-                        h8 X[2][2];
+                        h8 X[2][3];
                         {
                             f4 h[4];
                             h[2 * g2] = xs[(2 * g2) * 64 + lane];
@@ -609,9 +612,9 @@ void k_conv_f32x3(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                         static_for<NPR>([&](auto pc) {
                             constexpr int j = 2 * decltype(pc)::value;
                             const h8* fr = reinterpret_cast<const h8*>(ldsb(buf)) +
-                                           ((g2 * NB + oh * NBH + j) * 3) * 64 + lane;
+                                           ((g2 * NB + oh * NBH + j) * 2) * 64 + lane;
                             if constexpr (j + 1 < NBH) {
-                                if (own(j + 1)) mac3x2(fr, fr + 3 * 64, X[g2], nacc[j], nacc[j + 1]);
+                                if (own(j + 1)) mac3x2(fr, fr + 2 * 64, X[g2], nacc[j], nacc[j + 1]);
                                 else mac3(fr, X[g2], nacc[j]);
                             } else {
                                 if (own(j)) mac3(fr, X[g2], nacc[j]);
@@ -739,17 +742,14 @@ void pack_bf16_t(const float* W1, const float* W2, const float* W3, const float*
                         (l % 32 < C) ? to_bf16(W4[(l % 32) * W + fin(b, g2, l, u)]) : (uint16_t)0;
 }
 
-// The three A operands of an fp32 weight: 2^11 w0, w0 and w1, with w0 the
-// nearest fp16 to w and w1 the nearest fp16 to 2^11 (w - w0), which is exact
-// in fp32; 2^11 w0 is exact for |w| < 16
-void split_f16(float w, uint16_t (&p)[3]) {
-    if (!(w > -16.f && w < 16.f)) fail(PD_ERR_UNSUPPORTED, "fp32 conv weight outside (-16, 16)");
+// The two A operands of an fp32 weight: w0, the nearest fp16 to w, and w1,
+// the nearest fp16 to 2^11 (w - w0) (the difference is exact in fp32)
+void split_f16(float w, uint16_t (&p)[2]) {
+    if (!(w > -65504.f && w < 65504.f)) fail(PD_ERR_UNSUPPORTED, "fp32 conv weight outside fp16's range");
     const _Float16 w0 = (_Float16)w;
-    const _Float16 w0s = (_Float16)((float)w0 * 2048.f);
     const _Float16 w1 = (_Float16)((w - (float)w0) * 2048.f);
-    std::memcpy(&p[0], &w0s, 2);
-    std::memcpy(&p[1], &w0, 2);
-    std::memcpy(&p[2], &w1, 2);
+    std::memcpy(&p[0], &w0, 2);
+    std::memcpy(&p[1], &w1, 2);
 }
 
 template <int NB, int C>
@@ -765,9 +765,9 @@ void pack_x3_t(const float* W1, const float* W2, const float* W3, const float* W
                 f[L::off(0) * 4 + (nb * 64 + l) * L::KS1 + s] = W1[(32 * nb + l % 32) * C + 2 * s + l / 32];
     uint16_t* h = reinterpret_cast<uint16_t*>(out.data());
     auto put = [&](int unit, int u, float w) {                  // part k -> k fragments on
-        uint16_t p[3];
+        uint16_t p[2];
         split_f16(w, p);
-        for (int k = 0; k < 3; ++k) h[((size_t)unit + (size_t)k * 64) * 8 + u] = p[k];
+        for (int k = 0; k < 2; ++k) h[((size_t)unit + (size_t)k * 64) * 8 + u] = p[k];
     };
     auto fin = [](int b, int g2, int l, int u) { return 32 * b + 16 * g2 + 8 * (u / 4) + 4 * (l / 32) + u % 4; };
     for (int layer = 0; layer < 2; ++layer) {
@@ -777,7 +777,7 @@ void pack_x3_t(const float* W1, const float* W2, const float* W3, const float* W
                 for (int nb = 0; nb < NB; ++nb)
                     for (int l = 0; l < 64; ++l)
                         for (int u = 0; u < 8; ++u)
-                            put(L::off(1 + layer * NB + b) + ((g2 * NB + nb) * 3) * 64 + l, u,
+                            put(L::off(1 + layer * NB + b) + ((g2 * NB + nb) * 2) * 64 + l, u,
                                 Wm[(32 * nb + l % 32) * W + fin(b, g2, l, u)]);
     }
     float* f4w = f + (size_t)L::off(1 + 2 * NB) * 4;              // layer 4: fp32 [C][W]
