@@ -124,11 +124,44 @@ def test_conv1x1_forward(shape, width, M, cond):
     assert _rel(got, ref) <= REL_F32
 
 
+@pytest.mark.parametrize("w1_scale,w2_scale", [(1, 1e-6), (1, 1e-3), (1, 1e2), (100, 1e3)])
+def test_conv1x1_fp32_hidden_scales(w1_scale, w2_scale):
+    """Hidden activations far below fp16's range (W2 scaled down: layer-3
+    inputs near 1e-6) and far above it (W1 and W2 scaled up: layer-3 inputs
+    near 1e5): the per-tile power-of-two scale keeps the split products as
+    accurate as float32 against a float64 evaluation."""
+    wl = _wl("conv1x1", (4, 16, 16), 320, T=1000)
+    w = dict(W.make_weights(wl.model))
+    w["W1"] = (w["W1"].astype(np.float64) * w1_scale).astype(np.float32)
+    w["W2"] = (w["W2"].astype(np.float64) * w2_scale).astype(np.float32)
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((3, 4, 16, 16)).astype(np.float32)
+    n = rng.integers(0, 1000, 3).astype(np.int32)
+    got = _forward(wl, w, x, n)
+    tb = schedule.from_spec(wl.schedule)
+    ref64 = denoisers.Denoiser(wl.model, w, tb.alphabar, np.float64, False)(x.astype(np.float64), n)
+    ref64 = ref64.reshape(3, -1)
+    e_dev, e_32 = _rel(got, ref64), _rel(_oracle_eps(wl, w, x, n), ref64)
+    assert np.isfinite(got).all()
+    assert e_dev <= max(2 * e_32, 1e-7), (e_dev, e_32)
+
+
+def test_conv1x1_fp32_rejects_weights_beyond_fp16():
+    """A weight the two-part fp16 split cannot hold fails creation."""
+    wl = _wl("conv1x1", (4, 8, 8), 32, T=1000)
+    w = dict(W.make_weights(wl.model))
+    w["W3"] = w["W3"].copy()
+    w["W3"][0, 0] = 1e5
+    with pytest.raises(pd.PdError) as e:
+        pd.from_workload(wl, w)
+    assert e.value.code == pd.PD_ERR_UNSUPPORTED
+
+
 @pytest.mark.parametrize("scale", [1.0, 1e3, 1e-3])
 def test_conv1x1_forward_is_fp32_accurate(scale):
-    """The fp32 network runs on bf16 matrix cores with each operand split into
-    three bf16 parts: against a float64 evaluation it must be at least as
-    accurate as a plain float32 one, at any input scale."""
+    """The fp32 network runs on fp16 matrix cores with each operand split into
+    an fp16 part and a scaled fp16 remainder: against a float64 evaluation it
+    must be at least as accurate as a plain float32 one, at any input scale."""
     wl = _wl("conv1x1", (4, 16, 16), 320, T=1000)
     w = W.make_weights(wl.model)
     rng = np.random.default_rng(7)
