@@ -17,9 +17,12 @@
 namespace pd {
 namespace {
 
-constexpr int kScanWaves = 16;            // waves per scan block, split along the window
-constexpr int kScanMaxRows = 8;           // rows per wave: windows up to 16 * 8 = 128 points
-constexpr int kMaxWindow = kScanWaves * kScanMaxRows;
+// Waves per scan block, split along the window: 8 for windows of up to 64
+// points, 16 above (up to 8 rows per wave, so windows up to 128 points).  At
+// 64 points and 4 x 4 x 96 x 96 columns, 8 waves of 8 rows took 20.8 us per
+// launch against 25.3 us for 16 waves of 4; 16 rows per wave spill.
+constexpr int kScanMaxRows = 8;
+constexpr int kMaxWindow = 16 * kScanMaxRows;
 
 // Columns per lane of the scan: four (one 16-byte access per row) when the
 // sample size allows it, else one.
@@ -255,7 +258,7 @@ __global__ __launch_bounds__(1024) void k_picard_finalize(FinalizeArgs a, int nb
 
 
 // One block: 64 * VEC consecutive columns of one sample b, all window rows,
-// split over 16 waves (rows [w*ch, (w+1)*ch) per wave, ch <= R).  Drift and
+// split over NW waves (rows [w*ch, (w+1)*ch) per wave, ch <= R).  Drift and
 // noise are summed along the rows inside each wave, the wave totals are
 // exchanged through LDS, and the new points x^{k+1}_{t+j+1} = x_t + sum y +
 // sum z are written back to the ring.  All loads use clamped, always-valid
@@ -270,15 +273,14 @@ __global__ __launch_bounds__(1024) void k_picard_finalize(FinalizeArgs a, int nb
 // previous row's point and epsilon, or for a wave's first row the ones
 // before it (for the window's first row, the history row x_{t-1} that the
 // batch evaluated first).
-template <int R, int VEC, bool NOISE, bool DPM>
-__global__ __launch_bounds__(kScanWaves * 64) void k_picard_scan(
+template <int NW, int R, int VEC, bool NOISE, bool DPM>
+__global__ __launch_bounds__(NW * 64) void k_picard_scan(
     const LoopState* __restrict__ st, float* ring, const float* __restrict__ eps,
     const float* __restrict__ noise, const float* __restrict__ Atab,
     const float* __restrict__ Btab, const float* __restrict__ Rtab,
     const float* __restrict__ Stab, int p, int batch, int64_t D, float* __restrict__ partials,
     FinalizeArgs fin, int fuse_finalize) {
     typedef typename Cols<VEC>::type V;
-    constexpr int NW = kScanWaves;
     const LoopState cur = *st;
     const int pe = cur.p_eff;
     if (pe <= 0) return;
@@ -589,22 +591,22 @@ void launch_seq_heun_combine(float* eps, const float* eps2, int64_t n, hipStream
     PD_HIP(hipGetLastError());
 }
 
-template <int R, int VEC>
+template <int NW, int R, int VEC>
 static bool launch_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
                         const float* A, const float* B, const float* Rt, const float* St, int p,
                         int batch, int64_t D, float* partials, const FinalizeArgs& fin,
                         hipStream_t s) {
     const dim3 grid((unsigned)picard_partial_blocks(D), (unsigned)batch);
     const int fuse = grid.x * grid.y == 1;   // one block: the finalize works from LDS
-    const dim3 block(kScanWaves * 64);
+    const dim3 block(NW * 64);
     if (Rt)      // DPM-Solver integrates the noise-free chain
-        hipLaunchKernelGGL((k_picard_scan<R, VEC, false, true>), grid, block, 0, s, st, ring, eps,
+        hipLaunchKernelGGL((k_picard_scan<NW, R, VEC, false, true>), grid, block, 0, s, st, ring, eps,
                            noise, A, B, Rt, St, p, batch, D, partials, fin, fuse);
     else if (noise)
-        hipLaunchKernelGGL((k_picard_scan<R, VEC, true, false>), grid, block, 0, s, st, ring, eps,
+        hipLaunchKernelGGL((k_picard_scan<NW, R, VEC, true, false>), grid, block, 0, s, st, ring, eps,
                            noise, A, B, Rt, St, p, batch, D, partials, fin, fuse);
     else
-        hipLaunchKernelGGL((k_picard_scan<R, VEC, false, false>), grid, block, 0, s, st, ring, eps,
+        hipLaunchKernelGGL((k_picard_scan<NW, R, VEC, false, false>), grid, block, 0, s, st, ring, eps,
                            noise, A, B, Rt, St, p, batch, D, partials, fin, fuse);
     PD_HIP(hipGetLastError());
     return fuse != 0;
@@ -616,17 +618,19 @@ bool launch_picard_scan(const LoopState* st, float* ring, const float* eps, cons
                         hipStream_t s) {
     if (p > kMaxWindow) fail(PD_ERR_UNSUPPORTED, "window larger than 128 points");
     if (R && noise) fail(PD_ERR_INVALID_ARG, "the multistep drift is for the noise-free chain");
-    const int ch = (p + kScanWaves - 1) / kScanWaves;    // rows per wave at a full window
     const bool v4 = scan_vec(D) == 4;
-#define PD_SCAN(RR)                                                                             \
-    if (ch <= RR)                                                                               \
-        return v4 ? launch_scan<RR, 4>(st, ring, eps, noise, A, B, R, S, p, batch, D, partials,  \
+#define PD_SCAN(NW, RR)                                                                          \
+    return v4 ? launch_scan<NW, RR, 4>(st, ring, eps, noise, A, B, R, S, p, batch, D, partials, \
                                        fin, s)                                                   \
-                  : launch_scan<RR, 1>(st, ring, eps, noise, A, B, R, S, p, batch, D, partials,  \
+              : launch_scan<NW, RR, 1>(st, ring, eps, noise, A, B, R, S, p, batch, D, partials, \
                                        fin, s);
-    PD_SCAN(1) PD_SCAN(2) PD_SCAN(4) PD_SCAN(8)
+    if (p > 64) PD_SCAN(16, 8)
+    const int ch = (p + 7) / 8;      // rows per wave at a full window, 8 waves
+    if (ch <= 1) PD_SCAN(8, 1)
+    if (ch <= 2) PD_SCAN(8, 2)
+    if (ch <= 4) PD_SCAN(8, 4)
+    PD_SCAN(8, 8)
 #undef PD_SCAN
-    return false;
 }
 
 void launch_picard_finalize(const FinalizeArgs& fin, hipStream_t s) {
