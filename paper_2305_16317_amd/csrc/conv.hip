@@ -585,7 +585,7 @@ void k_conv_f32x3(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
                         if (m > 0.f && m <= 3.4028235e38f) {
                             const int be = (int)((__builtin_bit_cast(uint32_t, m) >> 23) & 0xff);
                             e = (be == 0 ? -126 : be - 127) - 3;
-                            e = e < -64 ? -64 : (e > 64 ? 64 : e);
+                            e = e < -100 ? -100 : (e > 120 ? 120 : e);   // 2^-e, 2^(e-11) normal
                         }
                         sx = pow2(-e);
                         cs_next = pow2(e - 11);
