@@ -9,10 +9,11 @@
 // D[i][j] in lane j + 32 ((i/4) % 2), register (i%4) + 4 (i/8), so the
 // accumulator of output block nb holds, in lane l and register r, feature
 // 32 nb + 8 (r/4) + 4 (l/32) + r%4 of pixel l%32.  On
-// v_mfma_f32_32x32x16_bf16 (A[i][k] in lane i + 32 (k/8), B[k][j] in lane
-// j + 32 (k/8), element k%8 of 8 packed bf16) accumulator registers
-// 8 g2 .. 8 g2 + 7 of block b, converted to bf16 and packed, are exactly the
-// B operand of k-step (b, g2) of the next layer: lane half h then carries
+// v_mfma_f32_32x32x16_bf16 and _f16 (A[i][k] in lane i + 32 (k/8), B[k][j] in
+// lane j + 32 (k/8), element k%8 of 8 packed 16-bit values) accumulator
+// registers 8 g2 .. 8 g2 + 7 of block b, activated, converted to 16 bits and
+// packed, are exactly the B operand of k-step (b, g2) of the next layer
+// (through an LDS exchange in k_conv_f32x3): lane half h then carries
 // input features 32 b + 16 g2 + 8 (u/4) + 4 h + u%4, u = 0..7, and the host
 // packs the weights with the same permutation of the reduction index.  No
 // activation ever leaves the registers.
