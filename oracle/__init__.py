@@ -65,8 +65,8 @@ class Problem:
         return samplers.sequential(self.tables, self.eps, self.x0, self.noise,
                                    self.dtype)
 
-    def picard(self, p=None, tau=None, tol_offset=0, on_iter=None):
+    def picard(self, p=None, tau=None, tol_offset=0, on_iter=None, rule="relaxed"):
         return samplers.picard(self.tables, self.eps, self.x0, self.noise,
                                self.w.p if p is None else p,
                                self.w.tau if tau is None else tau,
-                               self.dtype, tol_offset, on_iter)
+                               self.dtype, tol_offset, on_iter, rule)

@@ -23,7 +23,11 @@ picard()      -- Algorithm 1, step for step, on the whole trajectory array:
                  per-point error (1/D)|x^{k+1} - x^k|^2 over window offsets
                  [1, p), the stride = first offset whose error exceeds
                  tau^2 sigma^2 (else p), new points initialised to the window's
-                 last point, t += stride, p = min(p, T - t).
+                 last point, t += stride, p = min(p, T - t).  With
+                 ``rule="prop2"`` the stride test is Prop. 2's instead: the
+                 squared norm |x^{k+1} - x^k|^2 (no 1/D) against
+                 4 eps^2 sigma^2 / T^2, with the total-variation bound eps
+                 passed as ``tau``.
 
 Readings of the text that Algorithm 1 leaves open:
 * the sigma in the stride test is that of the point's own absolute step,
@@ -34,7 +38,10 @@ Readings of the text that Algorithm 1 leaves open:
 * with a batch of several samples sharing one window, an offset fails when any
   sample fails;
 * new points past T are not created (the window never extends past T);
-* a non-finite point or error stops the run with ``NumericError``.
+* a non-finite point or error stops the run with ``NumericError``;
+* Prop. 2's threshold factor 4 eps^2 / T^2 is formed in float64 from eps
+  (taken in the run's precision) and rounded once to that precision; the
+  threshold of a point is that factor times sigma^2, as for tau^2.
 The running sums follow the algorithm's formula literally, left end +
 cumulative drift + cumulative noise, each cumulative sum taken in order
 (numpy's ``cumsum`` accumulates sequentially).
@@ -156,20 +163,38 @@ def sequential_mean_form(tables, eps_fn: Callable, x0: np.ndarray,
     return x
 
 
+RULES = ("relaxed", "prop2")
+
+
+def stop_factor(rule: str, tau: float, T: int, dtype) -> np.floating:
+    """Factor of sigma^2 in the stride test's threshold: tau^2 for the relaxed
+    rule of Sec. 3.1 (per-dimension mean error), 4 eps^2 / T^2 for Prop. 2
+    (squared norm; eps = ``tau``)."""
+    f = np.dtype(dtype).type
+    t = f(tau)
+    if rule == "relaxed":
+        return t * t
+    if rule == "prop2":
+        e = float(t)
+        return f(4.0 * e * e / (float(T) * float(T)))
+    raise ValueError(f"unknown stopping rule {rule!r}")
+
+
 def picard(tables, eps_fn: Callable, x0: np.ndarray, noise: np.ndarray,
            p: int, tau: float, dtype=np.float32, tol_offset: int = 0,
-           on_iter: Optional[Callable] = None) -> PicardResult:
+           on_iter: Optional[Callable] = None, rule: str = "relaxed") -> PicardResult:
     """Algorithm 1 on a full [T+1, B, D] trajectory array.
 
     x0: [B, D] prior point; noise: [T, B, D] the up-front z_i.
+    rule: "relaxed" (Sec. 3.1: (1/D)|dx|^2 <= tau^2 sigma^2) or "prop2"
+    (Prop. 2: |dx|^2 <= 4 tau^2 sigma^2 / T^2, tau being the bound eps).
     ``on_iter(k, t, p_eff, x_old, x_new, err, stride)`` is called after each
     iteration, for tests: x_old[j] is x^k_{t+j} for j in [0, p_eff] and
     x_new[j] is x^{k+1}_{t+j+1} for j in [0, p_eff).
     """
     T = tables.T
     A, Bc, _, tolv = _tables(tables, dtype)
-    tau_d = np.dtype(dtype).type(tau)
-    tau2 = tau_d * tau_d
+    tau2 = stop_factor(rule, tau, T, dtype)
     x0 = np.asarray(x0, dtype=dtype)
     Bn, D = x0.shape
     X = np.empty((T + 1, Bn, D), dtype=dtype)
@@ -193,9 +218,14 @@ def picard(tables, eps_fn: Callable, x0: np.ndarray, noise: np.ndarray,
         tol = np.zeros(pe, dtype=dtype)
         for j in range(1, pe):
             dlt = Xn[j - 1] - X[t + j]          # x^{k+1}_{t+j} - x^k_{t+j}
-            err[j] = np.mean(dlt * dlt, axis=1, dtype=dtype)
+            if rule == "prop2":
+                err[j] = np.sum(dlt * dlt, axis=1, dtype=dtype)
+            else:
+                err[j] = np.mean(dlt * dlt, axis=1, dtype=dtype)
             s2 = tolv[t + j + tol_offset]
             tol[j] = tau2 * s2 if s2 != 0 else s2
+        if not np.all(np.isfinite(err)):
+            raise NumericError(f"non-finite error at iteration {k}")
         stride = stride_from_errors(err, tol, pe)
         x_old = X[t:t + pe + 1].copy() if on_iter is not None else None
         X[t + 1:t + pe + 1] = Xn

@@ -169,8 +169,10 @@ def test_first_k_points_exact_after_k_iterations():
 
 
 # ----------------------------------------------------------------- brute force
-def _brute_picard(tb, eps_fn, x0, z, p, tau):
-    """Algorithm 1 with explicit loops over single points and offsets."""
+def _brute_picard(tb, eps_fn, x0, z, p, tau, rule="relaxed"):
+    """Algorithm 1 with explicit loops over single points and offsets; with
+    rule="prop2" the stride test is Prop. 2's |dx|^2 <= 4 eps^2 sigma^2 / T^2
+    (eps = tau)."""
     T = tb.T
     x = {0: x0.copy()}
     for i in range(1, min(p, T) + 1):
@@ -190,9 +192,14 @@ def _brute_picard(tb, eps_fn, x0, z, p, tau):
         stride = pe
         for j in range(1, pe):
             d = new[t + j] - x[t + j]
-            errs = (d * d).sum(axis=1) / d.shape[1]
             s2 = tb.tol_var[t + j]
-            if any(not (e <= (tau * tau * s2 if s2 > 0 else 0.0)) for e in errs):
+            if rule == "prop2":
+                errs = (d * d).sum(axis=1)
+                thr = 4 * tau ** 2 * s2 / T ** 2 if s2 > 0 else 0.0
+            else:
+                errs = (d * d).sum(axis=1) / d.shape[1]
+                thr = tau * tau * s2 if s2 > 0 else 0.0
+            if any(not (e <= thr) for e in errs):
                 stride = j
                 break
         x.update(new)
@@ -280,3 +287,85 @@ def test_brute_force_longer_chains(tau, p):
         xb, kb, tb_ = _brute_picard(pr.tables, pr.eps, pr.x0, pr.noise, p, tau)
         assert (r.iters, r.trace) == (kb, tb_)
         assert np.allclose(r.x, xb, rtol=1e-13, atol=1e-13)
+
+
+# ------------------------------------------------- Prop. 2's stopping rule
+@pytest.mark.parametrize("T", [1, 2, 3, 4])
+@pytest.mark.parametrize("eps", [0.0, 1.0, 30.0, INF])
+@pytest.mark.parametrize("kind", ["ddpm", "ddim"])
+def test_prop2_brute_force_tiny(T, eps, kind):
+    pr = _gmm_problem(T=T, batch=2, kind=kind, seed=T + 7)
+    for p in range(1, T + 1):
+        r = pr.picard(p=p, tau=eps, rule="prop2")
+        xb, kb, tb_ = _brute_picard(pr.tables, pr.eps, pr.x0, pr.noise, p, eps, "prop2")
+        assert (r.iters, r.trace) == (kb, tb_)
+        assert np.allclose(r.x, xb, rtol=1e-13, atol=1e-13)
+        assert math.ceil(T / p) <= r.iters <= T
+
+
+@pytest.mark.parametrize("eps", [1.0, 5.0, 20.0])
+def test_prop2_brute_force_longer_chains(eps):
+    for kind in ("ddpm", "ddim"):
+        pr = _gmm_problem(T=24, batch=2, kind=kind, seed=13)
+        r = pr.picard(p=8, tau=eps, rule="prop2")
+        xb, kb, tb_ = _brute_picard(pr.tables, pr.eps, pr.x0, pr.noise, 8, eps, "prop2")
+        assert (r.iters, r.trace) == (kb, tb_)
+        assert np.allclose(r.x, xb, rtol=1e-13, atol=1e-13)
+
+
+def _pow2_problem(kind, dtype):
+    """D = 16 (sqrt D = 4) and T a power of two, so that tau = 2 eps / (T sqrt D)
+    and every threshold are exact binary fractions."""
+    sch = W.ScheduleSpec("ddpm", 32, 32) if kind == "ddpm" else W.ScheduleSpec("ddim", 64, 16)
+    wl = W.Workload("t", sch, W.ModelSpec("mlp", (4, 4), width=32, weight_seed=9),
+                    p=8, tau=0.1, batch=2, noise_seed=4)
+    return Problem(wl, W.make_weights(wl.model), dtype)
+
+
+@pytest.mark.parametrize("kind", ["ddpm", "ddim"])
+@pytest.mark.parametrize("dtype", [np.float32, np.float64])
+@pytest.mark.parametrize("eps", [0.5, 4.0, 64.0, 1024.0])
+def test_prop2_equals_relaxed_rule_at_matching_tau(kind, dtype, eps):
+    """Prop. 2 bounds the squared norm |dx|^2 by 4 eps^2 sigma^2 / T^2; the
+    relaxed rule bounds (1/D) |dx|^2 by tau^2 sigma^2.  The two tests are the
+    same inequality when tau = 2 eps / (T sqrt D): the same strides and the
+    same sample, bit for bit (every scaling here is by a power of two)."""
+    pr = _pow2_problem(kind, dtype)
+    T, D = pr.tables.T, pr.D
+    tau = 2.0 * eps / (T * math.sqrt(D))
+    a = pr.picard(tau=eps, rule="prop2")
+    b = pr.picard(tau=tau, rule="relaxed")
+    assert (a.iters, a.trace, a.evals) == (b.iters, b.trace, b.evals)
+    assert np.array_equal(a.x, b.x)
+    # the sqrt(D) factor matters: the relaxed rule at tau = 2 eps / T (no
+    # sqrt D) is a looser test and slides further on these inputs
+    c = pr.picard(tau=2.0 * eps / T, rule="relaxed")
+    assert c.iters <= a.iters
+
+
+@pytest.mark.parametrize("name", list(PROBLEMS))
+def test_prop2_infinite_bound_is_infinite_tolerance(name):
+    """eps = inf accepts every point whose sigma^2 > 0, as tau = inf does."""
+    pr = PROBLEMS[name](dtype=np.float64)
+    a = pr.picard(p=4, tau=INF, rule="prop2")
+    b = pr.picard(p=4, tau=INF)
+    assert a.trace == b.trace and np.array_equal(a.x, b.x)
+
+
+def test_prop2_zero_bound_reproduces_sequential():
+    pr = _mlp_problem(T=20, dtype=np.float64, batch=1)
+    r = pr.picard(p=20, tau=0.0, rule="prop2")
+    assert r.iters <= 20
+    assert np.allclose(r.x, pr.sequential(), rtol=1e-12, atol=1e-12)
+
+
+def test_overflowing_error_is_reported():
+    """Huge but finite points whose squared differences overflow float32: the
+    error is non-finite, and the run stops with NumericError."""
+    pr = _conv_problem(T=10, dtype=np.float32)
+    w = dict(pr.weights)
+    w["b4"] = np.full_like(w["b4"], 1e20)
+    wl = pr.w
+    pr2 = Problem(wl, w, np.float32)
+    with pytest.raises(samplers.NumericError, match="error"):
+        pr2.picard()
