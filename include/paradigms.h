@@ -96,17 +96,27 @@ const char* pd_version(void);
  * Tables are computed in double precision and rounded once to float.
  * tol_index_offset selects which variance the stride test of Algorithm 1
  * uses for the point x_{t+j}: 0 = sigma^2_{t+j} (default), -1 = sigma^2_{t+j-1}.
+ * stop_rule selects the stride test's error and threshold (see
+ * pd_sample_picard): PD_STOP_RELAXED, the relaxed tolerance of Sec. 3.1,
+ * (1/D) |x^{k+1} - x^k|^2 <= tau^2 sigma^2; or PD_STOP_PROP2, Prop. 2's
+ * total-variation rule |x^{k+1} - x^k|^2 <= 4 eps^2 sigma^2 / T^2, which
+ * bounds the total-variation distance of the sample from the sequential
+ * sampler's distribution by eps (given a linear convergence rate with factor
+ * at least 2).  For one point the two rules agree when tau = 2 eps / (T sqrt D).
  */
 #define PD_DDPM 0
 #define PD_DDIM 1
 #define PD_DDIM_HEUN 2
 #define PD_DDIM_DPM2M 3
+#define PD_STOP_RELAXED 0
+#define PD_STOP_PROP2 1
 
 typedef struct pd_schedule_desc {
     int32_t kind;              /* PD_DDPM, PD_DDIM, PD_DDIM_HEUN or PD_DDIM_DPM2M  */
     int32_t T_train;           /* length of the training chain, >= 2              */
     int32_t T;                 /* sampling steps; == T_train for DDPM             */
     int32_t tol_index_offset;  /* 0 or -1                                          */
+    int32_t stop_rule;         /* PD_STOP_RELAXED (default) or PD_STOP_PROP2       */
     double beta_start;         /* 0 < beta_start <= beta_end < 1                   */
     double beta_end;
     double eta;                /* DDIM only, in [0, 1]; 0 for HEUN and DPM2M       */
@@ -192,9 +202,13 @@ pd_status pd_denoiser_create(const pd_model_desc* desc, const int64_t* sample_sh
                              const pd_schedule* train, pd_denoiser** out);
 void pd_denoiser_destroy(pd_denoiser* d);
 
-/* eps[m] = eps(x[m], model_t[m]) for m in [0, M).  x, eps: device float
- * [M][D]; model_t: device int32 [M], each in [0, T_train).  Enqueued on
- * `stream`; x and eps must not overlap.  M = 0 is a no-op. */
+/* eps[m] = eps(x[m], model_t[m]) for m in [0, M) (the network evaluations of
+ * Algorithm 1's drift step).  x, eps: device float [M][D]; model_t: device
+ * int32 [M], each in [0, T_train).  Enqueued on `stream` of the denoiser's
+ * device; x and eps must not overlap.  M = 0 is a no-op.  Allocates nothing:
+ * the MLP's hidden activations go through scratch the denoiser allocated at
+ * creation (in chunks of 1024 rows), and calls on several threads or streams
+ * are ordered on the device so that they never share it at once. */
 pd_status pd_denoiser_forward(const pd_denoiser* d, const float* x, const int32_t* model_t,
                               int64_t M, float* eps, void* stream);
 
@@ -254,8 +268,13 @@ pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoiser* d, uint6
 /* ParaDiGMS sampling, Algorithm 1, with window p (clamped to T, at most 128)
  * and tolerance tau (>= 0; +inf accepts every point whose sigma^2 > 0).  The
  * stride test fails offset j in [1, p) when, for any sample b of the batch,
- * not ((1/D) |x^{k+1}_{t+j} - x^k_{t+j}|^2 <= tau^2 sigma^2), with the product
- * taken as 0 when sigma^2 = 0.  Returns PD_ERR_NUMERIC (with x_out
+ * not (e_b <= c sigma^2), with the product taken as 0 when sigma^2 = 0 and
+ *   PD_STOP_RELAXED: e_b = (1/D) |x^{k+1}_{t+j} - x^k_{t+j}|^2, c = tau^2
+ *                    (float product);
+ *   PD_STOP_PROP2:   e_b = |x^{k+1}_{t+j} - x^k_{t+j}|^2, c = 4 tau^2 / T^2
+ *                    formed in double from the float tau and rounded once
+ *                    to float; tau is Prop. 2's total-variation bound eps.
+ * The sums of squares are float32.  Returns PD_ERR_NUMERIC (with x_out
  * unspecified) if a point or error becomes non-finite.  x_out: device float
  * [batch][D], also written between batches of iterations (only its content
  * on return is the sample); ws as for pd_sample_sequential (its p must be

@@ -21,7 +21,8 @@ __all__ = [
     "PdError", "load", "lib_path", "Schedule", "Denoiser", "Workspace", "SampleStats",
     "pd_init_schedule", "pd_denoiser_create", "pd_denoiser_forward", "pd_normals",
     "pd_workspace_create", "pd_sample_sequential", "pd_sample_picard",
-    "PD_DDPM", "PD_DDIM", "PD_DDIM_HEUN", "PD_DDIM_DPM2M", "PD_MODEL_GMM2D", "PD_MODEL_MLP", "PD_MODEL_CONV1X1",
+    "PD_DDPM", "PD_DDIM", "PD_DDIM_HEUN", "PD_DDIM_DPM2M", "PD_STOP_RELAXED", "PD_STOP_PROP2",
+    "PD_MODEL_GMM2D", "PD_MODEL_MLP", "PD_MODEL_CONV1X1",
     "PD_F32", "PD_BF16", "EXPORTED_SYMBOLS",
 ]
 
@@ -29,6 +30,8 @@ PD_OK, PD_ERR_INVALID_ARG, PD_ERR_OOM, PD_ERR_DEVICE, PD_ERR_NUMERIC, PD_ERR_UNS
 STATUS_NAMES = {0: "PD_OK", 1: "PD_ERR_INVALID_ARG", 2: "PD_ERR_OOM", 3: "PD_ERR_DEVICE",
                 4: "PD_ERR_NUMERIC", 5: "PD_ERR_UNSUPPORTED"}
 PD_DDPM, PD_DDIM, PD_DDIM_HEUN, PD_DDIM_DPM2M = 0, 1, 2, 3
+PD_STOP_RELAXED, PD_STOP_PROP2 = 0, 1
+STOP_RULES = {"relaxed": PD_STOP_RELAXED, "prop2": PD_STOP_PROP2}
 PD_MODEL_GMM2D, PD_MODEL_MLP, PD_MODEL_CONV1X1 = 0, 1, 2
 PD_F32, PD_BF16 = 0, 1
 
@@ -48,7 +51,8 @@ class PdError(RuntimeError):
 
 class _ScheduleDesc(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("T_train", ctypes.c_int32), ("T", ctypes.c_int32),
-                ("tol_index_offset", ctypes.c_int32), ("beta_start", ctypes.c_double),
+                ("tol_index_offset", ctypes.c_int32), ("stop_rule", ctypes.c_int32),
+                ("beta_start", ctypes.c_double),
                 ("beta_end", ctypes.c_double), ("eta", ctypes.c_double)]
 
 
@@ -205,8 +209,8 @@ class SampleStats:
 # ------------------------------------------------------------------ entry points
 def pd_init_schedule(kind: int, T_train: int, T: int, beta_start: float = 1e-4,
                      beta_end: float = 0.02, eta: float = 0.0,
-                     tol_index_offset: int = 0) -> Schedule:
-    d = _ScheduleDesc(kind, T_train, T, tol_index_offset, beta_start, beta_end, eta)
+                     tol_index_offset: int = 0, stop_rule: int = PD_STOP_RELAXED) -> Schedule:
+    d = _ScheduleDesc(kind, T_train, T, tol_index_offset, stop_rule, beta_start, beta_end, eta)
     h = ctypes.c_void_p()
     _check(load().pd_init_schedule(ctypes.byref(d), ctypes.byref(h)))
     return Schedule(h, T, T_train)
@@ -309,9 +313,12 @@ def pd_sample_picard(sched: Schedule, den: Denoiser, p: int, tau: float, noise_s
 
 
 # ------------------------------------------------------------ workload helpers
-def from_workload(w, weights: Dict[str, np.ndarray], tol_index_offset: int = 0):
+def from_workload(w, weights: Dict[str, np.ndarray], tol_index_offset: int = 0,
+                  rule: str = "relaxed"):
     """(schedule, denoiser) handles for a ``workloads.Workload``.  The schedule
-    carries the training chain (T_train, abar) that the denoiser needs."""
+    carries the training chain (T_train, abar) that the denoiser needs, and
+    the stride test's reading (``tol_index_offset``) and rule ("relaxed" or
+    "prop2")."""
     s = w.schedule
     if s.kind == "ddpm":
         kind = PD_DDPM
@@ -319,7 +326,7 @@ def from_workload(w, weights: Dict[str, np.ndarray], tol_index_offset: int = 0):
         kind = {"euler": PD_DDIM, "heun": PD_DDIM_HEUN,
                 "dpm2m": PD_DDIM_DPM2M}[getattr(s, "solver", "euler")]
     sched = pd_init_schedule(kind, s.T_train, s.T, s.beta_start, s.beta_end, s.eta,
-                             tol_index_offset)
+                             tol_index_offset, STOP_RULES[rule])
     m = w.model
     mk = {"gmm2d": PD_MODEL_GMM2D, "mlp": PD_MODEL_MLP, "conv1x1": PD_MODEL_CONV1X1}[m.kind]
     den = pd_denoiser_create(mk, m.sample_shape, weights, sched, width=m.width,

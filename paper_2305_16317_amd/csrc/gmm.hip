@@ -185,7 +185,7 @@ __global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noi
             const float* xo = ring + ((m <= f ? m : f) % P1) * BD + 2 * b;
             const float* xv = xn + (o - 1) * BD + 2 * b;
             const float d0 = __fsub_rn(xv[0], xo[0]), d1 = __fsub_rn(xv[1], xo[1]);
-            const float err = __fadd_rn(d0 * d0, d1 * d1) / 2.0f;
+            const float err = __fadd_rn(d0 * d0, d1 * d1) / a.err_div;
             const float s2 = tb.V[m + a.tol_offset];
             const float tol = (s2 == 0.f) ? 0.f : a.tau2 * s2;
             if (!isfinite(err)) atomicOr(&s_bad, 1);

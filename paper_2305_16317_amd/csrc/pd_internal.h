@@ -92,7 +92,8 @@ struct GmmLoopArgs {
     LoopState* st_host;     // its host copy (mapped pinned memory), or nullptr
     int32_t* trace;         // [T] stride of every iteration (mapped pinned memory)
     int32_t T, p, batch, tol_offset;
-    float tau2;
+    float tau2;             // threshold factor c: offset o fails when !(err <= c sigma^2)
+    float err_div;          // err = (summed squared differences) / err_div
 };
 // LDS bytes the Picard loop needs at least (noise read per window from HBM);
 // the launcher stages all the noise in LDS when that fits in `max_lds`.
@@ -162,7 +163,8 @@ struct FinalizeArgs {
     int64_t D;
     int32_t T;
     const float* tol_var;
-    float tau2;
+    float tau2;                 // threshold factor c: offset o fails when !(err <= c sigma^2)
+    float err_div;              // err = (summed squared differences) / err_div: D or 1
     int32_t tol_offset;
     const int32_t* model_t;
     int32_t* trace;             // [T] strides (mapped pinned memory)

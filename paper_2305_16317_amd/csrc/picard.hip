@@ -212,7 +212,6 @@ __device__ void finalize_body(const FinalizeArgs& a, int nblk, const LoopState& 
     constexpr int kTeam = 16;
     const int team = threadIdx.x / kTeam, tl = threadIdx.x % kTeam;
     const int nteams = blockDim.x / kTeam;
-    const float Df = (float)a.D;
     for (int pair = team; pair < pe * a.batch; pair += nteams) {
         const int o = pair / a.batch, b = pair % a.batch;
         const float tol = o >= 1 ? offset_tol(a, t, o) : 0.f;    // in flight with the sums
@@ -233,7 +232,7 @@ __device__ void finalize_body(const FinalizeArgs& a, int nblk, const LoopState& 
             if (o == 0) {
                 bad = s != 0.f;
             } else {
-                const float err = s / Df;
+                const float err = s / a.err_div;
                 bad = !isfinite(err);
                 fails = !(err <= tol);
             }
@@ -466,7 +465,7 @@ __global__ __launch_bounds__(NW * 64) void k_picard_scan(
         if (o == 0) {
             bad = s_err[0] != 0.f;
         } else if (o < pe) {
-            const float err = s_err[o] / (float)D;
+            const float err = s_err[o] / fin.err_div;
             bad = !isfinite(err);
             fails = !(err <= ftol);
         }

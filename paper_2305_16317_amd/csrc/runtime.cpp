@@ -5,6 +5,7 @@
 #include <cstring>
 #include <exception>
 #include <memory>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -275,6 +276,8 @@ extern "C" pd_status pd_init_schedule(const pd_schedule_desc* desc, pd_schedule*
                 "DPM-Solver integrates the eta = 0 (ODE) chain only");
         require(d.tol_index_offset == 0 || d.tol_index_offset == -1,
                 "tol_index_offset must be 0 or -1");
+        require(d.stop_rule == PD_STOP_RELAXED || d.stop_rule == PD_STOP_PROP2,
+                "stop_rule must be PD_STOP_RELAXED or PD_STOP_PROP2");
         auto s = std::make_unique<pd_schedule>();
         s->desc = d;
         if (d.kind == PD_DDPM) s->desc.eta = 1.0;
@@ -312,6 +315,11 @@ extern "C" const char* pd_last_error(void) { return g_last_error.c_str(); }
 extern "C" const char* pd_version(void) { return "paradigms-gfx950 0.1"; }
 
 // ============================================================== denoiser
+// pd_denoiser_forward runs the MLP's hidden layers through a scratch buffer
+// the denoiser allocates once, at creation, for this many rows; larger calls
+// are processed in chunks of it.
+static constexpr int64_t kForwardRows = 1024;
+
 struct pd_denoiser {
     pd_model_desc desc{};
     std::vector<int64_t> shape;
@@ -323,6 +331,16 @@ struct pd_denoiser {
     DevBuf W[4], bias[4], shift1;
     // conv1x1
     DevBuf frags, shift_u, shift_c;
+    // pd_denoiser_forward's MLP scratch (kForwardRows rows).  Calls may come
+    // from several threads and streams: under fwd_mu, each call's kernels wait
+    // for fwd_done, the end of the previous call's use, and record it anew.
+    DevBuf fwd_scratch;
+    hipEvent_t fwd_done = nullptr;
+    mutable std::mutex fwd_mu;
+
+    ~pd_denoiser() {
+        if (fwd_done) (void)hipEventDestroy(fwd_done);
+    }
 
     bool guided() const { return desc.cond_dim > 0; }
 
@@ -445,6 +463,8 @@ static void create_denoiser(const pd_model_desc& m, const int64_t* shape, int32_
         d.W[2].upload(W3, (size_t)Wd * Wd);
         d.W[3].upload(W4, (size_t)Din * Wd);
         d.shift1.upload(sh.data(), sh.size());
+        d.fwd_scratch.alloc(d.scratch_floats(kForwardRows) * sizeof(float));
+        PD_HIP(hipEventCreateWithFlags(&d.fwd_done, hipEventDisableTiming));
         return;
     }
     std::vector<uint8_t> packed;
@@ -493,18 +513,26 @@ extern "C" pd_status pd_denoiser_forward(const pd_denoiser* d, const float* x,
         require(M >= 0 && M <= (int64_t)1 << 30, "M out of range");
         if (M == 0) return;
         require(x && model_t && eps, "NULL device pointer");
+        int dev = 0;
+        PD_HIP(hipGetDevice(&dev));
+        require(dev == d->device, "the denoiser lives on another device");
         const hipStream_t s = static_cast<hipStream_t>(stream);
-        const RowSrc src{x, nullptr, d->D, 1, (int32_t)M, model_t, nullptr};
-        const size_t sc = d->scratch_floats(M);
-        float* scratch = nullptr;
-        if (sc) PD_HIP(hipMallocAsync(reinterpret_cast<void**>(&scratch), sc * sizeof(float), s));
-        try {
-            d->forward(src, eps, scratch, s);
-        } catch (...) {
-            if (scratch) (void)hipFreeAsync(scratch, s);
-            throw;
+        if (!d->scratch_floats(1)) {          // no scratch: one enqueue of the whole batch
+            const RowSrc src{x, nullptr, d->D, 1, (int32_t)M, model_t, nullptr};
+            d->forward(src, eps, nullptr, s);
+            return;
         }
-        if (scratch) PD_HIP(hipFreeAsync(scratch, s));
+        // MLP: chunks of kForwardRows rows through the denoiser's scratch, after
+        // every earlier call's kernels that used it (a wait on an event no call
+        // has recorded yet is a no-op)
+        const std::lock_guard<std::mutex> lock(d->fwd_mu);
+        PD_HIP(hipStreamWaitEvent(s, d->fwd_done, 0));
+        for (int64_t m0 = 0; m0 < M; m0 += kForwardRows) {
+            const int64_t mc = M - m0 < kForwardRows ? M - m0 : kForwardRows;
+            const RowSrc src{x + m0 * d->D, nullptr, d->D, 1, (int32_t)mc, model_t + m0, nullptr};
+            d->forward(src, eps + m0 * d->D, d->fwd_scratch.as<float>(), s);
+        }
+        PD_HIP(hipEventRecord(d->fwd_done, s));
     });
 }
 
@@ -684,8 +712,23 @@ static bool use_fused_gmm_loop(const pd_schedule& s, const pd_denoiser& d, int T
            gmm_loop_lds_bytes(T, d.desc.n_components, p, batch) <= kFusedLoopLds;
 }
 
+// The stride test's threshold factor c (threshold c sigma^2) and the divisor
+// of the summed squared differences (the error is sum / div): the relaxed
+// rule of Sec. 3.1 compares the per-dimension mean with tau^2 sigma^2,
+// Prop. 2 the squared norm with 4 eps^2 sigma^2 / T^2 (eps = tau).
+struct StopTest {
+    float factor, err_div;
+};
+static StopTest stop_test(const pd_schedule& s, float tau, int64_t D) {
+    if (s.desc.stop_rule == PD_STOP_PROP2) {
+        const double e = (double)tau, T = (double)s.T;
+        return StopTest{(float)(4.0 * e * e / (T * T)), 1.0f};
+    }
+    return StopTest{tau * tau, (float)D};
+}
+
 static GmmLoopArgs gmm_loop_args(const pd_schedule& s, const pd_denoiser& d, pd_workspace& w, int p,
-                                 int batch, float tau2, float* x_out) {
+                                 int batch, StopTest stop, float* x_out) {
     GmmLoopArgs a;
     a.g = d.gmm();
     a.A = w.A.as<float>();
@@ -702,7 +745,8 @@ static GmmLoopArgs gmm_loop_args(const pd_schedule& s, const pd_denoiser& d, pd_
     a.p = p;
     a.batch = batch;
     a.tol_offset = s.desc.tol_index_offset;
-    a.tau2 = tau2;
+    a.tau2 = stop.factor;
+    a.err_div = stop.err_div;
     return a;
 }
 
@@ -725,7 +769,7 @@ extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoise
         draw_noise(w, noise_seed, st);
         if (use_fused_gmm_loop(*s, *d, s->T, 1, batch)) {
             tm.mark(-1);
-            launch_gmm_sequential_loop(gmm_loop_args(*s, *d, w, 1, batch, 0.f, x_out), st);
+            launch_gmm_sequential_loop(gmm_loop_args(*s, *d, w, 1, batch, StopTest{0.f, 2.f}, x_out), st);
             tm.mark(CAT_UPDATE);
             PD_HIP(hipStreamSynchronize(st));
             tm.collect();
@@ -786,7 +830,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         pd_workspace& w = *use_workspace(ws, own, s, d, pc, batch);
         const StreamDrain drain{st};
         const int64_t BD = (int64_t)batch * d->D;
-        const float tau2 = tau * tau;
+        const StopTest stop = stop_test(*s, tau, d->D);
         LoopState* dst = w.state.as<LoopState>();
 
         KernelTimer tm;
@@ -795,7 +839,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         draw_noise(w, noise_seed, st);
         if (use_fused_gmm_loop(*s, *d, T, pc, batch)) {
             tm.mark(-1);
-            launch_gmm_picard_loop(gmm_loop_args(*s, *d, w, pc, batch, tau2, x_out), kFusedLoopLds,
+            launch_gmm_picard_loop(gmm_loop_args(*s, *d, w, pc, batch, stop, x_out), kFusedLoopLds,
                                    st);
             tm.mark(CAT_UPDATE);
             PD_HIP(hipStreamSynchronize(st));     // the kernel wrote the state's host copy
@@ -812,7 +856,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         const int hist = s->dpm ? 1 : 0;     // the multistep drift's row x_{t-1}
         const int slots = pc + 1 + hist;
         const FinalizeArgs fin{dst, w.h_state_dev, w.partials.as<float>(), pc, batch, d->D, T,
-                               w.tolv.as<float>(), tau2, s->desc.tol_index_offset,
+                               w.tolv.as<float>(), stop.factor, stop.err_div, s->desc.tol_index_offset,
                                w.model_t.as<int32_t>(), w.h_trace_dev, w.slot.as<int32_t>(),
                                w.nrow.as<int32_t>(), mtn, nrow2, slots, hist};
         const float* xT = w.ring.as<float>() + (int64_t)(T % slots) * BD;

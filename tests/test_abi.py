@@ -63,6 +63,8 @@ def _status(fn, *args):
     (dict(kind=pd.PD_DDIM_HEUN, T=300), "T_train % T"),
     (dict(kind=pd.PD_DDIM_DPM2M, T=200, eta=0.3), "DPM-Solver"),
     (dict(kind=4, T=200), "kind"),
+    (dict(stop_rule=2), "stop_rule"),
+    (dict(stop_rule=-1), "stop_rule"),
 ])
 def test_schedule_validation(kw, msg):
     args = dict(kind=pd.PD_DDPM, T_train=1000, T=1000, beta_start=1e-4, beta_end=0.02,
@@ -147,7 +149,7 @@ C_PROGRAM = r"""
 #include "paradigms.h"
 
 int main(void) {
-    pd_schedule_desc d = {PD_DDPM, 1000, 1000, 0, 1e-4, 0.02, 0.0};
+    pd_schedule_desc d = {PD_DDPM, 1000, 1000, 0, PD_STOP_RELAXED, 1e-4, 0.02, 0.0};
     pd_schedule* s = NULL;
     if (pd_init_schedule(&d, &s) != PD_OK) { printf("init: %s\n", pd_last_error()); return 1; }
     int32_t T = 0;

@@ -1,7 +1,9 @@
 """Device path vs oracle, element by element on the same seeded inputs.
 
 Bars: bit-exact for integers (iteration counts, strides, evaluation counts);
-relative L2 <= 1e-5 for float32 results; the generated normals equal the
+relative L2 <= 1e-5 for float32 results, over every element of the sample
+(full-size samples against the oracle's stored float32 arrays); the
+generated normals equal the
 oracle's up to a handful of one-ulp roundings (Box-Muller runs in double on
 both sides with different libm implementations, then rounds once to float).
 """
@@ -200,6 +202,29 @@ def test_conv1x1_bf16_forward(shape, width, M, cond):
     assert _rel(got, ref32) <= 2e-2, _rel(got, ref32)
 
 
+def test_mlp_forward_chunks_and_concurrent_streams():
+    """pd_denoiser_forward allocates nothing: the MLP runs through the
+    denoiser's own scratch, 1024 rows at a time.  2500 rows span three chunks;
+    two calls enqueued on two streams share the scratch in turn and both match
+    the oracle."""
+    wl = _wl("mlp", (4, 3), 32)
+    w = W.make_weights(wl.model)
+    sched, den = pd.from_workload(wl, w)
+    rng = np.random.default_rng(3)
+    xs = [rng.standard_normal((M, 12)).astype(np.float32) for M in (2500, 1100)]
+    ns = [rng.integers(0, 100, x.shape[0]).astype(np.int32) for x in xs]
+    outs = [torch.empty((x.shape[0], 12), device="cuda") for x in xs]
+    xd = [_dev(x) for x in xs]
+    nd = [_dev(n, torch.int32) for n in ns]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for x, n, o, st in zip(xd, nd, outs, streams):
+        pd.pd_denoiser_forward(den, x, n, o, stream=st)
+    torch.cuda.synchronize()
+    for x, n, o in zip(xs, ns, outs):
+        assert _rel(o.cpu().numpy(), _oracle_eps(wl, w, x, n)) <= REL_F32
+
+
 def test_forward_empty_batch_is_noop():
     wl = _wl("conv1x1", (4, 8, 8), 32, T=10)
     sched, den = pd.from_workload(wl, W.make_weights(wl.model))
@@ -212,8 +237,8 @@ def test_forward_empty_batch_is_noop():
 
 # ------------------------------------------------------------------ samplers
 def _run(wl, weights, sampler="picard", p=None, tau=None, workspace=None, seed=None,
-         tol_offset=0):
-    sched, den = pd.from_workload(wl, weights, tol_offset)
+         tol_offset=0, rule="relaxed"):
+    sched, den = pd.from_workload(wl, weights, tol_offset, rule)
     x = torch.empty(wl.batch * wl.model.D, device="cuda")
     seed = wl.noise_seed if seed is None else seed
     if sampler == "picard":
@@ -261,6 +286,19 @@ SMALL = {
     "conv_cfg_f32": lambda: W.Workload("cfg", W.ScheduleSpec("ddpm", 50, 50),
                                        W.ModelSpec("conv1x1", (4, 8, 8), width=64, cond_dim=24,
                                                    guidance=7.5), p=16, tau=0.1),
+    # the scan variants of the full-size latent workloads at small size: windows
+    # of 33-64 points (eight waves of up to eight rows), four columns per lane,
+    # several column blocks per sample (the finalize step as its own launch);
+    # with noise (DDPM, as the 4x96x96 T = 1000 workload) and without (DDIM,
+    # as the four-sample T = 200 workload), the latter with a ragged last block
+    "conv_ddpm_p64_blocks": lambda: W.small_variant("latent_ddpm1000_p64", T=150, p=64,
+                                                    shape=(4, 16, 16), width=64),
+    "conv_ddpm_p48_ragged": lambda: W.small_variant("latent_ddpm1000_p64", T=100, p=48,
+                                                    shape=(4, 10, 10), width=32),
+    "conv_ddim_p64_b3": lambda: W.small_variant("latent_ddim200_b4", T=80, p=64,
+                                                shape=(4, 10, 10), width=32, batch=3),
+    "conv_ddim_p40_w320": lambda: W.small_variant("latent_ddim200_b4", T=60, p=40,
+                                                  shape=(4, 8, 12), width=320, batch=2),
 }
 
 BF16 = {
@@ -362,6 +400,37 @@ def test_tolerance_offset_matches_oracle(name):
     assert _rel(got, ref.x) <= REL_F32, _rel(got, ref.x)
 
 
+PROP2 = [("gmm_p7_b3", 1.0), ("gmm_p7_b3", 40.0), ("gmm_b48_general", 5.0),
+         ("mlp_small", 2.0), ("mlp_small", 50.0), ("mlp_b8", 10.0), ("conv_ddpm", 20.0),
+         ("conv_ddpm", 300.0), ("conv_ddim_b3", 50.0), ("conv_ddpm_p64_blocks", 200.0),
+         ("conv_ddim_p64_b3", 100.0)]
+
+
+@pytest.mark.parametrize("name,eps", PROP2)
+def test_prop2_rule_matches_oracle(name, eps):
+    """Prop. 2's stopping rule |x^{k+1} - x^k|^2 <= 4 eps^2 sigma^2 / T^2: the
+    strides bit for bit and the sample within 1e-5 of the oracle's."""
+    wl = SMALL[name]()
+    w = W.make_weights(wl.model)
+    got, st = _run(wl, w, tau=eps, rule="prop2")
+    ref = Problem(wl, w, np.float32).picard(tau=eps, rule="prop2")
+    assert (st.iters, st.trace, st.evals_per_sample) == (ref.iters, ref.trace, ref.evals)
+    assert _rel(got, ref.x) <= REL_F32, _rel(got, ref.x)
+
+
+def test_prop2_rule_is_relaxed_rule_at_matching_tau():
+    """On the device as in the oracle: Prop. 2 at eps equals the relaxed rule
+    at tau = 2 eps / (T sqrt D) (D = 16, T = 32: exact binary fractions)."""
+    wl = W.Workload("p2", W.ScheduleSpec("ddpm", 32, 32),
+                    W.ModelSpec("mlp", (4, 4), width=32, weight_seed=9), p=8, tau=0.1,
+                    batch=2, noise_seed=4)
+    w = W.make_weights(wl.model)
+    for eps in (0.5, 4.0, 64.0):
+        a, sa = _run(wl, w, tau=eps, rule="prop2")
+        b, sb = _run(wl, w, tau=2.0 * eps / (32 * 4.0))
+        assert sa == sb and np.array_equal(a.view(np.uint32), b.view(np.uint32)), eps
+
+
 def test_infinite_tolerance_single_sweeps():
     wl = SMALL["conv_ddpm"]()
     w = W.make_weights(wl.model)
@@ -369,6 +438,21 @@ def test_infinite_tolerance_single_sweeps():
     ref = Problem(wl, w, np.float32).picard(tau=float("inf"))
     assert st.trace == ref.trace
     assert _rel(got, ref.x) <= REL_F32
+
+
+def test_overflowing_error_reports_numeric_error():
+    """Huge but finite points (the last bias 1e20): the squared differences
+    overflow float32, the error is non-finite, and the sampler returns
+    PD_ERR_NUMERIC, as the oracle raises NumericError on the same input."""
+    from oracle.samplers import NumericError
+    wl = SMALL["conv_ddpm"]()
+    w = dict(W.make_weights(wl.model))
+    w["b4"] = np.full_like(w["b4"], 1e20)
+    with pytest.raises(NumericError):
+        Problem(wl, w, np.float32).picard()
+    with pytest.raises(pd.PdError) as e:
+        _run(wl, w)
+    assert e.value.code == pd.PD_ERR_NUMERIC
 
 
 def test_non_finite_reports_numeric_error():
@@ -394,30 +478,48 @@ def test_workspace_mismatch_rejected():
 
 # ------------------------------------------------------------ full-size workloads
 def _golden(name):
+    """The oracle's stored result of a full-size workload: the JSON summary
+    (K, strides, evaluations, squared norm) and the complete float32 samples."""
     path = os.path.join(HERE, "golden", f"{name}.json")
-    if not os.path.exists(path):
-        pytest.fail(f"{path} missing: run tests/golden/make_golden.py {name}")
-    return json.load(open(path))
+    arr = os.path.join(HERE, "golden", f"{name}.npz")
+    if not (os.path.exists(path) and os.path.exists(arr)):
+        pytest.fail(f"{path} or its .npz missing: run tests/golden/make_golden.py {name}")
+    g = json.load(open(path))
+    with np.load(arr) as z:
+        for key in z.files:
+            g[key]["x"] = z[key]
+    return g
 
 
-def _check_summary(got, g, tol):
-    flat = got.reshape(-1).astype(np.float32)
-    vals = flat[np.asarray(g["idx"])]
-    assert _rel(vals, g["values"]) <= tol, _rel(vals, g["values"])
-    n2 = float(np.sum(flat.astype(np.float64) ** 2))
-    assert abs(math.sqrt(n2) - math.sqrt(g["norm2"])) <= tol * math.sqrt(g["norm2"])
+def _check_full(got, g, tol):
+    """Every element: relative L2 over the whole sample within ``tol``; the
+    message names the worst element."""
+    ref = np.asarray(g["x"], np.float32)
+    got = np.asarray(got, np.float32).reshape(ref.shape)
+    assert np.isfinite(got).all()
+    rel = _rel(got, ref)
+    diff = np.abs(got.astype(np.float64) - ref.astype(np.float64))
+    worst = np.unravel_index(int(np.argmax(diff)), ref.shape)
+    msg = (f"rel L2 {rel:.3e} over {ref.size} values; worst element {worst}: "
+           f"{got[worst]!r} vs {ref[worst]!r}")
+    assert rel <= tol, msg
+    n2 = float(np.sum(got.astype(np.float64) ** 2))
+    assert abs(math.sqrt(n2) - math.sqrt(g["norm2"])) <= tol * math.sqrt(g["norm2"]), msg
 
 
 @pytest.mark.parametrize("name", ["gmm2d_ddpm100", "policy_mlp_ddpm100", "latent_ddpm1000_p64",
                                   "latent_ddim200_b4", "policy_mlp_heun20", "latent_heun100_p32",
                                   "policy_mlp_dpm15", "latent_dpm200_p64"])
 def test_full_size_picard_matches_oracle(name):
+    """Every value of the sample (147,456 for the four 4x96x96 samples of the
+    DDIM workload) within relative L2 1e-5 of the oracle's float32 sample;
+    K, strides and evaluations bit for bit."""
     g = _golden(name)
     wl = W.WORKLOADS[name]
     got, st = _run(wl, W.make_weights(wl.model))
     gp = g["picard"]
     assert (st.iters, st.trace, st.evals_per_sample) == (gp["iters"], gp["trace"], gp["evals"])
-    _check_summary(got, gp, REL_F32)
+    _check_full(got, gp, REL_F32)
 
 
 @pytest.mark.parametrize("name", ["gmm2d_ddpm100", "policy_mlp_ddpm100", "latent_ddpm1000_p64",
@@ -426,7 +528,19 @@ def test_full_size_sequential_matches_oracle(name):
     g = _golden(name)
     wl = W.WORKLOADS[name]
     got, st = _run(wl, W.make_weights(wl.model), "sequential")
-    _check_summary(got, g["sequential"], REL_F32)
+    _check_full(got, g["sequential"], REL_F32)
+
+
+@pytest.mark.parametrize("name,eps", [("gmm2d_ddpm100", 1.0), ("policy_mlp_ddpm100", 1.0),
+                                      ("policy_mlp_ddpm100", 10.0)])
+def test_full_size_prop2_matches_oracle(name, eps):
+    """Prop. 2's stopping rule at full size: strides bit for bit, every value
+    of the sample within 1e-5."""
+    g = _golden(name)[f"picard_prop2_eps{eps:g}"]
+    wl = W.WORKLOADS[name]
+    got, st = _run(wl, W.make_weights(wl.model), tau=eps, rule="prop2")
+    assert (st.iters, st.trace, st.evals_per_sample) == (g["iters"], g["trace"], g["evals"])
+    _check_full(got, g, REL_F32)
 
 
 @pytest.mark.parametrize("name", ["latent_ddpm1000_p64", "policy_mlp_ddpm100"])
@@ -436,7 +550,7 @@ def test_full_size_tolerance_offset_matches_oracle(name):
     wl = W.WORKLOADS[name]
     got, st = _run(wl, W.make_weights(wl.model), tol_offset=-1)
     assert (st.iters, st.trace, st.evals_per_sample) == (g["iters"], g["trace"], g["evals"])
-    _check_summary(got, g, REL_F32)
+    _check_full(got, g, REL_F32)
 
 
 def test_full_size_headline_in_bench_configuration():
@@ -457,7 +571,7 @@ def test_full_size_headline_in_bench_configuration():
                                  time_kernels=timed)
         torch.cuda.synchronize()
         assert (st.iters, st.trace, st.evals_per_sample) == (g["iters"], g["trace"], g["evals"])
-        _check_summary(x.cpu().numpy().reshape(wl.batch, -1), g, REL_F32)
+        _check_full(x.cpu().numpy().reshape(wl.batch, -1), g, REL_F32)
 
 
 def test_full_size_bf16_picard_matches_oracle():
@@ -472,7 +586,7 @@ def test_full_size_bf16_picard_matches_oracle():
     gp = g["picard"]
     assert abs(st.iters - gp["iters"]) <= max(1, gp["iters"] // 10), (st.iters, gp["iters"])
     assert st.network_rows == st.evals_per_sample * 2
-    _check_summary(got, gp, 2e-2)
+    _check_full(got, gp, 2e-2)
 
 
 # ------------------------------------------------------- Heun drift (DDIM ODE)
