@@ -212,6 +212,22 @@ void pd_denoiser_destroy(pd_denoiser* d);
 pd_status pd_denoiser_forward(const pd_denoiser* d, const float* x, const int32_t* model_t,
                               int64_t M, float* eps, void* stream);
 
+/* The same network evaluations as pd_denoiser_forward, for callers that
+ * cannot allocate or synchronise anything (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): no allocation, no
+ * event or lock; the launches on `stream` are all it does.  The MLP's hidden
+ * activations (2 * width floats per row) go to a static device array of
+ * 2^20 floats (4 MiB) that each GPU holds until the process ends, so for the
+ * MLP M * 2 * width <= 2^20 (M <= 512 at width 1024); larger M returns
+ * PD_ERR_INVALID_ARG.  The mixture and conv1x1 models use no scratch and take
+ * any M.  Every call on one GPU shares that array: calls whose work overlaps
+ * on the device (other streams, or host threads) race and give undefined
+ * results; calls ordered on one stream are safe.  Each layer overwrites its
+ * part before reading it, so nothing needs clearing between calls. */
+pd_status pd_denoiser_forward_static(const pd_denoiser* d, const float* x,
+                                     const int32_t* model_t, int64_t M, float* eps,
+                                     void* stream);
+
 /* ------------------------------------------------------------------ noise
  * The up-front draws of Algorithm 1 (prior point and every step's noise).
  * Philox4x32-10 (Salmon et al., SC'11): key = (seed mod 2^32, seed div 2^32),

@@ -19,7 +19,8 @@ import torch  # noqa: F401  (loads the HIP runtime first)
 
 __all__ = [
     "PdError", "load", "lib_path", "Schedule", "Denoiser", "Workspace", "SampleStats",
-    "pd_init_schedule", "pd_denoiser_create", "pd_denoiser_forward", "pd_normals",
+    "pd_init_schedule", "pd_denoiser_create", "pd_denoiser_forward",
+    "pd_denoiser_forward_static", "pd_normals",
     "pd_workspace_create", "pd_sample_sequential", "pd_sample_picard",
     "PD_DDPM", "PD_DDIM", "PD_DDIM_HEUN", "PD_DDIM_DPM2M", "PD_STOP_RELAXED", "PD_STOP_PROP2",
     "PD_MODEL_GMM2D", "PD_MODEL_MLP", "PD_MODEL_CONV1X1",
@@ -37,7 +38,8 @@ PD_F32, PD_BF16 = 0, 1
 
 EXPORTED_SYMBOLS = [
     "pd_last_error", "pd_version", "pd_init_schedule", "pd_destroy_schedule",
-    "pd_schedule_tables", "pd_schedule_multistep_tables", "pd_denoiser_create", "pd_denoiser_destroy", "pd_denoiser_forward",
+    "pd_schedule_tables", "pd_schedule_multistep_tables", "pd_denoiser_create", "pd_denoiser_destroy",
+    "pd_denoiser_forward", "pd_denoiser_forward_static",
     "pd_normals", "pd_workspace_create", "pd_workspace_destroy", "pd_sample_sequential",
     "pd_sample_picard",
 ]
@@ -101,6 +103,7 @@ def load() -> ctypes.CDLL:
         "pd_denoiser_create": ([P(_ModelDesc), P(i64), i32, P(P(f32)), i32, vp, P(vp)], i32),
         "pd_denoiser_destroy": ([vp], None),
         "pd_denoiser_forward": ([vp, vp, vp, i64, vp, vp], i32),
+        "pd_denoiser_forward_static": ([vp, vp, vp, i64, vp, vp], i32),
         "pd_normals": ([u64, ctypes.c_uint32, i64, vp, vp], i32),
         "pd_workspace_create": ([vp, vp, i32, i32, P(vp)], i32),
         "pd_workspace_destroy": ([vp], None),
@@ -249,6 +252,18 @@ def pd_denoiser_forward(den: Denoiser, x: torch.Tensor, model_t: torch.Tensor,
             raise ValueError("x/eps must be contiguous float32 and model_t int32, on the GPU")
     _check(load().pd_denoiser_forward(den.handle, _ptr(x), _ptr(model_t), M, _ptr(eps),
                                       _stream(stream)))
+
+
+def pd_denoiser_forward_static(den: Denoiser, x: torch.Tensor, model_t: torch.Tensor,
+                               eps: torch.Tensor, stream=None) -> None:
+    """pd_denoiser_forward without any allocation or synchronisation (the
+    MLP's scratch is a static per-GPU array: M * 2 * width <= 2^20)."""
+    M = x.shape[0] if x.dim() else 0
+    for t, dt in ((x, torch.float32), (eps, torch.float32), (model_t, torch.int32)):
+        if t.dtype != dt or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError("x/eps must be contiguous float32 and model_t int32, on the GPU")
+    _check(load().pd_denoiser_forward_static(den.handle, _ptr(x), _ptr(model_t), M, _ptr(eps),
+                                             _stream(stream)))
 
 
 def pd_normals(seed: int, rng_stream: int, out: torch.Tensor, stream=None) -> None:

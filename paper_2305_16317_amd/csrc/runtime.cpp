@@ -536,6 +536,60 @@ extern "C" pd_status pd_denoiser_forward(const pd_denoiser* d, const float* x,
     });
 }
 
+// ============================================================== allocation-free forward
+// pd_denoiser_forward_static, for callers that cannot allocate device memory
+// (code under graph capture, tight serving loops): the MLP's hidden layers
+// run through this file-scope device array instead of the denoiser's scratch.
+// Each GPU holds its own copy until the process ends.  In host code the name
+// stands for a host-side symbol, not a device address: kernels get the
+// address hipGetSymbolAddress returns for the current device.
+static constexpr size_t kStaticScratchFloats = (size_t)1 << 20;   // 4 MiB
+static __device__ __align__(256) float scratch[kStaticScratchFloats];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev`, which must be current; looked
+// up on the first call on each device.
+float* static_scratch(int dev) {
+    require(dev >= 0 && dev < kMaxDevices, "device index beyond the static scratch table");
+    const std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        PD_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) fail(PD_ERR_DEVICE, "hipGetSymbolAddress returned no address for the static scratch");
+        g_scratch_ptr[dev] = static_cast<float*>(p);
+    }
+    return g_scratch_ptr[dev];
+}
+}  // namespace
+
+extern "C" pd_status pd_denoiser_forward_static(const pd_denoiser* d, const float* x,
+                                                const int32_t* model_t, int64_t M, float* eps,
+                                                void* stream) {
+    return guard([&] {
+        require(d != nullptr, "denoiser must not be NULL");
+        require(M >= 0 && M <= (int64_t)1 << 30, "M out of range");
+        const size_t need = d->scratch_floats(M);
+        if (need > kStaticScratchFloats)
+            fail(PD_ERR_INVALID_ARG,
+                 "M = " + std::to_string(M) + " needs " + std::to_string(need) +
+                     " floats of scratch; the static scratch holds " +
+                     std::to_string(kStaticScratchFloats) + " (M <= " +
+                     std::to_string(kStaticScratchFloats / d->scratch_floats(1)) +
+                     " at this width)");
+        if (M == 0) return;
+        require(x && model_t && eps, "NULL device pointer");
+        int dev = 0;
+        PD_HIP(hipGetDevice(&dev));
+        require(dev == d->device, "the denoiser lives on another device");
+        const RowSrc src{x, nullptr, d->D, 1, (int32_t)M, model_t, nullptr};
+        d->forward(src, eps, need ? static_scratch(dev) : nullptr, static_cast<hipStream_t>(stream));
+    });
+}
+
 // ============================================================== noise
 extern "C" pd_status pd_normals(uint64_t seed, uint32_t rng_stream, int64_t count, float* out,
                                 void* stream) {
