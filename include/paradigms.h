@@ -169,11 +169,11 @@ pd_status pd_schedule_multistep_tables(const pd_schedule* s, float* R, float* S)
  *                 W4 [Dout][W], b4 [Dout]  (+ Wc [W][cond_dim], c [cond_dim])
  *  with Din = Dout = D (MLP) or C (CONV1X1).
  * dtype PD_F32 computes the network to float32 accuracy: for conv1x1 the
- * matmuls of layers 2 and 3 run on the fp16 matrix cores.  Each weight is
- * split into its nearest fp16 value and a 2^11-scaled fp16 remainder, each
- * activation likewise after a power-of-two scale per tile of 32 pixels, and
- * three part products per multiply-add leave an error of about one float32
- * rounding.  A conv1x1 weight of magnitude 65504 or more makes creation fail
+ * matmuls of layers 2, 3 and 4 run on the fp16 matrix cores (layer 1 on the
+ * fp32 ones).  Each weight is split into its nearest fp16 value and a
+ * 2^11-scaled fp16 remainder, each activation likewise after a power-of-two
+ * scale per tile of 16 pixels and layer, and three part products per
+ * multiply-add leave an error of about one float32 rounding.  A conv1x1 weight of magnitude 65504 or more makes creation fail
  * with PD_ERR_UNSUPPORTED; non-finite activations propagate as in float32.
  * dtype PD_BF16 (conv1x1 only) rounds every matmul operand to bfloat16
  * (round to nearest even) and accumulates in float32.

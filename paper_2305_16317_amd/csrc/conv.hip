@@ -1,22 +1,14 @@
 // Per-pixel 4-layer stack (a stack of 1x1 convolutions) of the latent
-// denoiser, fused into one kernel: k_conv_f32x3 for the fp32 network,
+// denoiser, fused into one kernel: k_conv_f32s for the fp32 network,
 // k_conv_bf16 for the network with bf16 matmul operands.
 //
-// Both share one design.  Each wave owns a tile of 32 pixels of one sample
-// and runs all four layers on it with the activations held in registers.
-// Layers are computed transposed, out^T = W h^T: the MFMA's M dimension is the
-// output feature and its N dimension the pixel.  Every 32x32 MFMA leaves
-// D[i][j] in lane j + 32 ((i/4) % 2), register (i%4) + 4 (i/8), so the
-// accumulator of output block nb holds, in lane l and register r, feature
-// 32 nb + 8 (r/4) + 4 (l/32) + r%4 of pixel l%32.  On
-// v_mfma_f32_32x32x16_bf16 and _f16 (A[i][k] in lane i + 32 (k/8), B[k][j] in
-// lane j + 32 (k/8), element k%8 of 8 packed 16-bit values) accumulator
-// registers 8 g2 .. 8 g2 + 7 of block b, activated, converted to 16 bits and
-// packed, are exactly the B operand of k-step (b, g2) of the next layer
-// (through an LDS exchange in k_conv_f32x3): lane half h then carries
-// input features 32 b + 16 g2 + 8 (u/4) + 4 h + u%4, u = 0..7, and the host
-// packs the weights with the same permutation of the reduction index.  No
-// activation ever leaves the registers.
+// Both run all four layers of a pixel tile inside the waves that own it, with
+// the activations in registers.  Layers are computed transposed,
+// out^T = W h^T: the MFMA's M dimension is the output feature and its N
+// dimension the pixel, so a layer's accumulators, activated and converted to
+// 16 bits, are the next layer's B operands once the host packs the weights
+// with the matching permutation of the reduction index (each kernel's layout
+// comment gives it).  No activation leaves the registers.
 //
 // Weights stream through LDS in slabs shared by a block's waves, double
 // buffered: the next slab is copied global -> LDS by the gfx950 LDS-DMA path
@@ -296,200 +288,205 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 }
 
 // ---------------------------------------------------------------- fp32
-// k_conv_f32x3: the fp32 network with fp32-accurate products on
-// v_mfma_f32_32x32x16_f16 for its two W x W layers.  Every fp32 operand is
-// split exactly into a leading fp16 part and a scaled fp16 remainder:
-// w = w0 + 2^-11 w1 with w0 the nearest fp16 to w and w1 the nearest fp16 to
-// 2^11 (w - w0), so w is kept to 2^-22 |w|.  The three products
-//   w0 (2^11 x0) + w0 x1 + w1 x0  =  2^11 (w0 x0 + w0 x1' + w1' x0)
-// (x1' = 2^-11 x1, w1' = 2^-11 w1) go into one fp32 accumulator; the one left
-// out, w1' x1', is about 2^-22 |w x|.  Each fp16 product is exact in fp32 and
-// the sums are fp32.  The weights are split on the host into the two A
-// operands w0 and w1.  The activations are split in registers into the three
-// B operands 2^11 x0, x1 and x0, after a per-tile power-of-two scale s that
-// puts the tile's largest input of the layer just below 2^4: 2^11 x0 then
-// stays below 2^15, inside fp16's range, and values down to 2^-28 of the
-// largest keep full precision.  The accumulator holds 2^11 s (W h), removed
-// exactly by the next activation step.  The bound on the inputs comes from
-// the pre-activation values, since |SiLU(u)| <= |u|.  A
-// 32x32x16 fp16 MFMA does 16 times the multiply-adds of an fp32 one in the
-// same time, so the three take 3/16 of the fp32 matrix-core time.
-//
-// Persistent blocks of 8 waves on 4 tiles: the two waves of a tile share a
-// SIMD and split the output blocks of every layer between them (half 0 the
-// first ceil(NB/2), half 1 the rest), so that one wave's SiLU and splitting
-// run beside the other's MFMAs.  A tile's activations and a layer's
-// accumulators would not fit one wave's 256 registers at two waves per SIMD;
-// halved they do.  The owner of an input block activates it (fp32 SiLU) into
-// an LDS exchange buffer one slab ahead, and both waves split it from there;
-// at layer 4 each wave sums over its own input blocks and half 1 passes its
-// partial sums to half 0 through the same buffer.
-//
-// Layer 1 (K = C) runs on fp32 MFMA (v_mfma_f32_32x32x2f32: A[i][k] in lane
-// i + 32 k, B[k][j] in lane j + 32 k, the same accumulator layout); its slab
-// holds, for output block nb and lane l, the C/2 values
-// W1[32 nb + l%32][2 s + l/32].  Layers 2 and 3 run on the split products,
-// with the weights split on the host: slab b holds input block b for every
-// output block nb, fragment ((g2 NB + nb) 2 + part), one 16-B unit per lane.
-// Layer 4 (C outputs) runs as fp32 fused multiply-adds on the VALU from W4
-// in fp32 ([C][W], 5 KB at width 320): on the matrix core its C rows would be
-// padded to 32.  LDS: two 40 KB slabs, two 16 KB exchange buffers and
-// the activation vectors, 122,432 bytes at width 320.
-typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
-typedef float fl2 __attribute__((ext_vector_type(2)));
 
 // 2^k for an integer |k| <= 126, built from its exponent field
 __device__ __forceinline__ float pow2(int k) { return __builtin_bit_cast(float, (k + 127) << 23); }
 
+// ---------------------------------------------------------------- fp32, 16-pixel tiles
+// k_conv_f32s: the fp32 network with the same split products, one wave per
+// tile of 16 pixels, every output feature of every layer in that wave.  Each
+// wave is self-contained: its activations never leave its registers, so no
+// two waves exchange data and the only synchronisation is the weight stream.
+// Eight waves (two per SIMD, on different tiles) share each streamed slab.
+//
+// v_mfma_f32_16x16x32_f16 (A[i][k] in lane i + 16 (k/8), B[k][j] in lane
+// j + 16 (k/8), element k%8 of 8 packed halves; D[i][j] in lane j + 16 (i/4),
+// register i%4): the accumulator of output block o (16 features) holds, in
+// lane l and register r, feature 16 o + 4 (l/16) + r of pixel l%16.
+// Registers 0..3 of blocks 2c and 2c + 1, activated and split, are the B
+// operands of reduction chunk c (32 inputs) of the next layer: lane group
+// g = l/16 carries inputs 32 c + 16 (u/4) + 4 g + u%4, u = 0..7, and the host
+// packs the weights with the same permutation.  Layer 1 (K = C = 4) is one
+// v_mfma_f32_16x16x4f32 per output block (A[i][k], B[k][j] in lanes i + 16 k,
+// j + 16 k; the same accumulator layout); layer 4 (C outputs) is one output
+// block whose rows past C are zero, on the split products like the mid
+// layers.
+//
+// Split products: the weights w = w0 + 2^-11 w1 as before.  The activation
+// h = SiLU(u) of a layer's input enters scaled, hs = S h with S = 2^(11-e) a
+// power of two per tile and layer that puts the tile's largest input below
+// 2^15 (e from its largest |u|): x0s = fp16(hs), x1 = fp16(hs - x0s) and
+// x0 = x0s 2^-11, so that w0 x0s + w0 x1 + w1 x0 = S (w h) to about 2^-22
+// |w h|, every fp16 product exact in fp32.  SiLU and the split fuse: with
+// r' = 1 / ((1 + e^-u) / S) (the scale folded into the reciprocal's
+// argument, an exact power-of-two scaling), hs = u r' is formed exactly
+// inside v_fma_mix: x0s = fp16(u r') and x1 = fp16(u r' - x0s) each round
+// once.  The next layer's accumulator holds S (W h); its epilogue
+// u = acc / S + bias removes the scale exactly.
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+
 template <int NB, int C>
-struct ConvLayoutX3 {                            // units of 16 B
-    static constexpr int KS1 = C / 2;            // layer-1 fp32 k-steps
-    static constexpr int SL1 = (NB * 64 * KS1 / 4 + 63) / 64 * 64;
-    static constexpr int SLM = 2 * NB * 2 * 64;
-    static constexpr int SL4 = (C * 32 * NB / 4 + 63) / 64 * 64;   // layer 4: W4 in fp32, [C][W]
-    static constexpr int BUF = SL1 > SLM ? SL1 : SLM;
-    static constexpr int TOTAL = SL1 + 2 * NB * SLM + SL4;
-    // slab 0: layer 1; 1 + layer * NB + b: input block b of layer 2 or 3;
-    // 1 + 2 NB: layer 4
-    static constexpr __host__ __device__ int off(int i) { return i == 0 ? 0 : SL1 + (i - 1) * SLM; }
-    static constexpr __host__ __device__ int size(int i) {
-        return i == 0 ? SL1 : i == 1 + 2 * NB ? SL4 : SLM;
-    }
+struct LayoutS {                                  // units of 16 B (one lane's operand)
+    static constexpr int NO = 2 * NB;             // 16-feature output blocks of a W-wide layer
+    static constexpr int KC = NB;                 // 32-input reduction chunks
+    static constexpr int L1 = (NO * 16 + 63) / 64 * 64;   // layer 1: one fp32 per lane per block
+    static constexpr int L4 = KC * 2 * 64;        // layer 4: parts w0, w1 per chunk
+    static constexpr int RES = L1 + L4;           // resident in LDS for the whole kernel
+    static constexpr int SLAB = NO * 2 * 64;      // one chunk of a mid layer: every block, both parts
+    static constexpr int TOTAL = RES + 2 * KC * SLAB;
+    static constexpr __host__ __device__ int mid(int layer, int c) { return RES + (layer * KC + c) * SLAB; }
 };
+
+// SiLU and split of 8 inputs (registers 0..3 of two output blocks): the B
+// operands x0s, x1, x0 of one reduction chunk (invS = 1/S).  The work comes in
+// four pieces of two inputs (q = 0..3, packed register q of each operand) and
+// a final one (x0), so that it can be spread between MFMA groups.
+struct SplitB {
+    u4v p0, p1, p2;
+};
+__device__ __forceinline__ void silu_split_q(const float v0, const float v1, float invS,
+                                             uint32_t& x0s, uint32_t& x1) {
+    // r' = S / (1 + e^-v): the fused multiply-add gives (1 + e^-v) / S with one
+    // rounding, the power-of-two scale exactly
+    const float e0 = __builtin_amdgcn_exp2f(v0 * -1.44269504f);
+    const float e1 = __builtin_amdgcn_exp2f(v1 * -1.44269504f);
+    const float r0 = __builtin_amdgcn_rcpf(__builtin_fmaf(e0, invS, invS));
+    const float r1 = __builtin_amdgcn_rcpf(__builtin_fmaf(e1, invS, invS));
+    uint32_t a, b;
+    asm("v_fma_mixlo_f16 %0, %1, %2, 0\n\t"
+        "v_fma_mixhi_f16 %0, %3, %4, 0"
+        : "=&v"(a) : "v"(v0), "v"(r0), "v"(v1), "v"(r1));
+    asm("v_fma_mixlo_f16 %0, %1, %2, -%5 op_sel_hi:[0,0,1]\n\t"
+        "v_fma_mixhi_f16 %0, %3, %4, -%5 op_sel:[0,0,1] op_sel_hi:[0,0,1]"
+        : "=&v"(b) : "v"(v0), "v"(r0), "v"(v1), "v"(r1), "v"(a));
+    x0s = a;
+    x1 = b;
+}
+__device__ __forceinline__ float f4_at(const f4& ua, const f4& ub, int i) { return i < 4 ? ua[i] : ub[i - 4]; }
+__device__ __forceinline__ void silu_split_piece(int q, const f4& ua, const f4& ub, float invS, SplitB& s) {
+    if (q < 4) {
+        uint32_t a, b;
+        silu_split_q(f4_at(ua, ub, 2 * q), f4_at(ua, ub, 2 * q + 1), invS, a, b);
+        s.p0[q] = a;
+        s.p1[q] = b;
+    } else {                                         // x0 = x0s 2^-11
+        s.p2 = __builtin_bit_cast(u4v, __builtin_bit_cast(h8, s.p0) * (_Float16)0.00048828125f);
+    }
+}
+__device__ __forceinline__ SplitB silu_split(const f4& ua, const f4& ub, float invS) {
+    SplitB s;
+#pragma unroll
+    for (int q = 0; q < 5; ++q) silu_split_piece(q, ua, ub, invS, s);
+    return s;
+}
+
+// One LDS-DMA copy, 16 B per lane from gbase + voff to the LDS address lds +
+// 16 lane (global_load_lds_dwordx4, M0 = lds), issued as inline assembly: the
+// compiler's wait-count pass does not see it, so it keeps counting the
+// kernel's own LDS reads precisely (with an LDS-DMA in flight it would wait
+// for every outstanding LDS read before each use).  Callers wait for these
+// copies explicitly (s_waitcnt vmcnt(0)) before any wave reads their data.
+__device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %2\n\t"
+                 "global_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(voff), "s"(gbase), "s"(lds)
+                 : "memory", "m0");
+}
+template <class T>
+__device__ __forceinline__ uint32_t lds_addr(T* p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) T*)p;
+}
 
 template <int NB, int C>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void k_conv_f32x3(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
-    using L = ConvLayoutX3<NB, C>;
-    constexpr int NT = 4;                            // tiles per block, two waves each
-    constexpr int NBH = (NB + 1) / 2;                // output blocks of half 0 (half 1: NB - NBH)
-    constexpr int NPR = (NBH + 1) / 2;               // pairs of them
-    constexpr int W = 32 * NB;
-    static_assert(C % 2 == 0 && C <= 8, "layer 1 pairs channels; at most 8 channels");
-    __shared__ bf8 lds_0[L::BUF];
-    __shared__ bf8 lds_1[L::BUF];
-    __shared__ f4 xch_0[NT * 4 * 64];                // one input block's activations per tile
-    __shared__ f4 xch_1[NT * 4 * 64];
-    __shared__ __attribute__((aligned(16))) float vec[(NT + 2) * W];   // shifts of the tiles, b2, b3
-    __shared__ float s_max[2][NT][2];                // per layer, tile and half: largest |input|
+void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
+    using L = LayoutS<NB, C>;
+    constexpr int NW = 8;                          // waves per block, one tile each
+    constexpr int NO = L::NO, KC = L::KC, W = 32 * NB;
+    constexpr int STRIDE = (W + 255) / 256 * 256;  // floats per vector row: whole 1 KB copies
+    static_assert(C == 4, "layer 1 is one 16x16x4 fp32 MFMA per output block");
+    __shared__ h8 res[L::RES];
+    __shared__ h8 slab_0[L::SLAB];
+    __shared__ h8 slab_1[L::SLAB];
+    __shared__ __attribute__((aligned(16))) float vec[(NW + 2) * STRIDE];   // shifts, b2, b3
 
     const int groups = src.active ? *src.active : src.max_groups;
     const int64_t ntiles = (int64_t)groups * src.group * tiles_per_row;
-    const int64_t ngroups = (ntiles + NT - 1) / NT;
+    const int64_t ngroups = (ntiles + NW - 1) / NW;
     if ((int64_t)blockIdx.x >= ngroups) return;              // uniform over the block
 
-    const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, lg = lane >> 4, lj = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int tile = wave & (NT - 1);                // waves tile and tile + NT share a SIMD
-    const int oh = wave >> 2;                        // output half
     const int64_t P = a.P;
-    // does this wave own its j-th output block (half 1 has one fewer when NB is odd)
-    auto own = [&](int j) { return NB % 2 == 0 || oh == 0 || j < NB - NBH; };
 
-    auto ldsb = [&](int buf) -> bf8* { return buf ? lds_1 : lds_0; };
-    auto xchb = [&](int buf) -> f4* { return (buf ? xch_1 : xch_0) + tile * 4 * 64; };
-    auto dma = [&](int i, int buf) {                         // slab i -> buffer, 1 KB per wave op
-        const int nch = L::size(i) / 64;
-        const char* gb = reinterpret_cast<const char*>(a.frags);
-        uint32_t lo = (uint32_t)lane * 16u;
-        asm volatile("" : "+s"(gb), "+v"(lo));
-        bf8* ls = ldsb(buf);
-        for (int c = wave; c < nch; c += 2 * NT) {
-            const uint32_t ob = (uint32_t)(L::off(i) + c * 64) * 16u + lo;
-            __builtin_amdgcn_global_load_lds(
-                (const __attribute__((address_space(1))) void*)(gb + (size_t)ob),
-                (__attribute__((address_space(3))) void*)(ls + c * 64), 16, 0, 0);
+    // n_units (a multiple of 64) 16-B units of the packed weights -> LDS, 1 KB per wave op
+    auto dma = [&](h8* dst, int off, int n_units) {
+        const uint32_t lo = (uint32_t)lane * 16u;
+        const uint32_t base = lds_addr(dst);
+        for (int c = wave; c < n_units / 64; c += NW)
+            dma16(a.frags, (uint32_t)(off + c * 64) * 16u + lo, base + (uint32_t)c * 1024u);
+    };
+    auto dma_slab = [&](int s, int buf) { dma(buf ? slab_1 : slab_0, L::mid(0, 0) + s * L::SLAB, L::SLAB); };
+    // this wave's first-layer shift (b1 + e_n, plus Wc c on the guided branch) -> its vector row
+    auto dma_shift = [&](int n, int br) {
+        const float* row = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * W;
+        const uint32_t base = lds_addr(vec + wave * STRIDE);
+        for (int c = 0; c < STRIDE / 256; ++c) {
+            int off = c * 256 + lane * 4;
+            off = off <= W - 4 ? off : W - 4;            // lanes past the row re-read its end
+            dma16(row, (uint32_t)off * 4u, base + (uint32_t)c * 1024u);
         }
     };
     auto land = [&]() {
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     };
-    // first-layer shift of this tile for the next pass (row n, branch br), by the tile's half-0 wave
-    auto dma_shift = [&](int n, int br) {
-        if (oh != 0) return;
-        const float* row = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * W;
-        float* dst = vec + tile * W;
-        for (int c = 0; c * 256 < W; ++c) {
-            const int off = c * 256 + lane * 4;
-            if (off < W)                                     // W is a multiple of 32
-                __builtin_amdgcn_global_load_lds(
-                    (const __attribute__((address_space(1))) void*)(row + off),
-                    (__attribute__((address_space(3))) void*)(dst + c * 256), 16, 0, 0);
-        }
+    auto mfma = [](const h8& w, const h8& x, const f4& c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(w, x, c, 0, 0, 0);
     };
-    // SiLU(cs acc + v) of output block nb, v = LDS vector row vrow, in fp32;
-    // cs (a power of two) removes the scale the accumulator carries
-    auto act = [&](const f16v& c, float cs, int vrow, int nb, f4 (&h)[4]) {
-        const float* v = vec + vrow * W + 32 * nb + 4 * half;
-        static_for<4>([&](auto q4c) {
-            constexpr int q4 = decltype(q4c)::value;
-            const f4 sh = *reinterpret_cast<const f4*>(v + 8 * q4);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) h[q4][q] = silu(__builtin_fmaf(c[4 * q4 + q], cs, sh[q]));
-        });
+    // the weight fragments w0, w1 of output blocks o and o + 1 (at fr, fr + 128),
+    // and their three split products
+    struct Frag2 {
+        h8 a0, a1, b0, b1;
     };
-    // largest |cs acc + v| over this wave's output blocks (the values act
-    // takes the SiLU of), reduced over the wave
-    auto in_max = [&](const f16v (&c)[NBH], float cs, int vrow) {
+    auto load2 = [](const h8* fr) -> Frag2 { return Frag2{fr[0], fr[64], fr[128], fr[192]}; };
+    auto mac3x2 = [&](const Frag2& f, const SplitB& b, f4& A, f4& B) {
+        const h8 p0 = __builtin_bit_cast(h8, b.p0), p1 = __builtin_bit_cast(h8, b.p1),
+                 p2 = __builtin_bit_cast(h8, b.p2);
+        A = mfma(f.a0, p0, A);
+        B = mfma(f.b0, p0, B);
+        A = mfma(f.a0, p1, A);
+        B = mfma(f.b0, p1, B);
+        A = mfma(f.a1, p2, A);
+        B = mfma(f.b1, p2, B);
+    };
+    auto mac3 = [&](const h8* fr, const SplitB& b, f4& A) {
+        const h8 a0 = fr[0], a1 = fr[64];
+        A = mfma(a0, __builtin_bit_cast(h8, b.p0), A);
+        A = mfma(a0, __builtin_bit_cast(h8, b.p1), A);
+        A = mfma(a1, __builtin_bit_cast(h8, b.p2), A);
+    };
+    // per-tile scale of a layer's input from its largest |u| (over the wave):
+    // S = 2^(11-e) puts it in [2^14, 2^15); a non-finite or zero maximum keeps
+    // e = 0 (non-finite values then propagate as in fp32)
+    auto scale_of = [&](const f4 (&u)[NO]) -> int {
         float m = 0.f;
-        static_for<NBH>([&](auto jc) {
-            constexpr int j = decltype(jc)::value;
-            if (own(j)) {
-                const float* v = vec + vrow * W + 32 * (oh * NBH + j) + 4 * half;
-                static_for<4>([&](auto q4c) {
-                    constexpr int q4 = decltype(q4c)::value;
-                    const f4 sh = *reinterpret_cast<const f4*>(v + 8 * q4);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q)
-                        m = __builtin_fmaxf(m, __builtin_fabsf(__builtin_fmaf(c[j][4 * q4 + q], cs, sh[q])));
-                });
-            }
+        static_for<NO>([&](auto oc) {
+            constexpr int o = decltype(oc)::value;
+            m = __builtin_fmaxf(m, __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(u[o][0]), __builtin_fabsf(u[o][1])),
+                                                   __builtin_fmaxf(__builtin_fabsf(u[o][2]), __builtin_fabsf(u[o][3]))));
         });
 #pragma unroll
         for (int o = 32; o >= 1; o >>= 1) m = __builtin_fmaxf(m, __shfl_xor(m, o));
-        return m;
-    };
-    // the fp16 parts 2^11 x0, x1 and x0 of half g2 of a block's activations,
-    // scaled by sx: the B operands of its k-step g2
-    auto split_g2 = [&](auto g2c, const f4 (&h)[4], float sx, h8 (&p)[2][3]) {
-        constexpr int g2 = decltype(g2c)::value;
-        static_for<2>([&](auto q4h) {
-            constexpr int q4 = 2 * g2 + decltype(q4h)::value;
-            static_for<2>([&](auto qc) {
-                constexpr int q = 2 * decltype(qc)::value;
-                constexpr int u = 4 * (q4 % 2) + q;
-                const fl2 hv = fl2{h[q4][q], h[q4][q + 1]} * sx;        // exact
-                const h2 x0 = __builtin_convertvector(hv, h2);
-                const fl2 r = (hv - __builtin_convertvector(x0, fl2)) * 2048.f;   // exact
-                const h2 x1 = __builtin_convertvector(r, h2);
-                const h2 x0s = x0 * (_Float16)2048.f;                    // exact
-                p[g2][0][u] = x0s[0]; p[g2][0][u + 1] = x0s[1];
-                p[g2][1][u] = x1[0]; p[g2][1][u + 1] = x1[1];
-                p[g2][2][u] = x0[0]; p[g2][2][u + 1] = x0[1];
-            });
-        });
-    };
-    auto mfma = [](const h8& w, const h8& x, const f16v& c) {
-        return __builtin_amdgcn_mfma_f32_32x32x16_f16(w, x, c, 0, 0, 0);
-    };
-    // fragments w0, w1 of one output block against 2^11 x0, x1, x0
-    auto mac3 = [&](const h8* fr, const h8 (&x)[3], f16v& acc) {
-        const h8 w0 = fr[0], w1 = fr[64];
-        acc = mfma(w0, x[0], acc);
-        acc = mfma(w0, x[1], acc);
-        acc = mfma(w1, x[2], acc);
-    };
-    auto mac3x2 = [&](const h8* fa, const h8* fb, const h8 (&x)[3], f16v& A, f16v& B) {
-        const h8 a0 = fa[0], a1 = fa[64];
-        const h8 b0 = fb[0], b1 = fb[64];
-        A = mfma(a0, x[0], A);
-        B = mfma(b0, x[0], B);
-        A = mfma(a0, x[1], A);
-        B = mfma(b0, x[1], B);
-        A = mfma(a1, x[2], A);
-        B = mfma(b1, x[2], B);
+        int e = 0;
+        if (m > 0.f && m <= 3.4028235e38f) {
+            const int be = (int)((__builtin_bit_cast(uint32_t, m) >> 23) & 0xff);
+            e = (be == 0 ? -126 : be - 127) - 3;
+            e = e < -100 ? -100 : (e > 120 ? 120 : e);   // S and 1/S stay normal
+        }
+        return __builtin_amdgcn_readfirstlane(e);
     };
     struct Tile {
         int64_t row, px;
@@ -499,7 +496,7 @@ void k_conv_f32x3(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
     };
     auto locate = [&](int64_t tg) -> Tile {
         Tile T;
-        const int64_t t = tg * NT + tile;
+        const int64_t t = tg * NW + wave;
         T.active = t < ntiles;
         const int64_t tt = T.active ? t : ntiles - 1;       // idle waves redo the last tile
         T.row = tt / tiles_per_row;
@@ -508,196 +505,147 @@ void k_conv_f32x3(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per
         const int64_t sl = src.slot ? __builtin_amdgcn_readfirstlane(src.slot[g]) : g;
         T.x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
         T.n = __builtin_amdgcn_readfirstlane(src.n[g]);
-        T.px = (int64_t)pt * 32 + (lane & 31);
+        T.px = (int64_t)pt * 16 + lj;
         T.pxok = T.px < P;
         return T;
     };
+    // layer-1 input: lane l carries channel l/16 of pixel l%16
+    auto load_x = [&](const Tile& T) -> float { return T.pxok ? T.x[lg * P + T.px] : 0.f; };
     const int nbranch = a.shift_c ? 2 : 1;
 
     Tile cur = locate(blockIdx.x);
-    dma(0, 0);
+    dma(res, 0, L::RES);
     dma_shift(cur.n, 0);
-    for (int i = tid; i < W; i += 2 * NT * 64) {
-        vec[NT * W + i] = a.b2[i];
-        vec[(NT + 1) * W + i] = a.b3[i];
+    dma_slab(0, 0);
+    for (int i = tid; i < W; i += NW * 64) {
+        vec[NW * STRIDE + i] = a.b2[i];
+        vec[(NW + 1) * STRIDE + i] = a.b3[i];
     }
     land();
-    float xin[L::KS1];
-#pragma unroll
-    for (int s = 0; s < L::KS1; ++s) xin[s] = cur.pxok ? cur.x[(2 * s + half) * P + cur.px] : 0.f;
+    float xin = load_x(cur);
 
     for (int64_t tg = blockIdx.x; tg < ngroups; tg += gridDim.x) {
         const bool last_group = tg + gridDim.x >= ngroups;
-        Tile nxt = locate(last_group ? tg : tg + gridDim.x);
-        float xnx[L::KS1];
-#pragma unroll
-        for (int s = 0; s < L::KS1; ++s) xnx[s] = nxt.pxok ? nxt.x[(2 * s + half) * P + nxt.px] : 0.f;
-
-        float eu[C];
-#pragma unroll
-        for (int c = 0; c < C; ++c) eu[c] = 0.f;
+        const Tile nxt = locate(last_group ? tg : tg + gridDim.x);
+        const float xnx = load_x(nxt);
+        f4 eu = f4{0.f, 0.f, 0.f, 0.f};
         for (int br = 0; br < nbranch; ++br) {
-            f16v acc[NBH];
+            f4 acc[NO], u[NO];
+            // ---- layer 1: u = W1 x + shift (fp32 MFMA), from the resident fragments
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's shift row
+            {
+                const float* a1 = reinterpret_cast<const float*>(res) + lane;
+                const float* sh = vec + wave * STRIDE + 4 * lg;
+                static_for<NO>([&](auto oc) {
+                    constexpr int o = decltype(oc)::value;
+                    const f4 c1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[o * 64], xin, f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                    const f4 sv = *reinterpret_cast<const f4*>(sh + 16 * o);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) u[o][r] = __fadd_rn(c1[r], sv[r]);
+                });
+            }
+            int e = scale_of(u);
+            float invS = pow2(e - 11);
+            SplitB b = silu_split(u[0], u[1], invS);
 
-            // ---- layer 1 (slab 0, buffer 0): this wave's output blocks on fp32 MFMA
-            dma(1, 1);
-            static_for<NBH>([&](auto jc) {
-                constexpr int j = decltype(jc)::value;
-                acc[j] = f16v{};
-                if (own(j)) {
-                    const float* f1 = reinterpret_cast<const float*>(lds_0) + ((oh * NBH + j) * 64 + lane) * L::KS1;
-                    static_for<L::KS1>([&](auto sc) {
-                        constexpr int s = decltype(sc)::value;
-                        acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(f1[s], xin[s], acc[j], 0, 0, 0);
-                    });
-                }
-            });
-
-            // ---- layers 2 and 3: one slab per input block; the block's owner
-            // activates it into an exchange buffer one slab ahead.  cs is the
-            // scale the accumulators carry (none after layer 1's fp32 MFMAs).
-            float cs = 1.f;
+            // ---- layers 2 and 3: one streamed slab per reduction chunk
             static_for<2>([&](auto lc) {
                 constexpr int layer = decltype(lc)::value;
-                const int vin = layer == 0 ? tile : NT;
-                {
-                    const float m = in_max(acc, cs, vin);
-                    if (lane == 0) s_max[layer][tile][oh] = m;   // read after the next barrier
-                }
-                if (oh == 0) {
-                    f4 h[4];
-                    act(acc[0], cs, vin, 0, h);
-                    f4* xd = xchb(0);
-                    static_for<4>([&](auto q4c) { xd[decltype(q4c)::value * 64 + lane] = h[decltype(q4c)::value]; });
-                }
-                f16v nacc[NBH];
-                static_for<NBH>([&](auto jc) { nacc[decltype(jc)::value] = f16v{}; });
-                float sx = 1.f, cs_next = 1.f;
-                static_for<NB>([&](auto bc) {
-                    constexpr int b = decltype(bc)::value;
-                    constexpr int slab = 1 + layer * NB + b;
-                    constexpr int buf = slab & 1;
-                    land();                                      // slab b and block b's activations are in
-                    dma(slab + 1, buf ^ 1);
-                    if constexpr (b == 0) {
-                        // the tile's scale: its largest input m below 2^4, m 2^e < 2^(e+1)
-                        const float m = __builtin_fmaxf(s_max[layer][tile][0], s_max[layer][tile][1]);
-                        int e = 0;
-                        if (m > 0.f && m <= 3.4028235e38f) {
-                            const int be = (int)((__builtin_bit_cast(uint32_t, m) >> 23) & 0xff);
-                            e = (be == 0 ? -126 : be - 127) - 3;
-                            e = e < -100 ? -100 : (e > 120 ? 120 : e);   // 2^-e, 2^(e-11) normal
-                        }
-                        sx = pow2(-e);
-                        cs_next = pow2(e - 11);
-                    }
-                    if constexpr (b + 1 < NB) {
-                        constexpr int o = (b + 1) < NBH ? 0 : 1, jl = (b + 1) - o * NBH;
-                        if (oh == o) {
-                            f4 h[4];
-                            act(acc[jl], cs, vin, b + 1, h);
-                            f4* xd = xchb((b + 1) & 1);
-                            static_for<4>([&](auto q4c) { xd[decltype(q4c)::value * 64 + lane] = h[decltype(q4c)::value]; });
+                static_for<NO>([&](auto oc) { acc[decltype(oc)::value] = f4{0.f, 0.f, 0.f, 0.f}; });
+                static_for<KC>([&](auto cc) {
+                    constexpr int c = decltype(cc)::value;
+                    constexpr int s = layer * KC + c;
+                    constexpr int buf = s & 1;
+                    land();                                  // slab s has landed; buffer buf^1 is free
+                    if constexpr (s + 1 < 2 * KC) {
+                        dma_slab(s + 1, buf ^ 1);
+                    } else {                                 // the next pass: its shift row and first slab
+                        const bool more = br + 1 < nbranch || !last_group;
+                        if (more) {
+                            if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
+                            else dma_shift(nxt.n, 0);
+                            dma_slab(0, buf ^ 1);
                         }
                     }
-                    const f4* xs = xchb(b & 1);
-                    static_for<2>([&](auto g2c) {
-                        constexpr int g2 = decltype(g2c)::value;
-                        h8 X[2][3];
-                        {
-                            f4 h[4];
-                            h[2 * g2] = xs[(2 * g2) * 64 + lane];
-                            h[2 * g2 + 1] = xs[(2 * g2 + 1) * 64 + lane];
-                            split_g2(g2c, h, sx, X);
-                        }
-                        static_for<NPR>([&](auto pc) {
-                            constexpr int j = 2 * decltype(pc)::value;
-                            const h8* fr = reinterpret_cast<const h8*>(ldsb(buf)) +
-                                           ((g2 * NB + oh * NBH + j) * 2) * 64 + lane;
-                            if constexpr (j + 1 < NBH) {
-                                if (own(j + 1)) mac3x2(fr, fr + 2 * 64, X[g2], nacc[j], nacc[j + 1]);
-                                else mac3(fr, X[g2], nacc[j]);
-                            } else {
-                                if (own(j)) mac3(fr, X[g2], nacc[j]);
-                            }
+                    // software pipeline: the fragments of pair j + 1 are loaded and
+                    // a fifth of the next chunk's SiLU and split is done before the
+                    // six MFMAs of pair j (the order is fixed: the scheduler keeps
+                    // the loads ahead of the products they feed)
+                    SplitB bn;
+                    const h8* fr = (buf ? slab_1 : slab_0) + lane;
+                    Frag2 cur2 = load2(fr);
+                    static_for<NO / 2>([&](auto pc) {
+                        constexpr int j = decltype(pc)::value;
+                        Frag2 nxt2;
+                        if constexpr (j + 1 < NO / 2) nxt2 = load2(fr + (2 * j + 2) * 128);
+                        if constexpr (c + 1 < KC && j < 5) silu_split_piece(j, u[2 * c + 2], u[2 * c + 3], invS, bn);
+                        mac3x2(cur2, b, acc[2 * j], acc[2 * j + 1]);
+                        // issue order inside the group: each MFMA followed by a
+                        // fragment load and two VALU instructions, so that the
+                        // SiLU chain's latency sits under the products
+                        static_for<4>([&](auto) {
+                            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+                            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+                            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);   // VALU
                         });
+                        static_for<2>([&](auto) {
+                            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                        });
+                        __builtin_amdgcn_sched_barrier(0);
+                        if constexpr (j + 1 < NO / 2) cur2 = nxt2;
                     });
+                    if constexpr (c + 1 < KC) {
+                        if constexpr (NO / 2 < 5) {          // fewer pairs than pieces
+                            static_for<5>([&](auto qc) {
+                                if constexpr (decltype(qc)::value >= NO / 2)
+                                    silu_split_piece(decltype(qc)::value, u[2 * c + 2], u[2 * c + 3], invS, bn);
+                            });
+                        }
+                        b = bn;
+                    }
                 });
-                static_for<NBH>([&](auto jc) { acc[decltype(jc)::value] = nacc[decltype(jc)::value]; });
-                cs = cs_next;
+                // epilogue: u = acc / S + bias (an exact scaling, then the add)
+                const float cs = invS;
+                const float* bias = vec + (NW + layer) * STRIDE + 4 * lg;
+                static_for<NO>([&](auto oc) {
+                    constexpr int o = decltype(oc)::value;
+                    const f4 bv = *reinterpret_cast<const f4*>(bias + 16 * o);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) u[o][r] = __builtin_fmaf(acc[o][r], cs, bv[r]);
+                });
+                e = scale_of(u);
+                invS = pow2(e - 11);
+                b = silu_split(u[0], u[1], invS);
             });
 
-            // ---- layer 4 (slab 2NB+1, buffer 1: W4 in fp32): C outputs as fp32
-            // dot products on the VALU, each half over its own input blocks, the
-            // lane halves (the same pixel) added by a lane swap; half 1 hands its
-            // sums to half 0
+            // ---- layer 4 (C outputs in one block, rows past C zero), resident fragments
+            f4 o4 = f4{0.f, 0.f, 0.f, 0.f};
             {
-                constexpr int slab = 1 + 2 * NB;
-                constexpr int buf = slab & 1;
-                constexpr int C4 = (C + 3) / 4;
-                land();
-                const bool more = br + 1 < nbranch || !last_group;
-                if (more) {                                      // next pass's layer 1
-                    dma(0, 0);
-                    if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
-                    else dma_shift(nxt.n, 0);
-                }
-                const float* w4 = reinterpret_cast<const float*>(ldsb(buf));
-                float part[4 * C4];
-#pragma unroll
-                for (int c = 0; c < 4 * C4; ++c) part[c] = 0.f;
-                static_for<NBH>([&](auto jc) {
-                    constexpr int j = decltype(jc)::value;
-                    if (own(j)) {
-                        f4 h[4];
-                        act(acc[j], cs, NT + 1, oh * NBH + j, h);
-                        static_for<4>([&](auto q4c) {
-                            constexpr int q4 = decltype(q4c)::value;
-                            const int f = 32 * (oh * NBH + j) + 8 * q4 + 4 * half;   // features f..f+3
-                            static_for<C>([&](auto cc) {
-                                constexpr int c = decltype(cc)::value;
-                                const f4 w = *reinterpret_cast<const f4*>(w4 + c * W + f);
-#pragma unroll
-                                for (int q = 0; q < 4; ++q) part[c] = __builtin_fmaf(w[q], h[q4][q], part[c]);
-                            });
-                        });
-                    }
+                const h8* f4r = res + L::L1 + lane;
+                static_for<KC>([&](auto cc) {
+                    constexpr int c = decltype(cc)::value;
+                    if constexpr (c > 0) b = silu_split(u[2 * c], u[2 * c + 1], invS);
+                    mac3(f4r + c * 128, b, o4);
                 });
+            }
+            // lanes 0..15 hold channel r of pixel l in register r
+            if (lane < 16) {
+                float* out = eps + cur.row * (int64_t)C * P;
 #pragma unroll
-                for (int c = 0; c < C; ++c) part[c] += __shfl_xor(part[c], 32);
-                f4* xp = xchb(0);
-                if (oh == 1) {
-#pragma unroll
-                    for (int k = 0; k < C4; ++k)
-                        xp[k * 64 + lane] = f4{part[4 * k], part[4 * k + 1], part[4 * k + 2], part[4 * k + 3]};
-                }
-                __syncthreads();
-                if (oh == 0 && half == 0) {
-                    float* out = eps + cur.row * (int64_t)C * P;
-#pragma unroll
-                    for (int k = 0; k < C4; ++k) {
-                        const f4 o1 = xp[k * 64 + lane];
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const int c = 4 * k + r;
-                            if (c < C) {
-                                const float v = (part[c] + o1[r]) + a.b4[c];
-                                if (br == 0) {
-                                    eu[c] = v;
-                                    if (nbranch == 1 && cur.active && cur.pxok) out[c * P + cur.px] = v;
-                                } else if (cur.active && cur.pxok) {
-                                    out[c * P + cur.px] = eu[c] + a.guidance * (v - eu[c]);
-                                }
-                            }
-                        }
+                for (int r = 0; r < C; ++r) {
+                    const float v = __builtin_fmaf(o4[r], invS, a.b4[r]);
+                    if (br == 0) {
+                        eu[r] = v;
+                        if (nbranch == 1 && cur.active && cur.pxok) out[r * P + cur.px] = v;
+                    } else if (cur.active && cur.pxok) {
+                        out[r * P + cur.px] = eu[r] + a.guidance * (v - eu[r]);
                     }
                 }
-                land();                                          // slab 0 is in buffer 0 again
             }
         }
         cur = nxt;
-#pragma unroll
-        for (int s = 0; s < L::KS1; ++s) xin[s] = xnx[s];
+        xin = xnx;
     }
 }
 
@@ -754,39 +702,49 @@ void split_f16(float w, uint16_t (&p)[2]) {
 }
 
 template <int NB, int C>
-void pack_x3_t(const float* W1, const float* W2, const float* W3, const float* W4,
-               std::vector<uint8_t>& out) {
-    using L = ConvLayoutX3<NB, C>;
+void pack_s_t(const float* W1, const float* W2, const float* W3, const float* W4,
+              std::vector<uint8_t>& out) {
+    using L = LayoutS<NB, C>;
     constexpr int W = 32 * NB;
     out.assign((size_t)L::TOTAL * 16, 0);
-    float* f = reinterpret_cast<float*>(out.data());            // layer 1: fp32 fragments
-    for (int nb = 0; nb < NB; ++nb)
-        for (int l = 0; l < 64; ++l)
-            for (int s = 0; s < L::KS1; ++s)
-                f[L::off(0) * 4 + (nb * 64 + l) * L::KS1 + s] = W1[(32 * nb + l % 32) * C + 2 * s + l / 32];
+    float* f = reinterpret_cast<float*>(out.data());
+    for (int o = 0; o < L::NO; ++o)
+        for (int l = 0; l < 64; ++l) f[o * 64 + l] = W1[(16 * o + l % 16) * C + l / 16];
     uint16_t* h = reinterpret_cast<uint16_t*>(out.data());
-    auto put = [&](int unit, int u, float w) {                  // part k -> k fragments on
-        uint16_t p[2];
-        split_f16(w, p);
-        for (int k = 0; k < 2; ++k) h[((size_t)unit + (size_t)k * 64) * 8 + u] = p[k];
+    // element u of lane l in reduction chunk c: input 32 c + 16 (u/4) + 4 (l/16) + u%4
+    auto fin = [](int c, int l, int u) { return 32 * c + 16 * (u / 4) + 4 * (l / 16) + u % 4; };
+    auto put = [&](int unit, int u, float w) {                  // parts 0, 1 -> units unit, unit + 64
+        uint16_t pr[2];
+        split_f16(w, pr);
+        for (int k = 0; k < 2; ++k) h[((size_t)unit + (size_t)k * 64) * 8 + u] = pr[k];
     };
-    auto fin = [](int b, int g2, int l, int u) { return 32 * b + 16 * g2 + 8 * (u / 4) + 4 * (l / 32) + u % 4; };
+    for (int c = 0; c < L::KC; ++c)
+        for (int l = 0; l < 64; ++l)
+            for (int u = 0; u < 8; ++u)
+                put(L::L1 + c * 128 + l, u, (l % 16) < C ? W4[(size_t)(l % 16) * W + fin(c, l, u)] : 0.f);
     for (int layer = 0; layer < 2; ++layer) {
         const float* Wm = layer == 0 ? W2 : W3;
-        for (int b = 0; b < NB; ++b)
-            for (int g2 = 0; g2 < 2; ++g2)
-                for (int nb = 0; nb < NB; ++nb)
-                    for (int l = 0; l < 64; ++l)
-                        for (int u = 0; u < 8; ++u)
-                            put(L::off(1 + layer * NB + b) + ((g2 * NB + nb) * 2) * 64 + l, u,
-                                Wm[(32 * nb + l % 32) * W + fin(b, g2, l, u)]);
+        for (int c = 0; c < L::KC; ++c)
+            for (int o = 0; o < L::NO; ++o)
+                for (int l = 0; l < 64; ++l)
+                    for (int u = 0; u < 8; ++u)
+                        put(L::mid(layer, c) + o * 128 + l, u, Wm[(size_t)(16 * o + l % 16) * W + fin(c, l, u)]);
     }
-    float* f4w = f + (size_t)L::off(1 + 2 * NB) * 4;              // layer 4: fp32 [C][W]
-    for (int c = 0; c < C; ++c)
-        for (int k = 0; k < W; ++k) f4w[c * W + k] = W4[(size_t)c * W + k];
 }
 
 int device_cus();
+
+template <int NB, int C>
+void launch_s_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
+    const int tiles_per_row = (int)((a.P + 15) / 16);
+    const int64_t ntiles = (int64_t)src.max_groups * src.group * tiles_per_row;
+    if (ntiles == 0) return;
+    int64_t blocks = (ntiles + 7) / 8;                       // persistent: one block per CU
+    if (blocks > device_cus()) blocks = device_cus();
+    hipLaunchKernelGGL((k_conv_f32s<NB, C>), dim3((unsigned)blocks), dim3(512), 0, s, a, src, eps,
+                       tiles_per_row);
+    PD_HIP(hipGetLastError());
+}
 
 template <int NB, int C>
 void launch_bf16_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
@@ -811,19 +769,6 @@ int device_cus() {
     return cus;
 }
 
-template <int NB, int C>
-void launch_x3_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
-    const int tiles_per_row = (int)((a.P + 31) / 32);
-    const int64_t ntiles = (int64_t)src.max_groups * src.group * tiles_per_row;
-    if (ntiles == 0) return;
-    int64_t blocks = (ntiles + 3) / 4;                       // persistent: one block per CU
-    if (blocks > device_cus()) blocks = device_cus();
-    hipLaunchKernelGGL((k_conv_f32x3<NB, C>), dim3((unsigned)blocks), dim3(512), 0, s, a, src, eps,
-                       tiles_per_row);
-    PD_HIP(hipGetLastError());
-}
-
-// (blocks of 32 features, channels): widths 32, 64, 96, 128 and 320 over 4 channels
 #define PD_CONV_SHAPES(X) X(1, 4) X(2, 4) X(3, 4) X(4, 4) X(10, 4)
 
 }  // namespace
@@ -839,7 +784,7 @@ bool conv_supported(int C, int width, bool bf16) {
 size_t conv_frag_bytes(int C, int width, bool bf16) {
 #define X(nb, c)                                                                      \
     if (C == c && width == 32 * nb)                                                   \
-        return bf16 ? (size_t)ConvLayoutBf16<nb, c>::TOTAL * 16 : (size_t)ConvLayoutX3<nb, c>::TOTAL * 16;
+        return bf16 ? (size_t)ConvLayoutBf16<nb, c>::TOTAL * 16 : (size_t)LayoutS<nb, c>::TOTAL * 16;
     PD_CONV_SHAPES(X)
 #undef X
     return 0;
@@ -852,7 +797,7 @@ void conv_pack_weights(int C, int width, bool bf16, const float* W1, const float
         if (bf16)                                                 \
             pack_bf16_t<nb, c>(W1, W2, W3, W4, out);              \
         else                                                      \
-            pack_x3_t<nb, c>(W1, W2, W3, W4, out);                \
+            pack_s_t<nb, c>(W1, W2, W3, W4, out);                 \
         return;                                                   \
     }
     PD_CONV_SHAPES(X)
@@ -866,7 +811,7 @@ void launch_conv1x1(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_
         if (a.bf16)                                                \
             launch_bf16_t<nb, c>(a, src, eps, s);                  \
         else                                                       \
-            launch_x3_t<nb, c>(a, src, eps, s);                    \
+            launch_s_t<nb, c>(a, src, eps, s);                     \
         return;                                                    \
     }
     PD_CONV_SHAPES(X)
