@@ -394,6 +394,13 @@ __device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, uint32_t
                  : "v"(voff), "s"(gbase), "s"(lds)
                  : "memory", "m0");
 }
+__device__ __forceinline__ void dma4(const void* gbase, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %2\n\t"
+                 "global_load_lds_dword %0, %1"
+                 :
+                 : "v"(voff), "s"(gbase), "s"(lds)
+                 : "memory", "m0");
+}
 template <class T>
 __device__ __forceinline__ uint32_t lds_addr(T* p) {
     return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) T*)p;
@@ -405,11 +412,17 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
     using L = LayoutS<NB, C>;
     constexpr int NW = 8;                          // waves per block, one tile each
     constexpr int NO = L::NO, KC = L::KC, W = 32 * NB;
-    constexpr int STRIDE = (W + 255) / 256 * 256;  // floats per vector row: whole 1 KB copies
+    constexpr int STRIDE = (W + 63) / 64 * 64;     // floats per vector row: whole 256-B copies
+    constexpr int NS = 2 * KC;                     // streamed slabs per pass
+    // each wave copies the same number of 1 KB pieces of every slab (repeating
+    // a piece where there are fewer than waves), so that a wave's own count
+    // of outstanding copies says which slab has landed
+    constexpr int PER_WAVE = (L::SLAB / 64 + NW - 1) / NW;
     static_assert(C == 4, "layer 1 is one 16x16x4 fp32 MFMA per output block");
     __shared__ h8 res[L::RES];
-    __shared__ h8 slab_0[L::SLAB];
-    __shared__ h8 slab_1[L::SLAB];
+    // three buffers: the slab in use and the next two (one array: the copies
+    // into it are invisible to the compiler, so nothing is serialised by it)
+    __shared__ h8 slabs[3 * L::SLAB];
     __shared__ __attribute__((aligned(16))) float vec[(NW + 2) * STRIDE];   // shifts, b2, b3
 
     const int groups = src.active ? *src.active : src.max_groups;
@@ -423,24 +436,52 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 
     // n_units (a multiple of 64) 16-B units of the packed weights -> LDS, 1 KB per wave op
     auto dma = [&](h8* dst, int off, int n_units) {
-        const uint32_t lo = (uint32_t)lane * 16u;
+        const char* gb = reinterpret_cast<const char*>(a.frags);
+        uint32_t lo = (uint32_t)lane * 16u;
+        asm volatile("" : "+s"(gb), "+v"(lo));
         const uint32_t base = lds_addr(dst);
         for (int c = wave; c < n_units / 64; c += NW)
-            dma16(a.frags, (uint32_t)(off + c * 64) * 16u + lo, base + (uint32_t)c * 1024u);
+            dma16(gb + (size_t)(off + c * 64) * 16u, lo, base + (uint32_t)c * 1024u);
     };
-    auto dma_slab = [&](int s, int buf) { dma(buf ? slab_1 : slab_0, L::mid(0, 0) + s * L::SLAB, L::SLAB); };
+    auto slab_buf = [&](int buf) -> h8* { return slabs + buf * L::SLAB; };
+    // streamed slab s (0 <= s < NS) -> buffer buf, PER_WAVE copies per wave
+    auto dma_slab = [&](int s, int buf) {
+        // the empty asm makes the base opaque: the copies' addresses are then
+        // formed where they are used, not hoisted out of the loops (where they
+        // would hold a hundred registers)
+        const char* gb = reinterpret_cast<const char*>(a.frags);
+        uint32_t lo = (uint32_t)lane * 16u;
+        asm volatile("" : "+s"(gb), "+v"(lo));
+        const uint32_t base = lds_addr(slab_buf(buf));
+        const int off = L::mid(0, 0) + s * L::SLAB;
+#pragma unroll
+        for (int i = 0; i < PER_WAVE; ++i) {
+            int c = wave + i * NW;
+            c = c < L::SLAB / 64 ? c : L::SLAB / 64 - 1;
+            dma16(gb + (size_t)(off + c * 64) * 16u, lo, base + (uint32_t)c * 1024u);
+        }
+    };
     // this wave's first-layer shift (b1 + e_n, plus Wc c on the guided branch) -> its vector row
+    // 16 B per lane while a whole 256 floats remain, then 4 B per lane (lanes
+    // past the row re-read its last value into the row's padding)
     auto dma_shift = [&](int n, int br) {
         const float* row = (br == 0 ? a.shift_u : a.shift_c) + (int64_t)n * W;
         const uint32_t base = lds_addr(vec + wave * STRIDE);
-        for (int c = 0; c < STRIDE / 256; ++c) {
-            int off = c * 256 + lane * 4;
-            off = off <= W - 4 ? off : W - 4;            // lanes past the row re-read its end
-            dma16(row, (uint32_t)off * 4u, base + (uint32_t)c * 1024u);
+        constexpr int N4 = W / 256;
+        for (int c = 0; c < N4; ++c) dma16(row, (uint32_t)(c * 256 + lane * 4) * 4u, base + (uint32_t)c * 1024u);
+        for (int c = N4 * 4; c < STRIDE / 64; ++c) {
+            int off = c * 64 + lane;
+            off = off < W ? off : W - 1;
+            dma4(row, (uint32_t)off * 4u, base + (uint32_t)c * 256u);
         }
     };
     auto land = [&]() {
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    };
+    // every copy but this wave's last PER_WAVE (the slab after the one needed) has landed
+    auto land_but_next = [&]() {
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(PER_WAVE) : "memory");
         __syncthreads();
     };
     auto mfma = [](const h8& w, const h8& x, const f4& c) {
@@ -517,12 +558,15 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
     dma(res, 0, L::RES);
     dma_shift(cur.n, 0);
     dma_slab(0, 0);
+    dma_slab(1, 1);
     for (int i = tid; i < W; i += NW * 64) {
         vec[NW * STRIDE + i] = a.b2[i];
         vec[(NW + 1) * STRIDE + i] = a.b3[i];
     }
     land();
     float xin = load_x(cur);
+    // slab s of the current pass sits in buffer (rot + s) % 3
+    int rot = 0;
 
     for (int64_t tg = blockIdx.x; tg < ngroups; tg += gridDim.x) {
         const bool last_group = tg + gridDim.x >= ngroups;
@@ -555,16 +599,23 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                 static_for<KC>([&](auto cc) {
                     constexpr int c = decltype(cc)::value;
                     constexpr int s = layer * KC + c;
-                    constexpr int buf = s & 1;
-                    land();                                  // slab s has landed; buffer buf^1 is free
-                    if constexpr (s + 1 < 2 * KC) {
-                        dma_slab(s + 1, buf ^ 1);
-                    } else {                                 // the next pass: its shift row and first slab
-                        const bool more = br + 1 < nbranch || !last_group;
+                    const int buf = (rot + s) % 3;
+                    // slab s has landed (at s = 0 everything has: slabs 0 and 1 were
+                    // copied during the previous pass); the buffer of slab s - 1
+                    // is free for slab s + 2
+                    if constexpr (s == 0) land();
+                    else land_but_next();
+                    const int nbuf = (rot + s + 2) % 3;
+                    const bool more = br + 1 < nbranch || !last_group;
+                    if constexpr (s + 2 < NS) {
+                        dma_slab(s + 2, nbuf);
+                    } else {                                 // the next pass's slabs 0 and 1
                         if (more) {
-                            if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
-                            else dma_shift(nxt.n, 0);
-                            dma_slab(0, buf ^ 1);
+                            if constexpr (s + 2 == NS) {
+                                if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
+                                else dma_shift(nxt.n, 0);
+                            }
+                            dma_slab(s + 2 - NS, nbuf);
                         }
                     }
                     // software pipeline: the fragments of pair j + 1 are loaded and
@@ -572,7 +623,7 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                     // six MFMAs of pair j (the order is fixed: the scheduler keeps
                     // the loads ahead of the products they feed)
                     SplitB bn;
-                    const h8* fr = (buf ? slab_1 : slab_0) + lane;
+                    const h8* fr = slab_buf(buf) + lane;
                     Frag2 cur2 = load2(fr);
                     static_for<NO / 2>([&](auto pc) {
                         constexpr int j = decltype(pc)::value;
@@ -619,6 +670,7 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                 b = silu_split(u[0], u[1], invS);
             });
 
+            rot = (rot + NS) % 3;
             // ---- layer 4 (C outputs in one block, rows past C zero), resident fragments
             f4 o4 = f4{0.f, 0.f, 0.f, 0.f};
             {
