@@ -387,18 +387,26 @@ __device__ __forceinline__ SplitB silu_split(const f4& ua, const f4& ub, float i
 // kernel's own LDS reads precisely (with an LDS-DMA in flight it would wait
 // for every outstanding LDS read before each use).  Callers wait for these
 // copies explicitly (s_waitcnt vmcnt(0)) before any wave reads their data.
+// The base address is uniform over the wave by construction; readfirstlane
+// puts it in scalar registers, as the instruction needs.
+__device__ __forceinline__ uint64_t uniform_addr(const void* p) {
+    const uint64_t v = (uint64_t)(uintptr_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
 __device__ __forceinline__ void dma16(const void* gbase, uint32_t voff, uint32_t lds) {
     asm volatile("s_mov_b32 m0, %2\n\t"
                  "global_load_lds_dwordx4 %0, %1"
                  :
-                 : "v"(voff), "s"(gbase), "s"(lds)
+                 : "v"(voff), "s"(uniform_addr(gbase)), "s"(__builtin_amdgcn_readfirstlane(lds))
                  : "memory", "m0");
 }
 __device__ __forceinline__ void dma4(const void* gbase, uint32_t voff, uint32_t lds) {
     asm volatile("s_mov_b32 m0, %2\n\t"
                  "global_load_lds_dword %0, %1"
                  :
-                 : "v"(voff), "s"(gbase), "s"(lds)
+                 : "v"(voff), "s"(uniform_addr(gbase)), "s"(__builtin_amdgcn_readfirstlane(lds))
                  : "memory", "m0");
 }
 template <class T>
