@@ -93,7 +93,7 @@ def metric_name(wl) -> str:
 
 
 def denoiser_kernel(wl, dtype: str) -> str:
-    conv = "k_conv_bf16" if dtype == "bf16" else "k_conv_f32x3"
+    conv = "k_conv_bf16" if dtype == "bf16" else "k_conv_f32s"
     return {"conv1x1": conv, "mlp": "k_linear", "gmm2d": "k_gmm"}[wl.model.kind]
 
 

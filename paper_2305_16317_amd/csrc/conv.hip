@@ -316,14 +316,17 @@ __device__ __forceinline__ float pow2(int k) { return __builtin_bit_cast(float, 
 // Split products: the weights w = w0 + 2^-11 w1 as before.  The activation
 // h = SiLU(u) of a layer's input enters scaled, hs = S h with S = 2^(11-e) a
 // power of two per tile and layer that puts the tile's largest input below
-// 2^15 (e from its largest |u|): x0s = fp16(hs), x1 = fp16(hs - x0s) and
+// 2^15 (e from its largest |t|, below): x0s = fp16(hs), x1 = fp16(hs - x0s) and
 // x0 = x0s 2^-11, so that w0 x0s + w0 x1 + w1 x0 = S (w h) to about 2^-22
-// |w h|, every fp16 product exact in fp32.  SiLU and the split fuse: with
-// r' = 1 / ((1 + e^-u) / S) (the scale folded into the reciprocal's
-// argument, an exact power-of-two scaling), hs = u r' is formed exactly
-// inside v_fma_mix: x0s = fp16(u r') and x1 = fp16(u r' - x0s) each round
-// once.  The next layer's accumulator holds S (W h); its epilogue
-// u = acc / S + bias removes the scale exactly.
+// |w h|, every fp16 product exact in fp32.  A pre-activation u is carried as
+// t = kNegLog2e u, the base-2 argument of e^-u, so that no multiply precedes
+// the exponential: the epilogue forms t = acc (kNegLog2e / S) + kNegLog2e b
+// in one fused multiply-add (the scaling exact, the bias row pre-multiplied).
+// SiLU and the split fuse: with e = 2^t and r = 1 / ((1 + e) kNegLog2e / S)
+// (one fused multiply-add for the product, the scale an exact power of two),
+// t r = S u / (1 + e) = hs, formed exactly inside v_fma_mix: x0s = fp16(t r)
+// and x1 = fp16(t r - x0s) each round once.  The next layer's accumulator
+// holds S (W h).
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 
 template <int NB, int C>
@@ -339,20 +342,22 @@ struct LayoutS {                                  // units of 16 B (one lane's o
 };
 
 // SiLU and split of 8 inputs (registers 0..3 of two output blocks): the B
-// operands x0s, x1, x0 of one reduction chunk (invS = 1/S).  The work comes in
-// four pieces of two inputs (q = 0..3, packed register q of each operand) and
-// a final one (x0), so that it can be spread between MFMA groups.
+// operands x0s, x1, x0 of one reduction chunk.  The inputs arrive as
+// t = kNegLog2e u (u the pre-activation) and c = kNegLog2e / S.  The work comes
+// in four pieces of two inputs (q = 0..3, packed register q of each operand)
+// and a final one (x0), so that it can be spread between MFMA groups.
 struct SplitB {
     u4v p0, p1, p2;
 };
-__device__ __forceinline__ void silu_split_q(const float v0, const float v1, float invS,
+__device__ __forceinline__ void silu_split_q(const float v0, const float v1, float c,
                                              uint32_t& x0s, uint32_t& x1) {
-    // r' = S / (1 + e^-v): the fused multiply-add gives (1 + e^-v) / S with one
-    // rounding, the power-of-two scale exactly
-    const float e0 = __builtin_amdgcn_exp2f(v0 * -1.44269504f);
-    const float e1 = __builtin_amdgcn_exp2f(v1 * -1.44269504f);
-    const float r0 = __builtin_amdgcn_rcpf(__builtin_fmaf(e0, invS, invS));
-    const float r1 = __builtin_amdgcn_rcpf(__builtin_fmaf(e1, invS, invS));
+    // e = 2^t = e^-u and r = 1 / ((1 + e) c): the fused multiply-add forms
+    // (1 + e) c with one rounding, and t r = S u / (1 + e) = S SiLU(u) since
+    // the same float constant kNegLog2e is in t and in c
+    const float e0 = __builtin_amdgcn_exp2f(v0);
+    const float e1 = __builtin_amdgcn_exp2f(v1);
+    const float r0 = __builtin_amdgcn_rcpf(__builtin_fmaf(e0, c, c));
+    const float r1 = __builtin_amdgcn_rcpf(__builtin_fmaf(e1, c, c));
     uint32_t a, b;
     asm("v_fma_mixlo_f16 %0, %1, %2, 0\n\t"
         "v_fma_mixhi_f16 %0, %3, %4, 0"
@@ -364,20 +369,20 @@ __device__ __forceinline__ void silu_split_q(const float v0, const float v1, flo
     x1 = b;
 }
 __device__ __forceinline__ float f4_at(const f4& ua, const f4& ub, int i) { return i < 4 ? ua[i] : ub[i - 4]; }
-__device__ __forceinline__ void silu_split_piece(int q, const f4& ua, const f4& ub, float invS, SplitB& s) {
+__device__ __forceinline__ void silu_split_piece(int q, const f4& ua, const f4& ub, float c, SplitB& s) {
     if (q < 4) {
         uint32_t a, b;
-        silu_split_q(f4_at(ua, ub, 2 * q), f4_at(ua, ub, 2 * q + 1), invS, a, b);
+        silu_split_q(f4_at(ua, ub, 2 * q), f4_at(ua, ub, 2 * q + 1), c, a, b);
         s.p0[q] = a;
         s.p1[q] = b;
     } else {                                         // x0 = x0s 2^-11
         s.p2 = __builtin_bit_cast(u4v, __builtin_bit_cast(h8, s.p0) * (_Float16)0.00048828125f);
     }
 }
-__device__ __forceinline__ SplitB silu_split(const f4& ua, const f4& ub, float invS) {
+__device__ __forceinline__ SplitB silu_split(const f4& ua, const f4& ub, float c) {
     SplitB s;
 #pragma unroll
-    for (int q = 0; q < 5; ++q) silu_split_piece(q, ua, ub, invS, s);
+    for (int q = 0; q < 5; ++q) silu_split_piece(q, ua, ub, c, s);
     return s;
 }
 
@@ -414,7 +419,7 @@ __device__ __forceinline__ uint32_t lds_addr(T* p) {
     return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) T*)p;
 }
 
-template <int NB, int C>
+template <int NB, int C, bool GUIDED>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_row) {
     using L = LayoutS<NB, C>;
@@ -517,15 +522,16 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
         A = mfma(a0, __builtin_bit_cast(h8, b.p1), A);
         A = mfma(a1, __builtin_bit_cast(h8, b.p2), A);
     };
-    // per-tile scale of a layer's input from its largest |u| (over the wave):
-    // S = 2^(11-e) puts it in [2^14, 2^15); a non-finite or zero maximum keeps
-    // e = 0 (non-finite values then propagate as in fp32)
-    auto scale_of = [&](const f4 (&u)[NO]) -> int {
+    // per-tile scale of a layer's input from its largest |t| (over the wave):
+    // S = 2^(11-e) puts S |t| in [2^14, 2^15), so S |u| = S |t| / log2(e) stays
+    // below 2^15; a non-finite or zero maximum keeps e = 0 (non-finite values
+    // then propagate as in fp32)
+    auto scale_of = [&](const f4 (&t)[NO]) -> int {
         float m = 0.f;
         static_for<NO>([&](auto oc) {
             constexpr int o = decltype(oc)::value;
-            m = __builtin_fmaxf(m, __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(u[o][0]), __builtin_fabsf(u[o][1])),
-                                                   __builtin_fmaxf(__builtin_fabsf(u[o][2]), __builtin_fabsf(u[o][3]))));
+            m = __builtin_fmaxf(m, __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(t[o][0]), __builtin_fabsf(t[o][1])),
+                                                   __builtin_fmaxf(__builtin_fabsf(t[o][2]), __builtin_fabsf(t[o][3]))));
         });
 #pragma unroll
         for (int o = 32; o >= 1; o >>= 1) m = __builtin_fmaxf(m, __shfl_xor(m, o));
@@ -538,10 +544,10 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
         return __builtin_amdgcn_readfirstlane(e);
     };
     struct Tile {
-        int64_t row, px;
-        bool active, pxok;
+        int64_t row;
+        bool active;
         const float* x;
-        int n;
+        int n, px;
     };
     auto locate = [&](int64_t tg) -> Tile {
         Tile T;
@@ -554,13 +560,12 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
         const int64_t sl = src.slot ? __builtin_amdgcn_readfirstlane(src.slot[g]) : g;
         T.x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
         T.n = __builtin_amdgcn_readfirstlane(src.n[g]);
-        T.px = (int64_t)pt * 16 + lj;
-        T.pxok = T.px < P;
+        T.px = pt * 16 + lj;
         return T;
     };
     // layer-1 input: lane l carries channel l/16 of pixel l%16
-    auto load_x = [&](const Tile& T) -> float { return T.pxok ? T.x[lg * P + T.px] : 0.f; };
-    const int nbranch = a.shift_c ? 2 : 1;
+    auto load_x = [&](const Tile& T) -> float { return T.px < P ? T.x[(int64_t)lg * P + T.px] : 0.f; };
+    constexpr int nbranch = GUIDED ? 2 : 1;
 
     Tile cur = locate(blockIdx.x);
     dma(res, 0, L::RES);
@@ -578,12 +583,13 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 
     for (int64_t tg = blockIdx.x; tg < ngroups; tg += gridDim.x) {
         const bool last_group = tg + gridDim.x >= ngroups;
-        const Tile nxt = locate(last_group ? tg : tg + gridDim.x);
-        const float xnx = load_x(nxt);
+        const int64_t tg_next = last_group ? tg : tg + gridDim.x;
         f4 eu = f4{0.f, 0.f, 0.f, 0.f};
+        float xnx = 0.f;
         for (int br = 0; br < nbranch; ++br) {
-            f4 acc[NO], u[NO];
-            // ---- layer 1: u = W1 x + shift (fp32 MFMA), from the resident fragments
+            f4 acc[NO], t[NO];
+            // ---- layer 1: t = kNegLog2e (W1 x + shift) (fp32 MFMA), from the
+            // resident fragments; the shift row holds kNegLog2e (b1 + e_n [+ Wc c])
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's shift row
             {
                 const float* a1 = reinterpret_cast<const float*>(res) + lane;
@@ -593,12 +599,13 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                     const f4 c1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[o * 64], xin, f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
                     const f4 sv = *reinterpret_cast<const f4*>(sh + 16 * o);
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) u[o][r] = __fadd_rn(c1[r], sv[r]);
+                    for (int r = 0; r < 4; ++r) t[o][r] = __builtin_fmaf(c1[r], kNegLog2e, sv[r]);
                 });
             }
-            int e = scale_of(u);
+            int e = scale_of(t);
             float invS = pow2(e - 11);
-            SplitB b = silu_split(u[0], u[1], invS);
+            float cS = kNegLog2e * invS;                  // exact: a power-of-two scaling
+            SplitB b = silu_split(t[0], t[1], cS);
 
             // ---- layers 2 and 3: one streamed slab per reduction chunk
             static_for<2>([&](auto lc) {
@@ -621,7 +628,7 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                         if (more) {
                             if constexpr (s + 2 == NS) {
                                 if (br + 1 < nbranch) dma_shift(cur.n, br + 1);
-                                else dma_shift(nxt.n, 0);
+                                else dma_shift(locate(tg_next).n, 0);
                             }
                             dma_slab(s + 2 - NS, nbuf);
                         }
@@ -637,7 +644,7 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                         constexpr int j = decltype(pc)::value;
                         Frag2 nxt2;
                         if constexpr (j + 1 < NO / 2) nxt2 = load2(fr + (2 * j + 2) * 128);
-                        if constexpr (c + 1 < KC && j < 5) silu_split_piece(j, u[2 * c + 2], u[2 * c + 3], invS, bn);
+                        if constexpr (c + 1 < KC && j < 5) silu_split_piece(j, t[2 * c + 2], t[2 * c + 3], cS, bn);
                         mac3x2(cur2, b, acc[2 * j], acc[2 * j + 1]);
                         // issue order inside the group: each MFMA followed by a
                         // fragment load and two VALU instructions, so that the
@@ -658,34 +665,37 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                         if constexpr (NO / 2 < 5) {          // fewer pairs than pieces
                             static_for<5>([&](auto qc) {
                                 if constexpr (decltype(qc)::value >= NO / 2)
-                                    silu_split_piece(decltype(qc)::value, u[2 * c + 2], u[2 * c + 3], invS, bn);
+                                    silu_split_piece(decltype(qc)::value, t[2 * c + 2], t[2 * c + 3], cS, bn);
                             });
                         }
                         b = bn;
                     }
                 });
-                // epilogue: u = acc / S + bias (an exact scaling, then the add)
-                const float cs = invS;
+                // epilogue: t = kNegLog2e (acc / S + bias) = acc (kNegLog2e / S) +
+                // kNegLog2e bias, the scaling exact, the bias row pre-multiplied
+                const float cs = cS;
                 const float* bias = vec + (NW + layer) * STRIDE + 4 * lg;
                 static_for<NO>([&](auto oc) {
                     constexpr int o = decltype(oc)::value;
                     const f4 bv = *reinterpret_cast<const f4*>(bias + 16 * o);
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) u[o][r] = __builtin_fmaf(acc[o][r], cs, bv[r]);
+                    for (int r = 0; r < 4; ++r) t[o][r] = __builtin_fmaf(acc[o][r], cs, bv[r]);
                 });
-                e = scale_of(u);
+                e = scale_of(t);
                 invS = pow2(e - 11);
-                b = silu_split(u[0], u[1], invS);
+                cS = kNegLog2e * invS;
+                b = silu_split(t[0], t[1], cS);
             });
 
             rot = (rot + NS) % 3;
+            if (br + 1 == nbranch) xnx = load_x(locate(tg_next));
             // ---- layer 4 (C outputs in one block, rows past C zero), resident fragments
             f4 o4 = f4{0.f, 0.f, 0.f, 0.f};
             {
                 const h8* f4r = res + L::L1 + lane;
                 static_for<KC>([&](auto cc) {
                     constexpr int c = decltype(cc)::value;
-                    if constexpr (c > 0) b = silu_split(u[2 * c], u[2 * c + 1], invS);
+                    if constexpr (c > 0) b = silu_split(t[2 * c], t[2 * c + 1], cS);
                     mac3(f4r + c * 128, b, o4);
                 });
             }
@@ -695,16 +705,18 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 #pragma unroll
                 for (int r = 0; r < C; ++r) {
                     const float v = __builtin_fmaf(o4[r], invS, a.b4[r]);
-                    if (br == 0) {
+                    const bool store = cur.active && cur.px < P;
+                    if constexpr (!GUIDED) {
+                        if (store) out[(int64_t)r * P + cur.px] = v;
+                    } else if (br == 0) {
                         eu[r] = v;
-                        if (nbranch == 1 && cur.active && cur.pxok) out[r * P + cur.px] = v;
-                    } else if (cur.active && cur.pxok) {
-                        out[r * P + cur.px] = eu[r] + a.guidance * (v - eu[r]);
+                    } else if (store) {
+                        out[(int64_t)r * P + cur.px] = eu[r] + a.guidance * (v - eu[r]);
                     }
                 }
             }
         }
-        cur = nxt;
+        cur = locate(tg_next);
         xin = xnx;
     }
 }
@@ -801,8 +813,12 @@ void launch_s_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s)
     if (ntiles == 0) return;
     int64_t blocks = (ntiles + 7) / 8;                       // persistent: one block per CU
     if (blocks > device_cus()) blocks = device_cus();
-    hipLaunchKernelGGL((k_conv_f32s<NB, C>), dim3((unsigned)blocks), dim3(512), 0, s, a, src, eps,
-                       tiles_per_row);
+    if (a.shift_c)
+        hipLaunchKernelGGL((k_conv_f32s<NB, C, true>), dim3((unsigned)blocks), dim3(512), 0, s, a, src, eps,
+                           tiles_per_row);
+    else
+        hipLaunchKernelGGL((k_conv_f32s<NB, C, false>), dim3((unsigned)blocks), dim3(512), 0, s, a, src, eps,
+                           tiles_per_row);
     PD_HIP(hipGetLastError());
 }
 

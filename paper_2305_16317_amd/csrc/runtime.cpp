@@ -470,7 +470,19 @@ static void create_denoiser(const pd_model_desc& m, const int64_t* shape, int32_
     std::vector<uint8_t> packed;
     conv_pack_weights(d.C, Wd, m.dtype == PD_BF16, W1, W2, W3, W4, packed);
     d.frags.upload(packed.data(), packed.size());
-    d.shift_u.upload(sh.data(), sh.size());
+    // the fp32 kernel's layer-1 shifts and biases b2, b3 are kept times kNegLog2e
+    const bool scaled = m.dtype != PD_BF16;
+    auto scale = [&](std::vector<float> v) {
+        if (scaled)
+            for (float& x : v) x *= kNegLog2e;
+        return v;
+    };
+    d.bias[1].upload(scale(std::vector<float>(w[3], w[3] + Wd)).data(), Wd);
+    d.bias[2].upload(scale(std::vector<float>(w[5], w[5] + Wd)).data(), Wd);
+    {
+        const std::vector<float> shs = scale(sh);
+        d.shift_u.upload(shs.data(), shs.size());
+    }
     if (m.cond_dim > 0) {
         const float* Wc = w[8];
         const float* c = w[9];
@@ -483,6 +495,7 @@ static void create_denoiser(const pd_model_desc& m, const int64_t* shape, int32_
         std::vector<float> shc(sh.size());
         for (int n = 0; n < Tt; ++n)
             for (int k = 0; k < Wd; ++k) shc[(size_t)n * Wd + k] = sh[(size_t)n * Wd + k] + wc[k];
+        shc = scale(std::move(shc));
         d.shift_c.upload(shc.data(), shc.size());
     }
 }
