@@ -39,8 +39,11 @@ __device__ __forceinline__ void static_for(F&& f) {
     static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-__device__ __forceinline__ float silu(float v) {
-    return v * __builtin_amdgcn_rcpf(1.0f + __expf(-v));
+// SiLU(u) from t = kNegLog2e u: e = 2^t = e^-u and SiLU(u) = u / (1 + e) =
+// t / ((1 + e) kNegLog2e), the constant cancelling exactly (the same float in
+// t and in the fused multiply-add)
+__device__ __forceinline__ float silu_t(float t) {
+    return t * __builtin_amdgcn_rcpf(__builtin_fmaf(__builtin_amdgcn_exp2f(t), kNegLog2e, kNegLog2e));
 }
 
 // Shift and bias vectors of the activations, staged in LDS: rows 0..NW-1 hold
@@ -138,8 +141,8 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                 (__attribute__((address_space(3))) void*)(dst + c * 256), 16, 0, 0);
         }
     };
-    // SiLU(acc + v) of block nb (v = LDS vector row vrow), rounded to bf16 and
-    // packed as the block's two B operands
+    // SiLU(acc + v) of block nb (v = LDS vector row vrow, held times
+    // kNegLog2e), rounded to bf16 and packed as the block's two B operands
     auto act = [&](const f16v& c, int vrow, int nb, bf8 (&hb)[2]) {
         int o = vrow * (AV::STRIDE / 4);
         asm volatile("" : "+s"(o));
@@ -147,7 +150,8 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
             constexpr int q4 = decltype(q4c)::value;
             const f4 sh = vec4[o + 8 * nb + 2 * q4 + half];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) hb[q4 / 2][4 * (q4 % 2) + q] = (__bf16)silu(c[4 * q4 + q] + sh[q]);
+            for (int q = 0; q < 4; ++q)
+                hb[q4 / 2][4 * (q4 % 2) + q] = (__bf16)silu_t(__builtin_fmaf(c[4 * q4 + q], kNegLog2e, sh[q]));
         });
         // pinned here: left to itself the compiler sinks the activation to the
         // slab that first reads it, keeping 16 fp32 accumulators live in place

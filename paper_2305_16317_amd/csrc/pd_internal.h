@@ -117,17 +117,16 @@ void launch_linear_dense(const LinearArgs& a, const float* x, const RowSrc& rows
                          hipStream_t s);
 
 // conv.hip: per-pixel 4-layer stack with fp32 or bf16 MFMA.
-// The fp32 kernel takes the argument of e^-u in base 2, t = kNegLog2e u, as its
-// working form of a pre-activation u: its layer-1 shifts and the biases b2, b3
-// are stored multiplied by kNegLog2e (float products); the bf16 kernel takes
-// them as they are.
+// The kernels take the argument of e^-u in base 2, t = kNegLog2e u, as their
+// working form of a pre-activation u: the layer-1 shifts and the biases b2, b3
+// are stored multiplied by kNegLog2e (float products).
 constexpr float kNegLog2e = -1.44269504f;     // -log2(e), rounded to float
 struct ConvArgs {
     const void* frags;      // packed weight fragments (layout in conv.hip)
-    const float* shift_u;   // [T_train][W] b1 + e_n (fp32: times kNegLog2e)
-    const float* shift_c;   // [T_train][W] b1 + e_n + Wc c (fp32: times kNegLog2e), or nullptr
-    const float* b2;        // [W] (fp32: times kNegLog2e)
-    const float* b3;        // [W] (fp32: times kNegLog2e)
+    const float* shift_u;   // [T_train][W] kNegLog2e (b1 + e_n)
+    const float* shift_c;   // [T_train][W] kNegLog2e (b1 + e_n + Wc c), or nullptr
+    const float* b2;        // [W] kNegLog2e b2
+    const float* b3;        // [W] kNegLog2e b3
     const float* b4;
     float guidance;
     int32_t C;              // channels

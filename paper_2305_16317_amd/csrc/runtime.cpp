@@ -470,11 +470,9 @@ static void create_denoiser(const pd_model_desc& m, const int64_t* shape, int32_
     std::vector<uint8_t> packed;
     conv_pack_weights(d.C, Wd, m.dtype == PD_BF16, W1, W2, W3, W4, packed);
     d.frags.upload(packed.data(), packed.size());
-    // the fp32 kernel's layer-1 shifts and biases b2, b3 are kept times kNegLog2e
-    const bool scaled = m.dtype != PD_BF16;
-    auto scale = [&](std::vector<float> v) {
-        if (scaled)
-            for (float& x : v) x *= kNegLog2e;
+    // the kernels take the layer-1 shifts and the biases b2, b3 times kNegLog2e
+    auto scale = [](std::vector<float> v) {
+        for (float& x : v) x *= kNegLog2e;
         return v;
     };
     d.bias[1].upload(scale(std::vector<float>(w[3], w[3] + Wd)).data(), Wd);
