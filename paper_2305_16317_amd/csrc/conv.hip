@@ -808,8 +808,6 @@ void pack_s_t(const float* W1, const float* W2, const float* W3, const float* W4
     }
 }
 
-int device_cus();
-
 template <int NB, int C>
 void launch_s_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s) {
     const int tiles_per_row = (int)((a.P + 15) / 16);
@@ -836,17 +834,6 @@ void launch_bf16_t(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t
     hipLaunchKernelGGL((k_conv_bf16<NB, C>), dim3((unsigned)blocks), dim3(kBf16Waves * 64), 0, s, a,
                        src, eps, tiles_per_row);
     PD_HIP(hipGetLastError());
-}
-
-int device_cus() {
-    static int cus = 0;
-    if (cus == 0) {
-        int dev = 0;
-        PD_HIP(hipGetDevice(&dev));
-        PD_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-        if (cus <= 0) cus = 256;
-    }
-    return cus;
 }
 
 #define PD_CONV_SHAPES(X) X(1, 4) X(2, 4) X(3, 4) X(4, 4) X(10, 4)

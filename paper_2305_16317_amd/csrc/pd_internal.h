@@ -21,6 +21,9 @@ struct Error {
 void hip_check(hipError_t e, const char* what);
 #define PD_HIP(call) ::pd::hip_check((call), #call)
 
+// compute units of the first device the library ran on (256 on MI355X)
+int device_cus();
+
 // ---------------------------------------------------------------- rows
 // Where the rows of one denoiser batch live.  Rows come in groups of `group`
 // consecutive rows (the samples of a batch at one trajectory point); group g
@@ -157,12 +160,15 @@ void launch_seq_heun_predict(const float* x, const float* eps, float A, float B,
 void launch_seq_heun_combine(float* eps, const float* eps2, int64_t n, hipStream_t s);
 void launch_seq_step_dpm(float* x, const float* eps, float* xp, float* ep, float P, float Q, float R,
                          float S, bool second, int64_t n, hipStream_t s);
-int picard_partial_blocks(int64_t D);
+// Blocks per sample of the scan (one column range each; the partial sums
+// come per block) and the columns each covers.
+int picard_partial_blocks(int64_t D, int batch);
+int picard_scan_cols(int64_t D, int batch);
 // Everything the stride rule and the slide need (the finalize step).
 struct FinalizeArgs {
     LoopState* st;
     LoopState* st_host;         // host copy of *st (mapped pinned memory), or nullptr
-    const float* partials;      // [batch][p][picard_partial_blocks(D)]
+    const float* partials;      // [batch][p][picard_partial_blocks(D, batch)]
     int32_t p, batch;
     int64_t D;
     int32_t T;

@@ -256,7 +256,8 @@ __global__ __launch_bounds__(1024) void k_picard_finalize(FinalizeArgs a, int nb
 }
 
 
-// One block: 64 * VEC consecutive columns of one sample b, all window rows,
+// One block: cpb <= 64 * VEC consecutive columns of one sample b (a multiple
+// of VEC, from picard_scan_cols), all window rows,
 // split over NW waves (rows [w*ch, (w+1)*ch) per wave, ch <= R).  Drift and
 // noise are summed along the rows inside each wave, the wave totals are
 // exchanged through LDS, and the new points x^{k+1}_{t+j+1} = x_t + sum y +
@@ -278,7 +279,7 @@ __global__ __launch_bounds__(NW * 64) void k_picard_scan(
     const float* __restrict__ noise, const float* __restrict__ Atab,
     const float* __restrict__ Btab, const float* __restrict__ Rtab,
     const float* __restrict__ Stab, int p, int batch, int64_t D, float* __restrict__ partials,
-    FinalizeArgs fin, int fuse_finalize) {
+    FinalizeArgs fin, int fuse_finalize, int cpb) {
     typedef typename Cols<VEC>::type V;
     const LoopState cur = *st;
     const int pe = cur.p_eff;
@@ -288,8 +289,10 @@ __global__ __launch_bounds__(NW * 64) void k_picard_scan(
     // it) in scalar registers
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int b = blockIdx.y, blk = blockIdx.x, nblk = gridDim.x;
-    const int64_t d = ((int64_t)blk * 64 + lane) * VEC;   // D is a multiple of VEC
-    const bool valid = d < D;
+    // lane l covers columns [blk cpb + l VEC, + VEC) of the block's cpb (D and
+    // cpb are multiples of VEC)
+    const int64_t d = (int64_t)blk * cpb + (int64_t)lane * VEC;
+    const bool valid = lane * VEC < cpb && d < D;
     const int64_t slotsz = (int64_t)batch * D;
     const int64_t col = (int64_t)b * D + (valid ? d : 0);
     const int P1 = fin.ring_slots;
@@ -535,8 +538,25 @@ __global__ __launch_bounds__(256) void k_seq_step(float* __restrict__ x,
 
 }  // namespace
 
-int picard_partial_blocks(int64_t D) {
-    const int64_t cols = 64 * (int64_t)scan_vec(D);
+// A block covers at most 64 lanes x VEC columns.  When the grid takes more
+// than one block, the columns are shared out evenly over the fewest rounds of
+// one block per compute unit that the 64-lane limit allows (a multiple of VEC
+// per block), so that no unit streams twice the data of another: at
+// 4x96x96 and one sample, 256 blocks of 144 columns instead of 144 of 256.
+int picard_scan_cols(int64_t D, int batch) {
+    const int vec = scan_vec(D);
+    const int64_t full = 64 * (int64_t)vec;
+    const int64_t blocks = (D + full - 1) / full * batch;
+    const int64_t cus = device_cus();
+    // one block keeps the fused finalize; a grid under half the units gains nothing
+    if (blocks <= 1 || 2 * blocks < cus) return (int)full;
+    const int64_t rounds = (blocks + cus - 1) / cus;
+    int64_t per = (D * batch + rounds * cus - 1) / (rounds * cus);   // columns per block
+    per = (per + vec - 1) / vec * vec;
+    return (int)(per < full ? per : full);
+}
+int picard_partial_blocks(int64_t D, int batch) {
+    const int64_t cols = picard_scan_cols(D, batch);
     return (int)((D + cols - 1) / cols);
 }
 
@@ -595,18 +615,19 @@ static bool launch_scan(const LoopState* st, float* ring, const float* eps, cons
                         const float* A, const float* B, const float* Rt, const float* St, int p,
                         int batch, int64_t D, float* partials, const FinalizeArgs& fin,
                         hipStream_t s) {
-    const dim3 grid((unsigned)picard_partial_blocks(D), (unsigned)batch);
+    const int cpb = picard_scan_cols(D, batch);
+    const dim3 grid((unsigned)picard_partial_blocks(D, batch), (unsigned)batch);
     const int fuse = grid.x * grid.y == 1;   // one block: the finalize works from LDS
     const dim3 block(NW * 64);
     if (Rt)      // DPM-Solver integrates the noise-free chain
         hipLaunchKernelGGL((k_picard_scan<NW, R, VEC, false, true>), grid, block, 0, s, st, ring, eps,
-                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse);
+                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse, cpb);
     else if (noise)
         hipLaunchKernelGGL((k_picard_scan<NW, R, VEC, true, false>), grid, block, 0, s, st, ring, eps,
-                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse);
+                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse, cpb);
     else
         hipLaunchKernelGGL((k_picard_scan<NW, R, VEC, false, false>), grid, block, 0, s, st, ring, eps,
-                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse);
+                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse, cpb);
     PD_HIP(hipGetLastError());
     return fuse != 0;
 }
@@ -634,7 +655,7 @@ bool launch_picard_scan(const LoopState* st, float* ring, const float* eps, cons
 
 void launch_picard_finalize(const FinalizeArgs& fin, hipStream_t s) {
     hipLaunchKernelGGL(k_picard_finalize, dim3(1), dim3(1024), 0, s, fin,
-                       picard_partial_blocks(fin.D));
+                       picard_partial_blocks(fin.D, fin.batch));
     PD_HIP(hipGetLastError());
 }
 

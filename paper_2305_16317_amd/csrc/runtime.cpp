@@ -149,6 +149,18 @@ int64_t product(const int64_t* shape, int32_t ndim) {
 }
 
 }  // namespace
+
+int device_cus() {
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0;
+        PD_HIP(hipGetDevice(&dev));
+        PD_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+        if (cus <= 0) cus = 256;
+    }
+    return cus;
+}
+
 }  // namespace pd
 
 using namespace pd;
@@ -670,7 +682,7 @@ static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, 
     w.state.alloc(sizeof(LoopState));
     w.slot.alloc(sizeof(int32_t) * (size_t)(p + hist));
     w.nrow.alloc(sizeof(int32_t) * (size_t)(p + hist));
-    w.partials.alloc(sizeof(float) * (size_t)picard_partial_blocks(d.D) * p * batch);
+    w.partials.alloc(sizeof(float) * (size_t)picard_partial_blocks(d.D, batch) * p * batch);
     if (s.heun) {
         w.xt.alloc(sizeof(float) * (size_t)p * BD);
         w.eps2.alloc(sizeof(float) * (size_t)p * BD);
