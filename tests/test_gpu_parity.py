@@ -299,6 +299,13 @@ SMALL = {
                                                 shape=(4, 10, 10), width=32, batch=3),
     "conv_ddim_p40_w320": lambda: W.small_variant("latent_ddim200_b4", T=60, p=40,
                                                   shape=(4, 8, 12), width=320, batch=2),
+    # grids wide enough for the scan to share the columns out evenly over the
+    # compute units: one 4x92x92 sample (249 blocks of 136 columns, the last
+    # ragged) and four 4x48x48 samples (64 blocks of 144 columns each)
+    "conv_even_split_b1": lambda: W.small_variant("latent_ddpm1000_p64", T=60, p=40,
+                                                  shape=(4, 92, 92), width=32),
+    "conv_even_split_b4": lambda: W.small_variant("latent_ddim200_b4", T=40, p=24,
+                                                  shape=(4, 48, 48), width=32, batch=4),
 }
 
 BF16 = {
