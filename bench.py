@@ -39,6 +39,19 @@ PEAK = {"f32": 157.3e12, "bf16": 2.5e15, "f16": 2.5e15}   # dense MFMA FLOP/s, M
 HBM_PEAK = 8.0e12                              # bytes/s
 
 
+def mlp_head_fused(wl) -> bool:
+    """The library runs the MLP's last layer inside the Picard update launch
+    (its epilogue is the update) for the Euler drift and windows of up to 128
+    points: the denoiser events then time the first three layers only."""
+    return (wl.model.kind == "mlp" and getattr(wl.schedule, "solver", "euler") == "euler"
+            and min(wl.p, wl.schedule.T) <= 128)
+
+
+def mlp_head_flops(model) -> float:
+    """FLOPs of the MLP's last layer for one network row."""
+    return 2.0 * model.width * model.D
+
+
 def flops_per_row(model) -> float:
     """Algorithmic matmul FLOPs of one network row (one full sample)."""
     if model.kind == "conv1x1":
@@ -108,7 +121,7 @@ def denoiser_roofline(wl, dtype: str, fl: float, seconds: float) -> dict:
     dense peak of the matrix-core instruction that executes them."""
     rate = fl / seconds if seconds > 0 else 0.0
     if wl.model.kind == "conv1x1" and dtype == "f32":
-        # the fp32 network's W x W layers run on v_mfma_f32_32x32x16_f16, three
+        # the fp32 network's layers 2-4 run on v_mfma_f32_16x16x32_f16, three
         # split products per multiply-add: the method's FLOPs are priced against
         # the fp16 peak; the products the matrix core executes (three per
         # FLOP, layers 1 and 4 counted alike) are reported beside it
@@ -125,7 +138,9 @@ def denoiser_roofline(wl, dtype: str, fl: float, seconds: float) -> dict:
             "flops": "method"}
 
 
-KERNEL_SOURCES = {"k_conv": ["conv.hip"], "k_picard": ["picard.hip"], "k_linear": ["mlp.hip"],
+KERNEL_SOURCES = {"k_conv": ["conv.hip"], "k_picard": ["picard.hip", "linear_tile.h"],
+                  "k_mlp_head": ["picard.hip", "linear_tile.h"],
+                  "k_linear": ["mlp.hip", "linear_tile.h"],
                   "k_gmm": ["gmm.hip"], "k_normals": ["rng.hip"]}
 
 
@@ -337,7 +352,9 @@ def main() -> int:
     upd_n = sum(st.kernel_times["update_launches"] for st in stats)
     fin_ms = sum(st.kernel_times["finalize_ms"] for st in stats)
     dtype = "bf16" if wl.model.dtype == "bf16" else "f32"
-    fl = flops_per_row(wl.model) * rows
+    head = mlp_head_fused(wl)
+    # with the fused head the denoiser events cover layers 1-3 only
+    fl = (flops_per_row(wl.model) - (mlp_head_flops(wl.model) if head else 0.0)) * rows
     has_noise = bool(np.any(sched.tables()["noise_std"] > 0))
     points = sum(window_points(st.trace, wl.p, wl.schedule.T) for st in stats)
     hist = (sum(history_rows(st.trace, wl.schedule.T) for st in stats)
@@ -369,14 +386,16 @@ def main() -> int:
         "evals_per_sample": [st.evals_per_sample for st in stats],
         "roofline": {**denoiser_roofline(wl, dtype, fl, den_ms * 1e-3),
                      "traffic": traffic, "kernel": kname,
-                     # the MLP's four layer launches are timed together, as one call
-                     "kernels_per_call": 4 if wl.model.kind == "mlp" else 1,
+                     # the MLP's layer launches are timed together, as one call
+                     "kernels_per_call": (3 if head else 4) if wl.model.kind == "mlp" else 1,
+                     **({"last_layer": "in the update launch (k_mlp_head_scan)"} if head else {}),
                      "flops_per_launch": fl / max(den_n, 1),
                      "mean_launch_ms": den_ms / max(den_n, 1), "launches": den_n},
         "roofline_update": {"bound": "hbm", "achieved": upd_rate / 1e9, "peak": HBM_PEAK / 1e9,
                             "unit": "GB/s", "frac": upd_rate / HBM_PEAK,
-                            "traffic": traffic_from_profiles(wl.name, "k_picard_scan"),
-                            "kernel": "k_picard_scan", "bytes_per_launch": ub / max(upd_n, 1),
+                            "traffic": traffic_from_profiles(wl.name, "k_mlp_head_scan" if head else "k_picard_scan"),
+                            "kernel": "k_mlp_head_scan" if head else "k_picard_scan",
+                            "bytes_per_launch": ub / max(upd_n, 1),
                             "mean_launch_us": 1e3 * upd_ms / max(upd_n, 1), "launches": upd_n,
                             "finalize_mean_us": 1e3 * fin_ms / max(upd_n, 1)},
         "time_split_ms_per_step": {"denoiser": den_ms / a.steps, "update": upd_ms / a.steps,

@@ -258,6 +258,10 @@ typedef struct pd_sample_stats {
     double update_ms;          /* out: summed event time of the update launches        */
     double finalize_ms;        /* out: summed event time of the finalize launches      */
 } pd_sample_stats;
+/* With the MLP denoiser and the Euler drift (PD_DDPM, PD_DDIM) ParaDiGMS runs
+ * the network's last layer inside the update launch, whose epilogue is the
+ * Picard update, error and stride step: denoiser_ms then times the first three
+ * layers, update_ms that fused launch, and finalize_launches is 0. */
 
 typedef struct pd_workspace pd_workspace;
 

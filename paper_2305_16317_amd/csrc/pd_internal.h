@@ -194,6 +194,28 @@ bool launch_picard_scan(const LoopState* st, float* ring, const float* eps, cons
                         int batch, int64_t D, float* partials, const FinalizeArgs& fin,
                         hipStream_t s);
 void launch_picard_finalize(const FinalizeArgs& fin, hipStream_t s);
+// The MLP's last layer fused with the Picard update, error and finalize (Euler
+// drift, no history row): one launch in place of the last layer, the scan and
+// the finalize step.  partials holds [batch][p][n_slabs]; count holds
+// n_slabs + 1 ints, zero between launches.
+struct HeadScanArgs {
+    LinearArgs l4;          // the last layer: W4 [D][W], b4, no activation
+    const float* h;         // [rows][W] the third layer's output
+    RowSrc rows;            // the window's rows (the layer's row count)
+    const LoopState* st;
+    float* ring;
+    float* eps;             // [rows][D] epsilon, written and read back
+    const float* noise;     // [T][batch][D] or nullptr
+    const float* A;
+    const float* B;
+    int32_t batch;
+    int64_t D;
+    float* partials;
+    int32_t* count;
+    int32_t n_slabs;        // 16-column slabs, ceil(D / 16)
+};
+bool mlp_head_scan_fits(int p);
+void launch_mlp_head_scan(const HeadScanArgs& a, const FinalizeArgs& fin, hipStream_t s);
 void launch_seq_step(float* x, const float* eps, const float* z, float A, float B, int64_t n,
                      hipStream_t s);
 

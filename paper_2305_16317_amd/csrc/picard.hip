@@ -12,6 +12,7 @@
 // copies the state into mapped host memory for the host's batch decisions.
 #include <type_traits>
 
+#include "linear_tile.h"
 #include "pd_internal.h"
 
 namespace pd {
@@ -253,6 +254,133 @@ __device__ void finalize_body(const FinalizeArgs& a, int nblk, const LoopState& 
 __global__ __launch_bounds__(1024) void k_picard_finalize(FinalizeArgs a, int nblk) {
     const LoopState cur = *a.st;
     finalize_body(a, nblk, cur);
+}
+
+// The MLP's last layer with the Picard update as its epilogue (Euler drift,
+// windows of up to kHeadGroups * kHeadRows points).  Each block computes one
+// 16 x 16 tile of epsilon exactly as the layer kernel does (linear_tile), then
+// counts itself in on its 16-column slab; the slab's last block, which then
+// sees every window row of those columns, rebuilds them: drift, running sums
+// of drift and noise, new points, and the per-offset squared differences
+// summed over its 16 columns into partials[b][o][slab] (offset 0 carries the
+// count of non-finite points in the window's last row, as in the scan
+// kernel).  The last slab to finish applies the stride rule and slides the
+// window (finalize_body).  Nothing waits: a block that is not last returns,
+// and a counter is reset by the block that completes it (count_in).  p_eff
+// never grows from one iteration to the next, so a block that
+// starts after the slide still finds itself past the window and returns.
+constexpr int kHeadGroups = kLinWaves * 4;   // 16-lane row groups of the block
+
+// Counts the block in on *cnt, which completes at n arrivals.  Each wave waits
+// for its own global stores to reach L2; after the barrier one thread makes the
+// block's stores visible device-wide (one L2 write-back per block, not per
+// wave) and counts.  The block that completes the count resets it, invalidates
+// its caches (so it reads what every counted block stored) and returns true;
+// every other block returns false.
+__device__ bool count_in(int32_t* cnt, int n) {
+    __shared__ int s_flag;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        const int last = atomicAdd(cnt, 1) == n - 1;
+        if (last) {
+            atomicExch(cnt, 0);                  // where the next launch's arrivals count
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        }
+        s_flag = last;
+    }
+    __syncthreads();
+    return s_flag != 0;
+}
+constexpr int kHeadRows = 4;                 // window rows per group
+static_assert(kHeadGroups * kHeadRows >= kMaxWindow, "the head covers every window size");
+
+template <bool NOISE>
+__global__ __launch_bounds__(kLinWaves * 64) void k_mlp_head_scan(HeadScanArgs a, FinalizeArgs fin) {
+    const LoopState cur = *a.st;
+    const int pe = cur.p_eff;
+    if (pe <= 0) return;
+    const int B = a.batch;
+    const int M = pe * B;                        // rows (window point, sample)
+    const int slab = blockIdx.x, m0 = blockIdx.y * 16, n0 = slab * 16;
+    if (m0 >= M) return;                         // uniform over the block
+    linear_tile<false>(a.l4, a.h, a.rows, 0, a.eps, M, m0, n0);
+
+    // the slab's last block rebuilds its columns from every block's epsilon
+    if (!count_in(&a.count[slab], (M + 15) / 16)) return;
+
+    const int t = cur.t, f = cur.f, P1 = fin.ring_slots;
+    const int64_t D = a.D, BD = (int64_t)B * D;
+    const int c = threadIdx.x & 15, g = threadIdx.x >> 4;
+    const int ch = (pe + kHeadGroups - 1) / kHeadGroups;          // rows per group
+    const int j0 = min(g * ch, pe), nr = min(j0 + ch, pe) - j0;
+    const int64_t d = n0 + c;
+    const bool valid = d < D;
+    const int64_t dc = valid ? d : 0;
+    __shared__ float s_tot[2][kHeadGroups][16], s_first[kHeadGroups][16];
+    for (int b = 0; b < B; ++b) {
+        const int64_t col = (int64_t)b * D + dc;
+        // every read of the ring comes before the first barrier; the writes
+        // all after it (the ring slots overlap)
+        const float anchor = a.ring[(int64_t)(t % P1) * BD + col];
+        float xo[kHeadRows], y[kHeadRows], z[kHeadRows];
+#pragma unroll
+        for (int r = 0; r < kHeadRows; ++r) {
+            const int j = min(j0 + r, pe - 1);        // clamped: always a window row
+            const int m = t + j;
+            const int sl = m <= f ? m % P1 : f % P1;  // points past f equal x_f
+            xo[r] = a.ring[(int64_t)sl * BD + col];
+            const float e = a.eps[((int64_t)j * B + b) * D + dc];
+            y[r] = drift(a.A[m], xo[r], a.B[m], e);
+            z[r] = NOISE ? a.noise[(int64_t)m * BD + col] : 0.f;
+            if (r >= nr) y[r] = z[r] = 0.f;           // rows past the group's range
+        }
+        float ty = 0.f, tz = 0.f;
+#pragma unroll
+        for (int r = 0; r < kHeadRows; ++r) {
+            ty = __fadd_rn(ty, y[r]);
+            tz = __fadd_rn(tz, z[r]);
+        }
+        s_tot[0][g][c] = ty;
+        s_tot[1][g][c] = tz;
+        s_first[g][c] = xo[0];                        // x^k_{t+j0}: the previous group's next old point
+        __syncthreads();
+        float py = 0.f, pz = 0.f;
+        for (int v = 0; v < g; ++v) {
+            py = __fadd_rn(py, s_tot[0][v][c]);
+            pz = __fadd_rn(pz, s_tot[1][v][c]);
+        }
+        const float next_old = g + 1 < kHeadGroups ? s_first[g + 1][c] : 0.f;
+        float sy = 0.f, sz = 0.f;
+#pragma unroll
+        for (int r = 0; r < kHeadRows; ++r) {
+            const int j = j0 + r;
+            const bool in = r < nr;
+            sy = __fadd_rn(sy, y[r]);
+            sz = __fadd_rn(sz, z[r]);
+            const float v = __fadd_rn(__fadd_rn(anchor, __fadd_rn(py, sy)), __fadd_rn(pz, sz));
+            // error of window offset o = j + 1: x^{k+1}_{t+j+1} against x^k_{t+j+1}
+            const float xold = (r + 1 < kHeadRows && r + 1 < nr) ? xo[r + 1 < kHeadRows ? r + 1 : r] : next_old;
+            float e2;
+            if (j + 1 < pe) {
+                const float dl = __fsub_rn(v, xold);
+                e2 = dl * dl;
+            } else {
+                e2 = isfinite(v) ? 0.f : 1.f;         // last row: count non-finite points
+            }
+            e2 = (in && valid) ? e2 : 0.f;
+            if (in && valid) a.ring[(int64_t)((t + j + 1) % P1) * BD + (int64_t)b * D + d] = v;
+            const float s16 = group_sum<16>(e2);      // the slab's 16 columns
+            if (in && c == 0)
+                a.partials[((int64_t)b * fin.p + (j + 1 < pe ? j + 1 : 0)) * a.n_slabs + slab] = s16;
+        }
+        __syncthreads();                              // LDS reuse by the next sample
+    }
+
+    // the last slab to finish applies the stride rule to every slab's partials
+    if (!count_in(&a.count[a.n_slabs], a.n_slabs)) return;
+    finalize_body(fin, a.n_slabs, cur);
 }
 
 
@@ -651,6 +779,21 @@ bool launch_picard_scan(const LoopState* st, float* ring, const float* eps, cons
     if (ch <= 4) PD_SCAN(8, 4)
     PD_SCAN(8, 8)
 #undef PD_SCAN
+}
+
+bool mlp_head_scan_fits(int p) { return p >= 1 && p <= kMaxWindow; }
+
+void launch_mlp_head_scan(const HeadScanArgs& a, const FinalizeArgs& fin, hipStream_t s) {
+    if (!mlp_head_scan_fits(fin.p)) fail(PD_ERR_UNSUPPORTED, "window larger than the fused head takes");
+    if ((a.l4.K % 4) != 0) fail(PD_ERR_UNSUPPORTED, "mlp layer sizes must be multiples of 4");
+    if (a.n_slabs != (int)((a.D + 15) / 16) || fin.history || fin.nrow2)
+        fail(PD_ERR_INVALID_ARG, "fused head: slab count or drift kind mismatch");
+    const dim3 grid((unsigned)a.n_slabs, (unsigned)(((int64_t)fin.p * a.batch + 15) / 16));
+    if (a.noise)
+        hipLaunchKernelGGL(k_mlp_head_scan<true>, grid, dim3(kLinWaves * 64), 0, s, a, fin);
+    else
+        hipLaunchKernelGGL(k_mlp_head_scan<false>, grid, dim3(kLinWaves * 64), 0, s, a, fin);
+    PD_HIP(hipGetLastError());
 }
 
 void launch_picard_finalize(const FinalizeArgs& fin, hipStream_t s) {

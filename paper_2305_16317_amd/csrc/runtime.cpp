@@ -365,26 +365,34 @@ struct pd_denoiser {
         return desc.kind == PD_MODEL_MLP ? (size_t)(2 * rows * desc.width) : 0;
     }
 
+    // MLP: the first three layers through scratch (2 * rows * width floats);
+    // returns the third layer's output, the last layer's input
+    const float* mlp_trunk(const RowSrc& src, float* scratch, hipStream_t s) const {
+        const int Wd = desc.width;
+        const int64_t rows = (int64_t)src.max_groups * src.group;
+        float* h1 = scratch;
+        float* h2 = scratch + rows * Wd;
+        LinearArgs l1{W[0].as<float>(), nullptr, shift1.as<float>(), (int)D, Wd, ACT_GELU};
+        LinearArgs l2{W[1].as<float>(), bias[1].as<float>(), nullptr, Wd, Wd, ACT_GELU};
+        LinearArgs l3{W[2].as<float>(), bias[2].as<float>(), nullptr, Wd, Wd, ACT_GELU};
+        launch_linear_gather(l1, src, D, h1, s);
+        launch_linear_dense(l2, h1, src, h2, s);
+        launch_linear_dense(l3, h2, src, h1, s);
+        return h1;
+    }
+    // MLP: the last layer (no activation)
+    LinearArgs mlp_head() const {
+        return LinearArgs{W[3].as<float>(), bias[3].as<float>(), nullptr, desc.width, (int)D, ACT_NONE};
+    }
+
     void forward(const RowSrc& src, float* eps, float* scratch, hipStream_t s) const {
         switch (desc.kind) {
             case PD_MODEL_GMM2D:
                 launch_gmm_eps(gmm(), src, eps, s);
                 break;
-            case PD_MODEL_MLP: {
-                const int Wd = desc.width;
-                const int64_t rows = (int64_t)src.max_groups * src.group;
-                float* h1 = scratch;
-                float* h2 = scratch + rows * Wd;
-                LinearArgs l1{W[0].as<float>(), nullptr, shift1.as<float>(), (int)D, Wd, ACT_GELU};
-                LinearArgs l2{W[1].as<float>(), bias[1].as<float>(), nullptr, Wd, Wd, ACT_GELU};
-                LinearArgs l3{W[2].as<float>(), bias[2].as<float>(), nullptr, Wd, Wd, ACT_GELU};
-                LinearArgs l4{W[3].as<float>(), bias[3].as<float>(), nullptr, Wd, (int)D, ACT_NONE};
-                launch_linear_gather(l1, src, D, h1, s);
-                launch_linear_dense(l2, h1, src, h2, s);
-                launch_linear_dense(l3, h2, src, h1, s);
-                launch_linear_dense(l4, h1, src, eps, s);
+            case PD_MODEL_MLP:
+                launch_linear_dense(mlp_head(), mlp_trunk(src, scratch, s), src, eps, s);
                 break;
-            }
             case PD_MODEL_CONV1X1: {
                 ConvArgs a{frags.p,           shift_u.as<float>(),
                            guided() ? shift_c.as<float>() : nullptr,
@@ -634,6 +642,7 @@ struct pd_workspace {
     DevBuf ring, eps, noise, A, B, zstd, tolv, model_t, state, slot, nrow, partials, scratch;
     DevBuf xt, eps2, model_t_next, nrow2;   // Heun: predictions, second epsilons, n_{i+1}
     DevBuf Rt, St, xprev, eprev;            // multistep: tables; the sequential loop's last step
+    DevBuf head_count;                      // fused MLP head: arrival counters per slab, + 1
     int ring_slots() const { return p + 1 + (s->dpm ? 1 : 0); }
     // mapped, coherent pinned host memory that the kernels write directly:
     // the loop state's host copy and the stride of every iteration
@@ -656,6 +665,13 @@ static void host_mapped(T** host, T** dev, size_t count) {
     std::memset(*host, 0, sizeof(T) * count);
     PD_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(dev), *host, 0));
 }
+
+// The MLP's last layer runs as the Picard update's prologue (one launch for
+// the layer, the update and the stride) when the drift is the Euler step.
+static bool use_mlp_head(const pd_schedule& s, const pd_denoiser& d, int p) {
+    return d.desc.kind == PD_MODEL_MLP && !s.heun && !s.dpm && mlp_head_scan_fits(p);
+}
+static int head_slabs(int64_t D) { return (int)((D + 15) / 16); }
 
 static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, int batch,
                              pd_workspace& w) {
@@ -682,7 +698,14 @@ static void create_workspace(const pd_schedule& s, const pd_denoiser& d, int p, 
     w.state.alloc(sizeof(LoopState));
     w.slot.alloc(sizeof(int32_t) * (size_t)(p + hist));
     w.nrow.alloc(sizeof(int32_t) * (size_t)(p + hist));
-    w.partials.alloc(sizeof(float) * (size_t)picard_partial_blocks(d.D, batch) * p * batch);
+    const bool head = use_mlp_head(s, d, p);
+    int nblk = picard_partial_blocks(d.D, batch);
+    if (head && head_slabs(d.D) > nblk) nblk = head_slabs(d.D);
+    w.partials.alloc(sizeof(float) * (size_t)nblk * p * batch);
+    if (head) {
+        w.head_count.alloc(sizeof(int32_t) * (size_t)(head_slabs(d.D) + 1));
+        PD_HIP(hipMemset(w.head_count.p, 0, w.head_count.bytes));
+    }
     if (s.heun) {
         w.xt.alloc(sizeof(float) * (size_t)p * BD);
         w.eps2.alloc(sizeof(float) * (size_t)p * BD);
@@ -937,6 +960,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                                w.model_t.as<int32_t>(), w.h_trace_dev, w.slot.as<int32_t>(),
                                w.nrow.as<int32_t>(), mtn, nrow2, slots, hist};
         const float* xT = w.ring.as<float>() + (int64_t)(T % slots) * BD;
+        const bool head = use_mlp_head(*s, *d, pc);
         const RowSrc src{w.ring.as<float>(), w.slot.as<int32_t>(), BD,     batch,
                          pc + hist,          w.nrow.as<int32_t>(), &dst->nrows};
         // The kernels write the loop state into host memory as they go, so
@@ -975,6 +999,18 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                 tm.mark(-1);
                 for (int it = 0; it < need; ++it) {
                     if (it == need - 1) PD_HIP(hipEventRecord(w.batch_event, st));
+                    if (head) {
+                        // the last layer with the update, error, stride and slide
+                        const float* h = d->mlp_trunk(src, w.scratch.as<float>(), st);
+                        tm.mark(CAT_DENOISER);
+                        const HeadScanArgs ha{d->mlp_head(), h, src, dst, w.ring.as<float>(),
+                                              w.eps.as<float>(), w.noise.as<float>(), w.A.as<float>(),
+                                              w.B.as<float>(), batch, d->D, w.partials.as<float>(),
+                                              w.head_count.as<int32_t>(), head_slabs(d->D)};
+                        launch_mlp_head_scan(ha, fin, st);
+                        tm.mark(CAT_UPDATE);
+                        continue;
+                    }
                     d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
                     if (s->heun) {   // second evaluation at every row's Euler prediction
                         launch_heun_predict(dst, w.ring.as<float>(), w.eps.as<float>(),
