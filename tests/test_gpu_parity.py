@@ -377,8 +377,12 @@ def test_window_of_one_is_sequential_bitwise(name):
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
 
 
-def test_runs_are_deterministic_and_workspace_reuse():
-    wl = SMALL["conv_ddpm"]()
+@pytest.mark.parametrize("name", ["conv_ddpm", "mlp_b8", "mlp_full"])
+def test_runs_are_deterministic_and_workspace_reuse(name):
+    """Two runs are bitwise equal, and so is a run on a workspace that served
+    another seed first (for the MLP this also checks that the fused last
+    layer's arrival counters are back at zero after every call)."""
+    wl = SMALL[name]()
     w = W.make_weights(wl.model)
     a, sa = _run(wl, w)
     b, sb = _run(wl, w)
@@ -386,11 +390,11 @@ def test_runs_are_deterministic_and_workspace_reuse():
     sched, den = pd.from_workload(wl, w)
     ws = pd.pd_workspace_create(sched, den, wl.p, wl.batch)
     for seed in (5, 0):
-        x = torch.empty(wl.model.D, device="cuda")
-        st = pd.pd_sample_picard(sched, den, wl.p, wl.tau, seed, 1, wl.model.sample_shape, x,
-                                 workspace=ws)
+        x = torch.empty(wl.batch * wl.model.D, device="cuda")
+        st = pd.pd_sample_picard(sched, den, wl.p, wl.tau, seed, wl.batch, wl.model.sample_shape,
+                                 x, workspace=ws)
         torch.cuda.synchronize()
-    assert np.array_equal(x.cpu().numpy().reshape(1, -1).view(np.uint32), a.view(np.uint32))
+    assert np.array_equal(x.cpu().numpy().reshape(a.shape).view(np.uint32), a.view(np.uint32))
     assert st == sa
 
 
