@@ -310,7 +310,7 @@ def main() -> int:
     a = ap.parse_args()
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only: --gpus {a.gpus} is not supported "
-              "(the window is not split across GPUs in this build)", file=sys.stderr)
+              "(the library runs on one GPU and does not split the window across GPUs)", file=sys.stderr)
         return 2
     if a.sweep:
         return sweep(a)

@@ -46,7 +46,7 @@ typedef int32_t pd_status;
 #define PD_ERR_OOM 2           /* device or host allocation failed                  */
 #define PD_ERR_DEVICE 3        /* no usable GPU, or a HIP call failed               */
 #define PD_ERR_NUMERIC 4       /* a trajectory point or error became non-finite     */
-#define PD_ERR_UNSUPPORTED 5   /* a valid request this build does not implement     */
+#define PD_ERR_UNSUPPORTED 5   /* a valid request the library does not implement     */
 
 /* Last error message of the calling thread ("" if none). */
 const char* pd_last_error(void);

@@ -2,10 +2,10 @@
 
 TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import this.
 
-Algorithm 1 draws the prior point and every step's noise up front ("sample
-the noise ahead of time", Sec. 3.1 and the first lines of Algorithm 1).  The
-paper does not name a generator; this build fixes a counter-based one so the
-oracle and the device can draw the *same* numbers independently:
+Algorithm 1 draws the prior point and every step's noise up front, before
+the first iteration (Sec. 3.1 and the setup of Algorithm 1).  The paper does
+not name a generator; the oracle and the library fix a counter-based one so
+that both draw the *same* numbers independently:
 
 * Philox4x32-10 as defined by Salmon, Moraes, Dror and Shaw, "Parallel Random
   Numbers: As Easy as 1, 2, 3" (SC'11): a 128-bit counter, a 64-bit key, ten
