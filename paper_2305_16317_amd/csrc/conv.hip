@@ -328,9 +328,12 @@ __device__ __forceinline__ float pow2(int k) { return __builtin_bit_cast(float, 
 // in one fused multiply-add (the scaling exact, the bias row pre-multiplied).
 // SiLU and the split fuse: with e = 2^t and r = 1 / ((1 + e) kNegLog2e / S)
 // (one fused multiply-add for the product, the scale an exact power of two),
-// t r = S u / (1 + e) = hs, formed exactly inside v_fma_mix: x0s = fp16(t r)
-// and x1 = fp16(t r - x0s) each round once.  The next layer's accumulator
-// holds S (W h).
+// t r = S u / (1 + e) = hs.  x0s = fp16(fl(t r)) (v_cvt_pk_f16_f32, two values
+// per instruction, nearest even), the remainder t r - x0s is formed exactly and
+// rounded once to fp32 (v_fma_mix_f32, the fp16 operand read in place), and
+// x1 = fp16 of it; both fp16 roundings are the half-rate conversions, not the
+// quarter-rate fp16-result v_fma_mix.  The next layer's accumulator holds
+// S (W h).
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 
 template <int NB, int C>
@@ -353,24 +356,30 @@ struct LayoutS {                                  // units of 16 B (one lane's o
 struct SplitB {
     u4v p0, p1, p2;
 };
-__device__ __forceinline__ void silu_split_q(const float v0, const float v1, float c,
-                                             uint32_t& x0s, uint32_t& x1) {
-    // e = 2^t = e^-u and r = 1 / ((1 + e) c): the fused multiply-add forms
-    // (1 + e) c with one rounding, and t r = S u / (1 + e) = S SiLU(u) since
-    // the same float constant kNegLog2e is in t and in c
-    const float e0 = __builtin_amdgcn_exp2f(v0);
-    const float e1 = __builtin_amdgcn_exp2f(v1);
-    const float r0 = __builtin_amdgcn_rcpf(__builtin_fmaf(e0, c, c));
-    const float r1 = __builtin_amdgcn_rcpf(__builtin_fmaf(e1, c, c));
+// stage 1 of two inputs: e = 2^t = e^-u and r = 1 / ((1 + e) c); the fused
+// multiply-add forms (1 + e) c with one rounding, and t r = S u / (1 + e) =
+// S SiLU(u) since the same float constant kNegLog2e is in t and in c
+struct SplitR { float r0, r1; };
+__device__ __forceinline__ SplitR silu_r(const float v0, const float v1, float c) {
+    return {__builtin_amdgcn_rcpf(__builtin_fmaf(__builtin_amdgcn_exp2f(v0), c, c)),
+            __builtin_amdgcn_rcpf(__builtin_fmaf(__builtin_amdgcn_exp2f(v1), c, c))};
+}
+// stage 2: x0s = fp16(fl(t r)) and x1 = fp16(t r - x0s), two halves each
+__device__ __forceinline__ void split_round(const float v0, const float v1, const SplitR& r,
+                                            uint32_t& x0s, uint32_t& x1) {
+    const float h0 = v0 * r.r0, h1 = v1 * r.r1;
     uint32_t a, b;
-    asm("v_fma_mixlo_f16 %0, %1, %2, 0\n\t"
-        "v_fma_mixhi_f16 %0, %3, %4, 0"
-        : "=&v"(a) : "v"(v0), "v"(r0), "v"(v1), "v"(r1));
-    asm("v_fma_mixlo_f16 %0, %1, %2, -%5 op_sel_hi:[0,0,1]\n\t"
-        "v_fma_mixhi_f16 %0, %3, %4, -%5 op_sel:[0,0,1] op_sel_hi:[0,0,1]"
-        : "=&v"(b) : "v"(v0), "v"(r0), "v"(v1), "v"(r1), "v"(a));
+    float d0, d1;
+    asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(a) : "v"(h0), "v"(h1));
+    asm("v_fma_mix_f32 %0, %1, %2, -%3 op_sel_hi:[0,0,1]" : "=v"(d0) : "v"(v0), "v"(r.r0), "v"(a));
+    asm("v_fma_mix_f32 %0, %1, %2, -%3 op_sel:[0,0,1] op_sel_hi:[0,0,1]" : "=v"(d1) : "v"(v1), "v"(r.r1), "v"(a));
+    asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(b) : "v"(d0), "v"(d1));
     x0s = a;
     x1 = b;
+}
+__device__ __forceinline__ void silu_split_q(const float v0, const float v1, float c,
+                                             uint32_t& x0s, uint32_t& x1) {
+    split_round(v0, v1, silu_r(v0, v1, c), x0s, x1);
 }
 __device__ __forceinline__ float f4_at(const f4& ua, const f4& ub, int i) { return i < 4 ? ua[i] : ub[i - 4]; }
 __device__ __forceinline__ void silu_split_piece(int q, const f4& ua, const f4& ub, float c, SplitB& s) {
@@ -379,6 +388,25 @@ __device__ __forceinline__ void silu_split_piece(int q, const f4& ua, const f4& 
         silu_split_q(f4_at(ua, ub, 2 * q), f4_at(ua, ub, 2 * q + 1), c, a, b);
         s.p0[q] = a;
         s.p1[q] = b;
+    } else {                                         // x0 = x0s 2^-11
+        s.p2 = __builtin_bit_cast(u4v, __builtin_bit_cast(h8, s.p0) * (_Float16)0.00048828125f);
+    }
+}
+// the same work in nine steps of about six vector instructions, to spread
+// between MFMA groups: step 2q is stage 1 of inputs 2q, 2q + 1, step 2q + 1
+// their stage 2, step 8 forms x0
+__device__ __forceinline__ void silu_split_step(int k, const f4& ua, const f4& ub, float c, SplitB& s, SplitR& st) {
+    if (k < 8) {
+        const int q = k >> 1;
+        const float v0 = f4_at(ua, ub, 2 * q), v1 = f4_at(ua, ub, 2 * q + 1);
+        if ((k & 1) == 0) {
+            st = silu_r(v0, v1, c);
+        } else {
+            uint32_t a, b;
+            split_round(v0, v1, st, a, b);
+            s.p0[q] = a;
+            s.p1[q] = b;
+        }
     } else {                                         // x0 = x0s 2^-11
         s.p2 = __builtin_bit_cast(u4v, __builtin_bit_cast(h8, s.p0) * (_Float16)0.00048828125f);
     }
@@ -638,38 +666,40 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                         }
                     }
                     // software pipeline: the fragments of pair j + 1 are loaded and
-                    // a fifth of the next chunk's SiLU and split is done before the
-                    // six MFMAs of pair j (the order is fixed: the scheduler keeps
-                    // the loads ahead of the products they feed)
+                    // one of the nine steps of the next chunk's SiLU and split is
+                    // done before the six MFMAs of pair j (the order is fixed: the
+                    // scheduler keeps the loads ahead of the products they feed)
                     SplitB bn;
+                    SplitR sr;
                     const h8* fr = slab_buf(buf) + lane;
                     Frag2 cur2 = load2(fr);
                     static_for<NO / 2>([&](auto pc) {
                         constexpr int j = decltype(pc)::value;
                         Frag2 nxt2;
                         if constexpr (j + 1 < NO / 2) nxt2 = load2(fr + (2 * j + 2) * 128);
-                        if constexpr (c + 1 < KC && j < 5) silu_split_piece(j, t[2 * c + 2], t[2 * c + 3], cS, bn);
+                        if constexpr (c + 1 < KC && j < 9) silu_split_step(j, t[2 * c + 2], t[2 * c + 3], cS, bn, sr);
                         mac3x2(cur2, b, acc[2 * j], acc[2 * j + 1]);
                         // issue order inside the group: each MFMA followed by a
-                        // fragment load and two VALU instructions, so that the
-                        // SiLU chain's latency sits under the products
+                        // fragment load and one VALU instruction (a vector
+                        // instruction beside each matrix one hides behind it; more
+                        // than two per MFMA largely serialise with them)
                         static_for<4>([&](auto) {
                             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
                             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
-                            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);   // VALU
+                            __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);   // VALU
                         });
                         static_for<2>([&](auto) {
                             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                            __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                            __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
                         });
                         __builtin_amdgcn_sched_barrier(0);
                         if constexpr (j + 1 < NO / 2) cur2 = nxt2;
                     });
                     if constexpr (c + 1 < KC) {
-                        if constexpr (NO / 2 < 5) {          // fewer pairs than pieces
-                            static_for<5>([&](auto qc) {
+                        if constexpr (NO / 2 < 9) {          // fewer pairs than steps
+                            static_for<9>([&](auto qc) {
                                 if constexpr (decltype(qc)::value >= NO / 2)
-                                    silu_split_piece(decltype(qc)::value, t[2 * c + 2], t[2 * c + 3], cS, bn);
+                                    silu_split_step(decltype(qc)::value, t[2 * c + 2], t[2 * c + 3], cS, bn, sr);
                             });
                         }
                         b = bn;
