@@ -649,11 +649,14 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
                     const int buf = (rot + s) % 3;
                     // slab s has landed (at s = 0 everything has: slabs 0 and 1 were
                     // copied during the previous pass); the buffer of slab s - 1
-                    // is free for slab s + 2
+                    // is free for slab s + 2.  Only the copies of slab s + 1 may
+                    // still be in flight; after the last slab of the last pass
+                    // none were issued, so nothing may be
+                    const bool more = br + 1 < nbranch || !last_group;
                     if constexpr (s == 0) land();
+                    else if constexpr (s + 1 == NS) { if (more) land_but_next(); else land(); }
                     else land_but_next();
                     const int nbuf = (rot + s + 2) % 3;
-                    const bool more = br + 1 < nbranch || !last_group;
                     if constexpr (s + 2 < NS) {
                         dma_slab(s + 2, nbuf);
                     } else {                                 // the next pass's slabs 0 and 1
