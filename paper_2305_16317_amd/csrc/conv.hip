@@ -294,6 +294,26 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
 // ---------------------------------------------------------------- fp32
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 
+// Largest value over the wave, the same in every lane: DPP steps build the
+// maximum of each 16-lane row in every lane of it (pairs, quads, half rows,
+// rows), two row broadcasts carry it into the last row, and lane 63 is read.
+// Maximum is exact, so any order of the steps gives the same value.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_max_step(float m) {
+    // lanes outside ROW_MASK keep their own value
+    const int v = __builtin_bit_cast(int, m);
+    return __builtin_fmaxf(m, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(v, v, CTRL, ROW_MASK, 0xf, false)));
+}
+__device__ __forceinline__ float wave_max_dpp(float m) {
+    m = dpp_max_step<0xb1, 0xf>(m);    // quad_perm [1,0,3,2]
+    m = dpp_max_step<0x4e, 0xf>(m);    // quad_perm [2,3,0,1]
+    m = dpp_max_step<0x141, 0xf>(m);   // row_half_mirror
+    m = dpp_max_step<0x140, 0xf>(m);   // row_mirror
+    m = dpp_max_step<0x142, 0xa>(m);   // row_bcast:15 into rows 1 and 3
+    m = dpp_max_step<0x143, 0xc>(m);   // row_bcast:31 into rows 2 and 3
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, m), 63));
+}
+
 // 2^k for an integer |k| <= 126, built from its exponent field
 __device__ __forceinline__ float pow2(int k) { return __builtin_bit_cast(float, (k + 127) << 23); }
 
@@ -565,8 +585,7 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
             m = __builtin_fmaxf(m, __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(t[o][0]), __builtin_fabsf(t[o][1])),
                                                    __builtin_fmaxf(__builtin_fabsf(t[o][2]), __builtin_fabsf(t[o][3]))));
         });
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) m = __builtin_fmaxf(m, __shfl_xor(m, o));
+        m = wave_max_dpp(m);
         int e = 0;
         if (m > 0.f && m <= 3.4028235e38f) {
             const int be = (int)((__builtin_bit_cast(uint32_t, m) >> 23) & 0xff);
