@@ -982,9 +982,14 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
             // overestimate what is left, and iterations enqueued past the end
             // (they find p_eff = 0 on the device and return at once) still cost
             // a dispatch each.  Iterations still queued count against it.
+            // The first batch adds one iteration more than the first window's
+            // slide of one requires: the host then decides the second batch
+            // from two finished iterations (the mean stride) while a third
+            // still runs, instead of draining the stream and leaving the GPU
+            // idle; it is wasted only when the loop ends within two iterations.
             const int in_flight = issued - k_host;
             int need = (T - t_host + pc - 1) / pc;
-            if (issued == 0 && T > 1) need = 1 + (T - 1 + pc - 1) / pc;
+            if (issued == 0 && T > 1) need = 2 + (T - 1 + pc - 1) / pc;
             const int first_stride = hs->first_stride;
             if (k_host >= 2 && t_host > first_stride) {
                 const double mean = (double)(t_host - first_stride) / (double)(k_host - 1);
