@@ -67,10 +67,50 @@ __device__ inline void mirror_state(const LoopState& v, LoopState* host) {
     __threadfence_system();
 }
 
+// The start of a Picard run: the loop state and the first window's row
+// descriptors, every window point a copy of x_0 (slot 0).  model_t_next and
+// nrow2: Heun only (nullptr otherwise), the network timestep of each window
+// row's next step and its per-window copy.  Run by the threads of one block.
+struct PicardInit {
+    LoopState* st;
+    int32_t* slot;
+    int32_t* nrow;
+    const int32_t* model_t;
+    const int32_t* model_t_next;
+    int32_t* nrow2;
+    int32_t T, p;
+};
+__device__ inline void picard_init_body(const PicardInit& a) {
+    const int pe = a.p < a.T ? a.p : a.T;
+    if (threadIdx.x == 0) {
+        a.st->t = 0;
+        a.st->k = 0;
+        a.st->f = 0;
+        a.st->p_eff = pe;
+        a.st->status = PD_OK;
+        a.st->first_stride = 0;
+        a.st->nrows = pe;
+        a.st->evals = 0;
+    }
+    for (int j = threadIdx.x; j < pe; j += blockDim.x) {
+        a.slot[j] = 0;
+        a.nrow[j] = a.model_t[j];
+        if (a.nrow2) a.nrow2[j] = a.model_t_next[j];
+    }
+}
+
 // ---------------------------------------------------------------- kernels
 // rng.hip
 void launch_normals(uint64_t seed, uint32_t rng_stream, int64_t count, const float* scale,
                     int64_t per_scale, float* out, hipStream_t s);
+// A sample's up-front draws in one launch: the prior x_0 (counter stream 0, BD
+// values into x0) and, when noise is given, every step's noise (stream 1,
+// noise_count values, value i scaled by scale[i / per_scale]); the values are
+// those of launch_normals with the same streams.  When init is given, the
+// first block also starts the Picard loop (picard_init_body).
+void launch_sample_setup(uint64_t seed, int64_t BD, float* x0, int64_t noise_count,
+                         const float* scale, int64_t per_scale, float* noise,
+                         const PicardInit* init, hipStream_t s);
 
 // gmm.hip: exact epsilon of an isotropic 2-D Gaussian mixture.
 struct GmmParams {
@@ -144,11 +184,6 @@ bool conv_supported(int C, int width, bool bf16);
 void launch_conv1x1(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s);
 
 // picard.hip
-// model_t_next / nrow2: Heun only (nullptr otherwise), the network timestep of
-// each window row's next step and its per-window copy.
-void launch_picard_init(LoopState* st, int32_t* slot, int32_t* nrow, const int32_t* model_t,
-                        const int32_t* model_t_next, int32_t* nrow2, int T, int p,
-                        hipStream_t s);
 // Heun on the window: Euler prediction of every row, then eps <- (eps + eps2)/2
 // for every row but the last step.
 void launch_heun_predict(const LoopState* st, const float* ring, const float* eps, const float* A,

@@ -75,30 +75,6 @@ __device__ __forceinline__ float drift(float A, float x, float B, float e) {
     return __fadd_rn(__fmul_rn(A, x), __fmul_rn(B, e));
 }
 
-// model_t_next / nrow2 (Heun only, else nullptr): the network timestep of the
-// step after each window row, for the second evaluation at the Euler prediction.
-__global__ void k_picard_init(LoopState* st, int32_t* slot, int32_t* nrow,
-                              const int32_t* __restrict__ model_t,
-                              const int32_t* __restrict__ model_t_next, int32_t* nrow2, int T,
-                              int p) {
-    const int pe = p < T ? p : T;
-    if (threadIdx.x == 0) {
-        st->t = 0;
-        st->k = 0;
-        st->f = 0;
-        st->p_eff = pe;
-        st->status = PD_OK;
-        st->first_stride = 0;
-        st->nrows = pe;
-        st->evals = 0;
-    }
-    for (int j = threadIdx.x; j < pe; j += blockDim.x) {
-        slot[j] = 0;            // every initial window point is a copy of x_0
-        nrow[j] = model_t[j];
-        if (nrow2) nrow2[j] = model_t_next[j];
-    }
-}
-
 // Heun's method, window side (rows j < p_eff of the current window):
 // predict:  xt[j] = x_{t+j} + (A x_{t+j} + B eps[j])      (the Euler step)
 // combine:  eps[j] = (eps[j] + eps2[j]) / 2  for every step but the last, so
@@ -686,14 +662,6 @@ int picard_scan_cols(int64_t D, int batch) {
 int picard_partial_blocks(int64_t D, int batch) {
     const int64_t cols = picard_scan_cols(D, batch);
     return (int)((D + cols - 1) / cols);
-}
-
-void launch_picard_init(LoopState* st, int32_t* slot, int32_t* nrow, const int32_t* model_t,
-                        const int32_t* model_t_next, int32_t* nrow2, int T, int p,
-                        hipStream_t s) {
-    hipLaunchKernelGGL(k_picard_init, dim3(1), dim3(256), 0, s, st, slot, nrow, model_t,
-                       model_t_next, nrow2, T, p);
-    PD_HIP(hipGetLastError());
 }
 
 static unsigned stream_blocks(int64_t n) {

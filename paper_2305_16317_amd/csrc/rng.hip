@@ -30,14 +30,13 @@ __device__ __forceinline__ void philox4x32_10(uint32_t& c0, uint32_t& c1, uint32
     }
 }
 
-__global__ __launch_bounds__(256) void k_normals(uint64_t seed, uint32_t rng_stream,
-                                                 int64_t count, const float* __restrict__ scale,
-                                                 int64_t per_scale, float* __restrict__ out) {
-    const int64_t nq = (count + 3) / 4;
-    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+// Values 4q .. 4q + 3 of counter stream rng_stream (those below count) into out.
+__device__ __forceinline__ void normals_quad(uint64_t seed, uint32_t rng_stream, int64_t q,
+                                             int64_t count, const float* __restrict__ scale,
+                                             int64_t per_scale, float* __restrict__ out) {
     const double kTwoPi = 6.283185307179586;   // 2 * pi in double
     const double kInv32 = 2.3283064365386963e-10;   // 2^-32
-    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < nq; q += step) {
+    {
         uint32_t c0 = (uint32_t)q, c1 = (uint32_t)((uint64_t)q >> 32), c2 = rng_stream, c3 = 0;
         philox4x32_10(c0, c1, c2, c3, (uint32_t)seed, (uint32_t)(seed >> 32));
         const double u0 = ((double)c0 + 0.5) * kInv32;
@@ -66,6 +65,29 @@ __global__ __launch_bounds__(256) void k_normals(uint64_t seed, uint32_t rng_str
     }
 }
 
+__global__ __launch_bounds__(256) void k_normals(uint64_t seed, uint32_t rng_stream,
+                                                 int64_t count, const float* __restrict__ scale,
+                                                 int64_t per_scale, float* __restrict__ out) {
+    const int64_t nq = (count + 3) / 4;
+    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < nq; q += step)
+        normals_quad(seed, rng_stream, q, count, scale, per_scale, out);
+}
+
+// Quads [0, nq0) of stream 0 go to x0, the next ones to the noise (stream 1).
+__global__ __launch_bounds__(256) void k_sample_setup(uint64_t seed, int64_t BD, float* __restrict__ x0,
+                                                      int64_t noise_count, const float* __restrict__ scale,
+                                                      int64_t per_scale, float* __restrict__ noise,
+                                                      PicardInit init, int has_init) {
+    if (has_init && blockIdx.x == 0) picard_init_body(init);
+    const int64_t nq0 = (BD + 3) / 4, nq = nq0 + (noise_count + 3) / 4;
+    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < nq; q += step) {
+        if (q < nq0) normals_quad(seed, 0, q, BD, nullptr, 1, x0);
+        else normals_quad(seed, 1, q - nq0, noise_count, scale, per_scale, noise);
+    }
+}
+
 }  // namespace
 
 void launch_normals(uint64_t seed, uint32_t rng_stream, int64_t count, const float* scale,
@@ -76,6 +98,20 @@ void launch_normals(uint64_t seed, uint32_t rng_stream, int64_t count, const flo
     if (blocks > 65536) blocks = 65536;
     hipLaunchKernelGGL(k_normals, dim3((unsigned)blocks), dim3(256), 0, s, seed, rng_stream,
                        count, scale, per_scale, out);
+    PD_HIP(hipGetLastError());
+}
+
+void launch_sample_setup(uint64_t seed, int64_t BD, float* x0, int64_t noise_count,
+                         const float* scale, int64_t per_scale, float* noise,
+                         const PicardInit* init, hipStream_t s) {
+    if (!noise) noise_count = 0;
+    const int64_t nq = (BD + 3) / 4 + (noise_count + 3) / 4;
+    int64_t blocks = (nq + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    if (blocks < 1) blocks = 1;
+    const PicardInit none{};
+    hipLaunchKernelGGL(k_sample_setup, dim3((unsigned)blocks), dim3(256), 0, s, seed, BD, x0,
+                       noise_count, scale, per_scale, noise, init ? *init : none, init ? 1 : 0);
     PD_HIP(hipGetLastError());
 }
 

@@ -778,11 +778,12 @@ static pd_workspace* use_workspace(pd_workspace* ws, std::unique_ptr<pd_workspac
     return own.get();
 }
 
-static void draw_noise(pd_workspace& w, uint64_t seed, hipStream_t st) {
+// x_0 into ring slot 0 and every step's noise, in one launch that also starts
+// the Picard loop when init is given
+static void draw_noise(pd_workspace& w, uint64_t seed, const PicardInit* init, hipStream_t st) {
     const int64_t BD = (int64_t)w.batch * w.D;
-    launch_normals(seed, 0, BD, nullptr, 1, w.ring.as<float>(), st);   // x_0 into slot 0
-    if (w.noise.p)
-        launch_normals(seed, 1, (int64_t)w.T * BD, w.zstd.as<float>(), BD, w.noise.as<float>(), st);
+    launch_sample_setup(seed, BD, w.ring.as<float>(), (int64_t)w.T * BD, w.zstd.as<float>(), BD,
+                        w.noise.as<float>(), init, st);
 }
 
 static void fill_stats(pd_sample_stats* stats, int iters, int64_t evals, int batch, bool guided,
@@ -866,7 +867,7 @@ extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoise
         KernelTimer tm;
         tm.on = stats && stats->time_kernels;
         tm.st = st;
-        draw_noise(w, noise_seed, st);
+        draw_noise(w, noise_seed, nullptr, st);
         if (use_fused_gmm_loop(*s, *d, s->T, 1, batch)) {
             tm.mark(-1);
             launch_gmm_sequential_loop(gmm_loop_args(*s, *d, w, 1, batch, StopTest{0.f, 2.f}, x_out), st);
@@ -936,8 +937,13 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         KernelTimer tm;
         tm.on = stats && stats->time_kernels;
         tm.st = st;
-        draw_noise(w, noise_seed, st);
-        if (use_fused_gmm_loop(*s, *d, T, pc, batch)) {
+        const bool fused_gmm = use_fused_gmm_loop(*s, *d, T, pc, batch);
+        const int32_t* mtn = s->heun ? w.model_t_next.as<int32_t>() : nullptr;
+        int32_t* nrow2 = s->heun ? w.nrow2.as<int32_t>() : nullptr;
+        const PicardInit init{dst, w.slot.as<int32_t>(), w.nrow.as<int32_t>(), w.model_t.as<int32_t>(),
+                              mtn, nrow2, T, pc};
+        draw_noise(w, noise_seed, fused_gmm ? nullptr : &init, st);
+        if (fused_gmm) {
             tm.mark(-1);
             launch_gmm_picard_loop(gmm_loop_args(*s, *d, w, pc, batch, stop, x_out), kFusedLoopLds,
                                    st);
@@ -948,10 +954,6 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
             fill_stats(stats, w.h_state->k, w.h_state->evals, batch, d->guided(), w.h_trace, tm);
             return;
         }
-        const int32_t* mtn = s->heun ? w.model_t_next.as<int32_t>() : nullptr;
-        int32_t* nrow2 = s->heun ? w.nrow2.as<int32_t>() : nullptr;
-        launch_picard_init(dst, w.slot.as<int32_t>(), w.nrow.as<int32_t>(),
-                           w.model_t.as<int32_t>(), mtn, nrow2, T, pc, st);
         const RowSrc src2{w.xt.as<float>(), nullptr, BD, batch, pc, nrow2, &dst->p_eff};
         const int hist = s->dpm ? 1 : 0;     // the multistep drift's row x_{t-1}
         const int slots = pc + 1 + hist;
