@@ -219,6 +219,9 @@ struct FinalizeArgs {
     int32_t* nrow2;                // Heun only, else nullptr
     int32_t ring_slots;            // p + 1, or p + 2 with a history row
     int32_t history;               // 1: the next batch starts with x_{t-1} (multistep drift)
+    const float* xT;               // x_T's ring slot
+    float* x_out;                  // [BD]: the iteration that reaches T copies x_T here
+    int64_t BD;                    // batch * D
 };
 // Scan + error partials of one iteration.  Returns true when the grid is a
 // single block, which then also ran the finalize step (from LDS).

@@ -163,6 +163,15 @@ __device__ void finalize_apply(const FinalizeArgs& a, int stride, int bad, const
         a.nrow[hn + j] = model_t(m);
         if (a.nrow2) a.nrow2[j] = model_t_next(m);
     }
+    // the iteration that reaches T copies x_T out, so the host needs no copy
+    // launch: its new points are this block's own stores (waited for here) or
+    // were made visible to it by kernel order or the count-in.  The condition
+    // is uniform over the block.
+    if (!bad && tn >= T) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        for (int64_t i = threadIdx.x; i < a.BD; i += blockDim.x) a.x_out[i] = a.xT[i];
+    }
 }
 
 // Tolerance of window offset o >= 1 (Algorithm 1's stride test compares the

@@ -957,11 +957,11 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         const RowSrc src2{w.xt.as<float>(), nullptr, BD, batch, pc, nrow2, &dst->p_eff};
         const int hist = s->dpm ? 1 : 0;     // the multistep drift's row x_{t-1}
         const int slots = pc + 1 + hist;
+        const float* xT = w.ring.as<float>() + (int64_t)(T % slots) * BD;
         const FinalizeArgs fin{dst, w.h_state_dev, w.partials.as<float>(), pc, batch, d->D, T,
                                w.tolv.as<float>(), stop.factor, stop.err_div, s->desc.tol_index_offset,
                                w.model_t.as<int32_t>(), w.h_trace_dev, w.slot.as<int32_t>(),
-                               w.nrow.as<int32_t>(), mtn, nrow2, slots, hist};
-        const float* xT = w.ring.as<float>() + (int64_t)(T % slots) * BD;
+                               w.nrow.as<int32_t>(), mtn, nrow2, slots, hist, xT, x_out, BD};
         const bool head = use_mlp_head(*s, *d, pc);
         const RowSrc src{w.ring.as<float>(), w.slot.as<int32_t>(), BD,     batch,
                          pc + hist,          w.nrow.as<int32_t>(), &dst->nrows};
@@ -1039,10 +1039,6 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                     }
                 }
                 issued += need;
-                // x_T's slot, copied out after every batch so that the last
-                // one needs no further round trip (earlier copies are
-                // overwritten)
-                PD_HIP(hipMemcpyAsync(x_out, xT, sizeof(float) * BD, hipMemcpyDeviceToDevice, st));
                 // every iteration but the batch's last has run: decide the
                 // next batch while that one runs
                 PD_HIP(hipEventSynchronize(w.batch_event));
@@ -1055,7 +1051,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
             t_host = hs->t;
             if (t_host >= T || hs->status != PD_OK) break;
         }
-        PD_HIP(hipStreamSynchronize(st));     // every queued launch and the copy of x_T
+        PD_HIP(hipStreamSynchronize(st));     // every queued launch (the last wrote x_T out)
         if (w.h_state->status != PD_OK) fail(PD_ERR_NUMERIC, "non-finite point or error in the window");
         if (w.h_state->t < T) fail(PD_ERR_DEVICE, "Picard loop did not reach T");
         const int iters = w.h_state->k;
