@@ -204,7 +204,8 @@ void pd_denoiser_destroy(pd_denoiser* d);
 
 /* eps[m] = eps(x[m], model_t[m]) for m in [0, M) (the network evaluations of
  * Algorithm 1's drift step).  x, eps: device float [M][D]; model_t: device
- * int32 [M], each in [0, T_train).  Enqueued on `stream` of the denoiser's
+ * int32 [M], each in [0, T_train); a value outside that range is clamped to
+ * it (the network's tables hold only those timesteps).  Enqueued on `stream` of the denoiser's
  * device; x and eps must not overlap.  M = 0 is a no-op.  Allocates nothing:
  * the MLP's hidden activations go through scratch the denoiser allocated at
  * creation (in chunks of 1024 rows), and calls on several threads or streams

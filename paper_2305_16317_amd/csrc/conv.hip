@@ -174,7 +174,7 @@ void k_conv_bf16(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
         const int g = (int)(T.row / src.group), bb = (int)(T.row % src.group);
         const int64_t sl = src.slot ? __builtin_amdgcn_readfirstlane(src.slot[g]) : g;
         T.x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
-        T.n = __builtin_amdgcn_readfirstlane(src.n[g]);
+        T.n = __builtin_amdgcn_readfirstlane(row_timestep(src, g));
         T.px = (int64_t)pt * 32 + (lane & 31);
         T.pxok = T.px < P;
         return T;
@@ -610,7 +610,7 @@ void k_conv_f32s(ConvArgs a, RowSrc src, float* __restrict__ eps, int tiles_per_
         const int g = (int)(T.row / src.group), bb = (int)(T.row % src.group);
         const int64_t sl = src.slot ? __builtin_amdgcn_readfirstlane(src.slot[g]) : g;
         T.x = src.base + sl * src.slot_stride + (int64_t)bb * C * P;
-        T.n = __builtin_amdgcn_readfirstlane(src.n[g]);
+        T.n = __builtin_amdgcn_readfirstlane(row_timestep(src, g));
         T.px = pt * 16 + lj;
         return T;
     };

@@ -83,7 +83,7 @@ __global__ __launch_bounds__(256) void k_gmm_eps(GmmParams g, RowSrc src,
     const int64_t sl = src.slot ? src.slot[gi] : gi;
     const float* x = src.base + sl * src.slot_stride + (int64_t)b * 2;
     float e0, e1;
-    gmm_eps_row(g, src.n[gi], x[0], x[1], e0, e1);
+    gmm_eps_row(g, row_timestep(src, gi), x[0], x[1], e0, e1);
     eps[r * 2] = e0;
     eps[r * 2 + 1] = e1;
 }

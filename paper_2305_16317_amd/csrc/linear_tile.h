@@ -73,7 +73,7 @@ __device__ __forceinline__ void linear_tile(const LinearArgs& a, const float* __
     float addv = 0.f;
     if (owner) {
         const int mc = min(em, M - 1), nc = min(en, N - 1);
-        addv = a.shift != nullptr ? a.shift[(int64_t)src.n[mc / src.group] * N + nc] : a.bias[nc];
+        addv = a.shift != nullptr ? a.shift[(int64_t)row_timestep(src, mc / src.group) * N + nc] : a.bias[nc];
     }
 
     // this wave's chunks: a contiguous run of 16-wide k chunks

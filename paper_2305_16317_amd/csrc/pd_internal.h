@@ -38,7 +38,15 @@ struct RowSrc {
     int32_t max_groups;
     const int32_t* n;
     const int32_t* active;
+    int32_t n_max;          // T_train - 1: the last timestep the network's tables hold
 };
+// Network timestep of row group g, clamped into the tables' range (a timestep
+// outside [0, T_train) from a caller gives the nearest end's network, never a
+// read past the tables).
+__device__ inline int row_timestep(const RowSrc& s, int64_t g) {
+    const int n = s.n[g];
+    return n < 0 ? 0 : (n > s.n_max ? s.n_max : n);
+}
 
 // Loop state of one Picard run, in device memory.
 struct LoopState {

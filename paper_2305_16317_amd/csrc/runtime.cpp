@@ -549,7 +549,7 @@ extern "C" pd_status pd_denoiser_forward(const pd_denoiser* d, const float* x,
         require(dev == d->device, "the denoiser lives on another device");
         const hipStream_t s = static_cast<hipStream_t>(stream);
         if (!d->scratch_floats(1)) {          // no scratch: one enqueue of the whole batch
-            const RowSrc src{x, nullptr, d->D, 1, (int32_t)M, model_t, nullptr};
+            const RowSrc src{x, nullptr, d->D, 1, (int32_t)M, model_t, nullptr, d->T_train - 1};
             d->forward(src, eps, nullptr, s);
             return;
         }
@@ -560,7 +560,8 @@ extern "C" pd_status pd_denoiser_forward(const pd_denoiser* d, const float* x,
         PD_HIP(hipStreamWaitEvent(s, d->fwd_done, 0));
         for (int64_t m0 = 0; m0 < M; m0 += kForwardRows) {
             const int64_t mc = M - m0 < kForwardRows ? M - m0 : kForwardRows;
-            const RowSrc src{x + m0 * d->D, nullptr, d->D, 1, (int32_t)mc, model_t + m0, nullptr};
+            const RowSrc src{x + m0 * d->D, nullptr, d->D, 1, (int32_t)mc, model_t + m0, nullptr,
+                             d->T_train - 1};
             d->forward(src, eps + m0 * d->D, d->fwd_scratch.as<float>(), s);
         }
         PD_HIP(hipEventRecord(d->fwd_done, s));
@@ -616,7 +617,7 @@ extern "C" pd_status pd_denoiser_forward_static(const pd_denoiser* d, const floa
         int dev = 0;
         PD_HIP(hipGetDevice(&dev));
         require(dev == d->device, "the denoiser lives on another device");
-        const RowSrc src{x, nullptr, d->D, 1, (int32_t)M, model_t, nullptr};
+        const RowSrc src{x, nullptr, d->D, 1, (int32_t)M, model_t, nullptr, d->T_train - 1};
         d->forward(src, eps, need ? static_scratch(dev) : nullptr, static_cast<hipStream_t>(stream));
     });
 }
@@ -882,13 +883,13 @@ extern "C" pd_status pd_sample_sequential(const pd_schedule* s, const pd_denoise
         tm.mark(-1);
         int64_t evals = 0;
         for (int i = 0; i < s->T; ++i) {
-            const RowSrc src{x, nullptr, BD, batch, 1, w.model_t.as<int32_t>() + i, nullptr};
+            const RowSrc src{x, nullptr, BD, batch, 1, w.model_t.as<int32_t>() + i, nullptr, d->T_train - 1};
             d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
             ++evals;
             if (s->heun && i + 1 < s->T) {     // Heun: second evaluation at the Euler prediction
                 launch_seq_heun_predict(x, w.eps.as<float>(), s->A[i], s->B[i], BD, w.xt.as<float>(), st);
                 const RowSrc src2{w.xt.as<float>(), nullptr, BD, batch, 1,
-                                  w.model_t_next.as<int32_t>() + i, nullptr};
+                                  w.model_t_next.as<int32_t>() + i, nullptr, d->T_train - 1};
                 d->forward(src2, w.eps2.as<float>(), w.scratch.as<float>(), st);
                 launch_seq_heun_combine(w.eps.as<float>(), w.eps2.as<float>(), BD, st);
                 ++evals;
@@ -954,7 +955,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
             fill_stats(stats, w.h_state->k, w.h_state->evals, batch, d->guided(), w.h_trace, tm);
             return;
         }
-        const RowSrc src2{w.xt.as<float>(), nullptr, BD, batch, pc, nrow2, &dst->p_eff};
+        const RowSrc src2{w.xt.as<float>(), nullptr, BD, batch, pc, nrow2, &dst->p_eff, d->T_train - 1};
         const int hist = s->dpm ? 1 : 0;     // the multistep drift's row x_{t-1}
         const int slots = pc + 1 + hist;
         const float* xT = w.ring.as<float>() + (int64_t)(T % slots) * BD;
@@ -964,7 +965,7 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                                w.nrow.as<int32_t>(), mtn, nrow2, slots, hist, xT, x_out, BD};
         const bool head = use_mlp_head(*s, *d, pc);
         const RowSrc src{w.ring.as<float>(), w.slot.as<int32_t>(), BD,     batch,
-                         pc + hist,          w.nrow.as<int32_t>(), &dst->nrows};
+                         pc + hist,          w.nrow.as<int32_t>(), &dst->nrows, d->T_train - 1};
         // The kernels write the loop state into host memory as they go, so
         // the host decides each next batch while the GPU still runs the
         // previous batch's last iteration (it waits on an event recorded
