@@ -192,12 +192,10 @@ bool conv_supported(int C, int width, bool bf16);
 void launch_conv1x1(const ConvArgs& a, const RowSrc& src, float* eps, hipStream_t s);
 
 // picard.hip
-// Heun on the window: Euler prediction of every row, then eps <- (eps + eps2)/2
-// for every row but the last step.
+// Heun on the window: Euler prediction of every row (the scan averages the
+// two evaluations, launch_picard_scan's eps2).
 void launch_heun_predict(const LoopState* st, const float* ring, const float* eps, const float* A,
                          const float* B, int p, int64_t BD, float* xt, hipStream_t s);
-void launch_heun_combine(const LoopState* st, float* eps, const float* eps2, int p, int T,
-                         int64_t BD, hipStream_t s);
 void launch_seq_heun_predict(const float* x, const float* eps, float A, float B, int64_t n,
                              float* xt, hipStream_t s);
 void launch_seq_heun_combine(float* eps, const float* eps2, int64_t n, hipStream_t s);
@@ -235,10 +233,12 @@ struct FinalizeArgs {
 // single block, which then also ran the finalize step (from LDS).
 // R, S: the multistep (DPM-Solver) coefficients of x_{i-1} and eps_{i-1}, or
 // nullptr; eps then has the history row first when st->nrows > st->p_eff.
+// eps2: Heun's second evaluations [p][BD], or nullptr; every row's drift then
+// takes the mean (eps + eps2) / 2 but at the chain's last step.
 bool launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
                         const float* A, const float* B, const float* R, const float* S, int p,
                         int batch, int64_t D, float* partials, const FinalizeArgs& fin,
-                        hipStream_t s);
+                        const float* eps2, hipStream_t s);
 void launch_picard_finalize(const FinalizeArgs& fin, hipStream_t s);
 // The MLP's last layer fused with the Picard update, error and finalize (Euler
 // drift, no history row): one launch in place of the last layer, the scan and

@@ -77,9 +77,9 @@ __device__ __forceinline__ float drift(float A, float x, float B, float e) {
 
 // Heun's method, window side (rows j < p_eff of the current window):
 // predict:  xt[j] = x_{t+j} + (A x_{t+j} + B eps[j])      (the Euler step)
-// combine:  eps[j] = (eps[j] + eps2[j]) / 2  for every step but the last, so
-//           that the scan's A x + B eps is A x + (B / 2)(eps + eps2) rounded
-//           exactly as written (halving is exact).
+// The scan then takes (eps[j] + eps2[j]) / 2 in place of eps[j] for every step
+// but the last, so that its A x + B eps is A x + (B / 2)(eps + eps2) rounded
+// exactly as written (halving is exact).
 __global__ __launch_bounds__(256) void k_heun_predict(const LoopState* __restrict__ st,
                                                       const float* __restrict__ ring,
                                                       const float* __restrict__ eps,
@@ -99,17 +99,6 @@ __global__ __launch_bounds__(256) void k_heun_predict(const LoopState* __restric
     }
 }
 
-__global__ __launch_bounds__(256) void k_heun_combine(const LoopState* __restrict__ st,
-                                                      float* __restrict__ eps,
-                                                      const float* __restrict__ eps2, int T,
-                                                      int64_t BD) {
-    const int pe = st->p_eff, t = st->t;
-    const int inner = t + pe < T ? pe : pe - 1;   // the last step keeps its Euler drift
-    const int64_t n = (int64_t)inner * BD;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x)
-        eps[i] = __fmul_rn(__fadd_rn(eps[i], eps2[i]), 0.5f);
-}
 
 // Barrier for LDS traffic only: global stores issued before it need not have
 // completed (later kernels read them, no wave of this block does).
@@ -392,7 +381,7 @@ __global__ __launch_bounds__(NW * 64) void k_picard_scan(
     const float* __restrict__ noise, const float* __restrict__ Atab,
     const float* __restrict__ Btab, const float* __restrict__ Rtab,
     const float* __restrict__ Stab, int p, int batch, int64_t D, float* __restrict__ partials,
-    FinalizeArgs fin, int fuse_finalize, int cpb) {
+    FinalizeArgs fin, int fuse_finalize, int cpb, const float* __restrict__ eps2) {
     typedef typename Cols<VEC>::type V;
     const LoopState cur = *st;
     const int pe = cur.p_eff;
@@ -465,6 +454,14 @@ __global__ __launch_bounds__(NW * 64) void k_picard_scan(
         const int sl = m <= f ? m % P1 : slot_f;      // points past f equal x_f
         xo[r] = *reinterpret_cast<const V*>(ring + (int64_t)sl * slotsz + col);
         y[r] = *reinterpret_cast<const V*>(eps + (int64_t)(j + hist) * slotsz + col);
+        if (eps2 != nullptr && m + 1 < fin.T) {
+            // Heun: the mean of the two evaluations, for every step but the
+            // chain's last (which keeps its Euler drift)
+            const V e2 = *reinterpret_cast<const V*>(eps2 + (int64_t)j * slotsz + col);
+#pragma unroll
+            for (int c = 0; c < VEC; ++c)
+                col_at<VEC>(y[r], c) = __fmul_rn(__fadd_rn(col_at<VEC>(y[r], c), col_at<VEC>(e2, c)), 0.5f);
+        }
         if constexpr (NOISE) z[r] = *reinterpret_cast<const V*>(noise + (int64_t)m * slotsz + col);
         else z[r] = V(0.f);
     }
@@ -685,12 +682,6 @@ void launch_heun_predict(const LoopState* st, const float* ring, const float* ep
     PD_HIP(hipGetLastError());
 }
 
-void launch_heun_combine(const LoopState* st, float* eps, const float* eps2, int p, int T,
-                         int64_t BD, hipStream_t s) {
-    hipLaunchKernelGGL(k_heun_combine, dim3(stream_blocks((int64_t)p * BD)), dim3(256), 0, s, st,
-                       eps, eps2, T, BD);
-    PD_HIP(hipGetLastError());
-}
 
 void launch_seq_heun_predict(const float* x, const float* eps, float A, float B, int64_t n,
                              float* xt, hipStream_t s) {
@@ -719,20 +710,20 @@ template <int NW, int R, int VEC>
 static bool launch_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
                         const float* A, const float* B, const float* Rt, const float* St, int p,
                         int batch, int64_t D, float* partials, const FinalizeArgs& fin,
-                        hipStream_t s) {
+                        const float* eps2, hipStream_t s) {
     const int cpb = picard_scan_cols(D, batch);
     const dim3 grid((unsigned)picard_partial_blocks(D, batch), (unsigned)batch);
     const int fuse = grid.x * grid.y == 1;   // one block: the finalize works from LDS
     const dim3 block(NW * 64);
     if (Rt)      // DPM-Solver integrates the noise-free chain
         hipLaunchKernelGGL((k_picard_scan<NW, R, VEC, false, true>), grid, block, 0, s, st, ring, eps,
-                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse, cpb);
+                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse, cpb, eps2);
     else if (noise)
         hipLaunchKernelGGL((k_picard_scan<NW, R, VEC, true, false>), grid, block, 0, s, st, ring, eps,
-                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse, cpb);
+                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse, cpb, eps2);
     else
         hipLaunchKernelGGL((k_picard_scan<NW, R, VEC, false, false>), grid, block, 0, s, st, ring, eps,
-                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse, cpb);
+                           noise, A, B, Rt, St, p, batch, D, partials, fin, fuse, cpb, eps2);
     PD_HIP(hipGetLastError());
     return fuse != 0;
 }
@@ -740,15 +731,16 @@ static bool launch_scan(const LoopState* st, float* ring, const float* eps, cons
 bool launch_picard_scan(const LoopState* st, float* ring, const float* eps, const float* noise,
                         const float* A, const float* B, const float* R, const float* S, int p,
                         int batch, int64_t D, float* partials, const FinalizeArgs& fin,
-                        hipStream_t s) {
+                        const float* eps2, hipStream_t s) {
     if (p > kMaxWindow) fail(PD_ERR_UNSUPPORTED, "window larger than 128 points");
     if (R && noise) fail(PD_ERR_INVALID_ARG, "the multistep drift is for the noise-free chain");
+    if (R && eps2) fail(PD_ERR_INVALID_ARG, "the multistep and Heun drifts do not combine");
     const bool v4 = scan_vec(D) == 4;
 #define PD_SCAN(NW, RR)                                                                          \
     return v4 ? launch_scan<NW, RR, 4>(st, ring, eps, noise, A, B, R, S, p, batch, D, partials, \
-                                       fin, s)                                                   \
+                                       fin, eps2, s)                                             \
               : launch_scan<NW, RR, 1>(st, ring, eps, noise, A, B, R, S, p, batch, D, partials, \
-                                       fin, s);
+                                       fin, eps2, s);
     if (p > 64) PD_SCAN(16, 8)
     const int ch = (p + 7) / 8;      // rows per wave at a full window, 8 waves
     if (ch <= 1) PD_SCAN(8, 1)

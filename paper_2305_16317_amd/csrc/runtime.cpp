@@ -1025,14 +1025,13 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                                             w.A.as<float>(), w.B.as<float>(), pc, BD,
                                             w.xt.as<float>(), st);
                         d->forward(src2, w.eps2.as<float>(), w.scratch.as<float>(), st);
-                        launch_heun_combine(dst, w.eps.as<float>(), w.eps2.as<float>(), pc, T, BD,
-                                            st);
                     }
                     tm.mark(CAT_DENOISER);
                     const bool fused = launch_picard_scan(
                         dst, w.ring.as<float>(), w.eps.as<float>(), w.noise.as<float>(),
                         w.A.as<float>(), w.B.as<float>(), w.Rt.as<float>(), w.St.as<float>(), pc,
-                        batch, d->D, w.partials.as<float>(), fin, st);
+                        batch, d->D, w.partials.as<float>(), fin,
+                        s->heun ? w.eps2.as<float>() : nullptr, st);   // Heun: the scan averages
                     tm.mark(CAT_UPDATE);
                     if (!fused) {
                         launch_picard_finalize(fin, st);
