@@ -682,7 +682,6 @@ void launch_heun_predict(const LoopState* st, const float* ring, const float* ep
     PD_HIP(hipGetLastError());
 }
 
-
 void launch_seq_heun_predict(const float* x, const float* eps, float A, float B, int64_t n,
                              float* xt, hipStream_t s) {
     if (n <= 0) return;

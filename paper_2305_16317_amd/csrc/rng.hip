@@ -36,32 +36,30 @@ __device__ __forceinline__ void normals_quad(uint64_t seed, uint32_t rng_stream,
                                              int64_t per_scale, float* __restrict__ out) {
     const double kTwoPi = 6.283185307179586;   // 2 * pi in double
     const double kInv32 = 2.3283064365386963e-10;   // 2^-32
-    {
-        uint32_t c0 = (uint32_t)q, c1 = (uint32_t)((uint64_t)q >> 32), c2 = rng_stream, c3 = 0;
-        philox4x32_10(c0, c1, c2, c3, (uint32_t)seed, (uint32_t)(seed >> 32));
-        const double u0 = ((double)c0 + 0.5) * kInv32;
-        const double u1 = ((double)c1 + 0.5) * kInv32;
-        const double u2 = ((double)c2 + 0.5) * kInv32;
-        const double u3 = ((double)c3 + 0.5) * kInv32;
-        const double r01 = sqrt(-2.0 * log(u0));
-        const double r23 = sqrt(-2.0 * log(u2));
-        double s1, co1, s3, co3;
-        sincos(kTwoPi * u1, &s1, &co1);
-        sincos(kTwoPi * u3, &s3, &co3);
-        float v[4] = {(float)(r01 * co1), (float)(r01 * s1), (float)(r23 * co3), (float)(r23 * s3)};
-        const int64_t base = 4 * q;
-        if (scale != nullptr) {
+    uint32_t c0 = (uint32_t)q, c1 = (uint32_t)((uint64_t)q >> 32), c2 = rng_stream, c3 = 0;
+    philox4x32_10(c0, c1, c2, c3, (uint32_t)seed, (uint32_t)(seed >> 32));
+    const double u0 = ((double)c0 + 0.5) * kInv32;
+    const double u1 = ((double)c1 + 0.5) * kInv32;
+    const double u2 = ((double)c2 + 0.5) * kInv32;
+    const double u3 = ((double)c3 + 0.5) * kInv32;
+    const double r01 = sqrt(-2.0 * log(u0));
+    const double r23 = sqrt(-2.0 * log(u2));
+    double s1, co1, s3, co3;
+    sincos(kTwoPi * u1, &s1, &co1);
+    sincos(kTwoPi * u3, &s3, &co3);
+    float v[4] = {(float)(r01 * co1), (float)(r01 * s1), (float)(r23 * co3), (float)(r23 * s3)};
+    const int64_t base = 4 * q;
+    if (scale != nullptr) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-                if (base + e < count) v[e] = scale[(base + e) / per_scale] * v[e];
-        }
-        if (base + 3 < count && (count & 3) == 0) {
-            *reinterpret_cast<float4*>(out + base) = make_float4(v[0], v[1], v[2], v[3]);
-        } else {
+        for (int e = 0; e < 4; ++e)
+            if (base + e < count) v[e] = scale[(base + e) / per_scale] * v[e];
+    }
+    if (base + 3 < count && (count & 3) == 0) {
+        *reinterpret_cast<float4*>(out + base) = make_float4(v[0], v[1], v[2], v[3]);
+    } else {
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-                if (base + e < count) out[base + e] = v[e];
-        }
+        for (int e = 0; e < 4; ++e)
+            if (base + e < count) out[base + e] = v[e];
     }
 }
 
@@ -74,7 +72,9 @@ __global__ __launch_bounds__(256) void k_normals(uint64_t seed, uint32_t rng_str
         normals_quad(seed, rng_stream, q, count, scale, per_scale, out);
 }
 
-// Quads [0, nq0) of stream 0 go to x0, the next ones to the noise (stream 1).
+// The prior (stream 0, BD values into x0) and then the noise (stream 1,
+// noise_count values) share one grid of quads; the first block also starts
+// the Picard loop when has_init is set.
 __global__ __launch_bounds__(256) void k_sample_setup(uint64_t seed, int64_t BD, float* __restrict__ x0,
                                                       int64_t noise_count, const float* __restrict__ scale,
                                                       int64_t per_scale, float* __restrict__ noise,
