@@ -10,6 +10,7 @@
 #include <string>
 #include <vector>
 
+#include "mlp.h"
 #include "pd_internal.h"
 
 namespace pd {
@@ -1019,13 +1020,22 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
                         tm.mark(CAT_UPDATE);
                         continue;
                     }
-                    d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
-                    if (s->heun) {   // second evaluation at every row's Euler prediction
-                        launch_heun_predict(dst, w.ring.as<float>(), w.eps.as<float>(),
-                                            w.A.as<float>(), w.B.as<float>(), pc, BD,
-                                            w.xt.as<float>(), st);
-                        d->forward(src2, w.eps2.as<float>(), w.scratch.as<float>(), st);
+                    if (s->heun && d->desc.kind == PD_MODEL_MLP) {
+                        // the MLP's last layer also writes every row's Euler prediction
+                        const HeunPredictArgs hp{dst, w.ring.as<float>(), w.A.as<float>(),
+                                                 w.B.as<float>(), slots, w.xt.as<float>()};
+                        launch_linear_dense_predict(d->mlp_head(),
+                                                    d->mlp_trunk(src, w.scratch.as<float>(), st),
+                                                    src, hp, w.eps.as<float>(), st);
+                    } else {
+                        d->forward(src, w.eps.as<float>(), w.scratch.as<float>(), st);
+                        if (s->heun)
+                            launch_heun_predict(dst, w.ring.as<float>(), w.eps.as<float>(),
+                                                w.A.as<float>(), w.B.as<float>(), pc, BD,
+                                                w.xt.as<float>(), st);
                     }
+                    // Heun: the second evaluation, at every row's Euler prediction
+                    if (s->heun) d->forward(src2, w.eps2.as<float>(), w.scratch.as<float>(), st);
                     tm.mark(CAT_DENOISER);
                     const bool fused = launch_picard_scan(
                         dst, w.ring.as<float>(), w.eps.as<float>(), w.noise.as<float>(),
