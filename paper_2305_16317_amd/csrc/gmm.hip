@@ -92,6 +92,27 @@ __device__ __forceinline__ float drift(float A, float x, float B, float e) {
     return __fadd_rn(__fmul_rn(A, x), __fmul_rn(B, e));
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave (every lane active): four
+// shift-right steps give the running sum within each row of 16 lanes (lanes
+// whose source lies before the row start add zero), then the last lane of
+// row 0 is added to row 1 and that of row 2 to row 3, and lane 31 (the total
+// of rows 0 and 1) to rows 2 and 3.  The additions are fixed, so the result
+// does not depend on timing.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_or_zero(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                                 ROW_MASK, 0xf, true));
+}
+__device__ __forceinline__ float wave_prefix_sum(float v) {
+    v = __fadd_rn(v, dpp_or_zero<0x111, 0xf>(v));   // row_shr:1
+    v = __fadd_rn(v, dpp_or_zero<0x112, 0xf>(v));   // row_shr:2
+    v = __fadd_rn(v, dpp_or_zero<0x114, 0xf>(v));   // row_shr:4
+    v = __fadd_rn(v, dpp_or_zero<0x118, 0xf>(v));   // row_shr:8
+    v = __fadd_rn(v, dpp_or_zero<0x142, 0xa>(v));   // row_bcast:15 into rows 1, 3
+    v = __fadd_rn(v, dpp_or_zero<0x143, 0xc>(v));   // row_bcast:31 into rows 2, 3
+    return v;
+}
+
 // Per trajectory index i, everything one step needs, staged in LDS by every
 // thread of the workgroup: drift coefficients, tolerance variance and the
 // network-timestep constants of the mixture's eps, plus the component means.
@@ -139,6 +160,10 @@ __global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noi
     __shared__ int s_stride, s_bad;
     const int tid = threadIdx.x, nth = blockDim.x;
     const int K = a.g.K;
+    // the window's running sums: a wave per column when every wave has at
+    // most two columns (the block is whole waves), else a thread per column
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), nwaves = nth / 64;
+    const bool wave_scan = BD <= 2 * nwaves;
     M mu;
     if constexpr (M::kBound > 0) mu.load(a.g.means, K);
     else mu.p = tb.means;
@@ -168,14 +193,33 @@ __global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noi
         __syncthreads();
         // Picard update: x_t + running sum of drifts + running sum of noise
         const float* z = noise_in_lds ? zw + t * BD : zw;
-        for (int c = tid; c < BD; c += nth) {
-            const float anchor = ring[(t % P1) * BD + c];
-            float sy = 0.f, sz = 0.f;
+        if (wave_scan) {
+            // one wave per column: the running sums of 64 rows at a time as a
+            // wave prefix sum, carried from one run of rows to the next
+            for (int c = wave; c < BD; c += nwaves) {
+                const float anchor = ring[(t % P1) * BD + c];
+                float cy = 0.f, cz = 0.f;
+                for (int j0 = 0; j0 < pe; j0 += 64) {
+                    const int j = j0 + lane;
+                    const bool in = j < pe;
+                    const float sy = __fadd_rn(cy, wave_prefix_sum(in ? y[j * BD + c] : 0.f));
+                    const float sz = __fadd_rn(cz, wave_prefix_sum(in ? z[j * BD + c] : 0.f));
+                    if (in) xn[j * BD + c] = __fadd_rn(__fadd_rn(anchor, sy), sz);
+                    cy = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sy), 63));
+                    cz = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sz), 63));
+                }
+            }
+        } else {
+            // one thread per column, in order along the window
+            for (int c = tid; c < BD; c += nth) {
+                const float anchor = ring[(t % P1) * BD + c];
+                float sy = 0.f, sz = 0.f;
 #pragma unroll 8
-            for (int j = 0; j < pe; ++j) {
-                sy = __fadd_rn(sy, y[j * BD + c]);
-                sz = __fadd_rn(sz, z[j * BD + c]);
-                xn[j * BD + c] = __fadd_rn(__fadd_rn(anchor, sy), sz);
+                for (int j = 0; j < pe; ++j) {
+                    sy = __fadd_rn(sy, y[j * BD + c]);
+                    sz = __fadd_rn(sz, z[j * BD + c]);
+                    xn[j * BD + c] = __fadd_rn(__fadd_rn(anchor, sy), sz);
+                }
             }
         }
         __syncthreads();

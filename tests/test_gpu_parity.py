@@ -260,6 +260,10 @@ SMALL = {
     # component counts past the register-held means (16) and between 8 and 16
     "gmm_k12": lambda: W.small_variant("gmm2d_ddpm100", p=20, batch=2, n_components=12),
     "gmm_k40": lambda: W.small_variant("gmm2d_ddpm100", p=33, batch=5, n_components=40),
+    # the fused loop's wave-per-column running sums: two columns per wave and
+    # one ragged run of rows; one column per wave and two full runs of 64
+    "gmm_wave_b2": lambda: W.small_variant("gmm2d_ddpm100", p=40, batch=2),
+    "gmm_wave_p128": lambda: W.small_variant("gmm2d_ddpm100", T=200, p=128, batch=1),
     "mlp_full": lambda: W.WORKLOADS["policy_mlp_ddpm100"],
     "mlp_small": lambda: W.small_variant("policy_mlp_ddpm100", T=30, p=9, shape=(4, 3), width=32, batch=2),
     # eight samples sharing the window: 40-row layer launches, any-of-batch strides
