@@ -141,8 +141,8 @@ def denoiser_roofline(wl, dtype: str, fl: float, seconds: float) -> dict:
 KERNEL_SOURCES = {"k_conv": ["conv.hip"], "k_picard": ["picard.hip", "linear_tile.h"],
                   "k_mlp_head": ["picard.hip", "linear_tile.h"],
                   "k_linear": ["mlp.hip", "linear_tile.h"],
-                  "k_gmm": ["gmm.hip"], "k_normals": ["rng.hip"],
-                  "k_sample_setup": ["rng.hip"]}
+                  "k_gmm": ["gmm.hip", "gmm.h", "philox.h"], "k_normals": ["rng.hip", "philox.h"],
+                  "k_sample_setup": ["rng.hip", "philox.h"]}
 
 
 def source_hash(kernel_tag: str) -> str:

@@ -4,7 +4,9 @@
 // per-timestep constants are float tables built in double on the host.
 // For this model the whole sampling loop (Picard or sequential) also runs in
 // a single workgroup: the state is a few KB and fits in LDS.
+#include "gmm.h"
 #include "pd_internal.h"
+#include "philox.h"
 
 namespace pd {
 namespace {
@@ -149,7 +151,7 @@ __device__ __forceinline__ float* gmm_stage(const GmmLoopArgs& g, float* sm, Gmm
 // then taken by one thread, in order along the window.  With `noise_in_lds`
 // all T noise vectors are staged once, else each window's are read from HBM.
 template <class M>
-__global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noise_in_lds) {
+__global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noise_in_lds, GmmDraw draw) {
     extern __shared__ float sm[];
     const int B = a.batch, P1 = a.p + 1, BD = 2 * B, T = a.T;
     GmmStepTables tb;
@@ -167,9 +169,29 @@ __global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noi
     M mu;
     if constexpr (M::kBound > 0) mu.load(a.g.means, K);
     else mu.p = tb.means;
-    for (int i = tid; i < BD; i += nth) ring[i] = a.x0[i];
-    if (noise_in_lds)
-        for (int i = tid; i < T * BD; i += nth) zw[i] = a.noise ? a.noise[i] : 0.f;
+    if (draw.on) {
+        // x_0 (stream 0) into ring slot 0 and every step's noise (stream 1)
+        // into LDS, four values per counter block
+        const int nq0 = (BD + 3) / 4, nq1 = (T * BD + 3) / 4;
+        for (int q = tid; q < nq0 + (draw.zstd ? nq1 : 0); q += nth) {
+            const bool prior = q < nq0;
+            const int qq = prior ? q : q - nq0;
+            float v[4];
+            normals4(draw.seed, prior ? 0u : 1u, qq, v);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int i = 4 * qq + e;
+                if (prior && i < BD) ring[i] = v[e];
+                if (!prior && i < T * BD) zw[i] = draw.zstd[i / BD] * v[e];
+            }
+        }
+        if (!draw.zstd)
+            for (int i = tid; i < T * BD; i += nth) zw[i] = 0.f;
+    } else {
+        for (int i = tid; i < BD; i += nth) ring[i] = a.x0[i];
+        if (noise_in_lds)
+            for (int i = tid; i < T * BD; i += nth) zw[i] = a.noise ? a.noise[i] : 0.f;
+    }
     int t = 0, k = 0, f = 0;
     int pe = a.p < T ? a.p : T;
     int64_t evals = 0;
@@ -338,23 +360,34 @@ size_t gmm_loop_lds_bytes(int T, int K, int p, int batch) {
     return sizeof(float) * picard_loop_floats(T, K, p, batch, false);
 }
 
+bool gmm_loop_stages_noise(int T, int K, int p, int batch, size_t max_lds) {
+    return sizeof(float) * picard_loop_floats(T, K, p, batch, true) <= max_lds;
+}
+
 void launch_gmm_picard_loop(const GmmLoopArgs& a, size_t max_lds, hipStream_t s) {
+    launch_gmm_picard_loop(a, GmmDraw{0, 0, nullptr}, max_lds, s);
+}
+
+void launch_gmm_picard_loop(const GmmLoopArgs& a, const GmmDraw& draw, size_t max_lds,
+                            hipStream_t s) {
     if (a.g.K > kMaxK) fail(PD_ERR_UNSUPPORTED, "gmm2d supports at most 64 components");
     const size_t full = sizeof(float) * picard_loop_floats(a.T, a.g.K, a.p, a.batch, true);
     const bool noise_in_lds = full <= max_lds;
+    if (draw.on && !noise_in_lds)
+        fail(PD_ERR_INVALID_ARG, "gmm2d loop: drawing the noise in the loop needs it all in LDS");
     const size_t lds = noise_in_lds ? full : gmm_loop_lds_bytes(a.T, a.g.K, a.p, a.batch);
     // enough waves for one drift per thread: fewer waves meet at the barriers
     const int64_t work = (int64_t)a.p * a.batch;
     const int threads = work < 1024 ? (int)((work + 63) / 64) * 64 : 1024;
     if (a.g.K <= 8)
         hipLaunchKernelGGL(k_gmm_picard_loop<MeansReg<8>>, dim3(1), dim3(threads), lds, s, a,
-                           (int)noise_in_lds);
+                           (int)noise_in_lds, draw);
     else if (a.g.K <= 16)
         hipLaunchKernelGGL(k_gmm_picard_loop<MeansReg<16>>, dim3(1), dim3(threads), lds, s, a,
-                           (int)noise_in_lds);
+                           (int)noise_in_lds, draw);
     else
         hipLaunchKernelGGL(k_gmm_picard_loop<MeansMem>, dim3(1), dim3(threads), lds, s, a,
-                           (int)noise_in_lds);
+                           (int)noise_in_lds, draw);
     PD_HIP(hipGetLastError());
 }
 

@@ -10,6 +10,7 @@
 #include <string>
 #include <vector>
 
+#include "gmm.h"
 #include "mlp.h"
 #include "pd_internal.h"
 
@@ -944,11 +945,16 @@ extern "C" pd_status pd_sample_picard(const pd_schedule* s, const pd_denoiser* d
         int32_t* nrow2 = s->heun ? w.nrow2.as<int32_t>() : nullptr;
         const PicardInit init{dst, w.slot.as<int32_t>(), w.nrow.as<int32_t>(), w.model_t.as<int32_t>(),
                               mtn, nrow2, T, pc};
-        draw_noise(w, noise_seed, fused_gmm ? nullptr : &init, st);
+        // the mixture's loop draws x_0 and the noise itself when all of it fits in its LDS
+        const bool draw_in_loop =
+            fused_gmm && gmm_loop_stages_noise(T, d->desc.n_components, pc, batch, kFusedLoopLds);
+        if (!draw_in_loop) draw_noise(w, noise_seed, fused_gmm ? nullptr : &init, st);
         if (fused_gmm) {
             tm.mark(-1);
-            launch_gmm_picard_loop(gmm_loop_args(*s, *d, w, pc, batch, stop, x_out), kFusedLoopLds,
-                                   st);
+            const GmmDraw draw{draw_in_loop ? 1 : 0, noise_seed,
+                               w.noise.p ? w.zstd.as<float>() : nullptr};
+            launch_gmm_picard_loop(gmm_loop_args(*s, *d, w, pc, batch, stop, x_out), draw,
+                                   kFusedLoopLds, st);
             tm.mark(CAT_UPDATE);
             PD_HIP(hipStreamSynchronize(st));     // the kernel wrote the state's host copy
             if (w.h_state->status != PD_OK) fail(PD_ERR_NUMERIC, "non-finite point or error in the window");
