@@ -262,7 +262,11 @@ typedef struct pd_sample_stats {
 /* With the MLP denoiser and the Euler drift (PD_DDPM, PD_DDIM) ParaDiGMS runs
  * the network's last layer inside the update launch, whose epilogue is the
  * Picard update, error and stride step: denoiser_ms then times the first three
- * layers, update_ms that fused launch, and finalize_launches is 0. */
+ * layers, update_ms that fused launch, and finalize_launches is 0.  With the
+ * 2-D mixture, when the sample's loop state fits in one workgroup, the whole
+ * loop (for Picard sampling also the up-front draws) is one launch:
+ * update_launches is 1, update_ms times it, and the denoiser and finalize
+ * counts are 0. */
 
 typedef struct pd_workspace pd_workspace;
 
