@@ -280,6 +280,12 @@ SMALL = {
                                   W.ModelSpec("conv1x1", (4, 4, 8), width=32), p=4, tau=0.1),
     "gmm_T2": lambda: W.Workload("t2", W.ScheduleSpec("ddpm", 2, 2), W.ModelSpec("gmm2d", (2,)),
                                  p=4, tau=0.1, batch=3),
+    # the mixture loop drawing its own prior without noise (DDIM) and with it
+    # (DDIM, eta > 0), on the wave-per-column running sums
+    "gmm_ddim": lambda: W.Workload("gmm_ddim", W.ScheduleSpec("ddim", 100, 50),
+                                   W.ModelSpec("gmm2d", (2,)), p=50, tau=0.1),
+    "gmm_ddim_eta": lambda: W.Workload("gmm_eta", W.ScheduleSpec("ddim", 200, 40, eta=0.5),
+                                       W.ModelSpec("gmm2d", (2,)), p=40, tau=0.1, batch=2),
     "conv_ddim_eta": lambda: W.Workload("eta", W.ScheduleSpec("ddim", 300, 30, eta=0.7),
                                         W.ModelSpec("conv1x1", (4, 6, 7), width=32), p=8,
                                         tau=0.1, batch=2),
@@ -371,7 +377,7 @@ def test_sequential_matches_oracle(name):
     assert _rel(got, ref) <= REL_F32
 
 
-@pytest.mark.parametrize("name", ["gmm_p7_b3", "gmm_k40", "mlp_small", "conv_ddpm", "conv_ddim_b3"])
+@pytest.mark.parametrize("name", ["gmm_p7_b3", "gmm_k40", "gmm_ddim", "gmm_ddim_eta", "mlp_small", "conv_ddpm", "conv_ddim_b3"])
 def test_window_of_one_is_sequential_bitwise(name):
     wl = SMALL[name]()
     w = W.make_weights(wl.model)
