@@ -620,6 +620,8 @@ HEUN = {
     # the mixture runs the general kernels here (its fused loop is Euler only)
     "heun_gmm": lambda: _heun(W.ModelSpec("gmm2d", (2,)), 40, 12, 2),
     "heun_mlp": lambda: _heun(W.ModelSpec("mlp", (4, 3), width=32), 30, 9, 2),
+    # the last layer's fused prediction over many row tiles, three samples a row group
+    "heun_mlp_wide": lambda: _heun(W.ModelSpec("mlp", (4, 5), width=32), 80, 64, 3),
     "heun_conv": lambda: _heun(W.ModelSpec("conv1x1", (4, 6, 7), width=32), 24, 8, 3),
     "heun_conv_full_window": lambda: _heun(W.ModelSpec("conv1x1", (4, 8, 8), width=64), 16, 16, 1),
 }
