@@ -148,7 +148,8 @@ __device__ __forceinline__ float* gmm_stage(const GmmLoopArgs& g, float* sm, Gmm
 // step tables, the window ring, the drift batch, the new points and the
 // noise live in LDS, the loop state in registers, and one launch runs every
 // iteration.  Drifts are formed in parallel; each column's running sums are
-// then taken by one thread, in order along the window.  With `noise_in_lds`
+// then taken by one wave as a prefix sum when no wave has more than two
+// columns, else by one thread in order along the window.  With `noise_in_lds`
 // all T noise vectors are staged once, else each window's are read from HBM.
 template <class M>
 __global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noise_in_lds, GmmDraw draw) {
