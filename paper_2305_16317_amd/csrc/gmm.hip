@@ -70,6 +70,48 @@ __device__ __forceinline__ void gmm_eps_core(const M& means, int K, float a, flo
     e1 = coef * (x1 - a * m1);
 }
 
+// The same eps with the components shared out over the four lanes of a quad
+// (lane q takes components q, q + 4, ..., the means read from LDS): the
+// largest logit and the three weighted sums are combined across the quad by
+// two exchange steps (lanes l ^ 1, then l ^ 2).  Each step adds a lane's value
+// to its partner's, and addition is commutative, so every lane of the quad
+// ends with the same sums and the same eps.  All four lanes must be active.
+template <int CTRL>
+__device__ __forceinline__ float quad_partner(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xf,
+                                                              0xf, false));
+}
+__device__ __forceinline__ void gmm_eps_quad(const float* means, int K, int q, float a,
+                                             float inv2s2, float coef, float x0, float x1,
+                                             float& e0, float& e1) {
+    auto logit = [&](int k) {
+        const float d0 = x0 - a * means[2 * k];
+        const float d1 = x1 - a * means[2 * k + 1];
+        return -(d0 * d0 + d1 * d1) * inv2s2;
+    };
+    float mx = -INFINITY;
+    for (int k = q; k < K; k += 4) mx = fmaxf(mx, logit(k));
+    mx = fmaxf(mx, quad_partner<0xb1>(mx));   // quad_perm [1, 0, 3, 2]
+    mx = fmaxf(mx, quad_partner<0x4e>(mx));   // quad_perm [2, 3, 0, 1]
+    float sw = 0.f, m0 = 0.f, m1 = 0.f;
+    for (int k = q; k < K; k += 4) {
+        const float w = expf(logit(k) - mx);
+        sw += w;
+        m0 += w * means[2 * k];
+        m1 += w * means[2 * k + 1];
+    }
+    sw += quad_partner<0xb1>(sw);
+    m0 += quad_partner<0xb1>(m0);
+    m1 += quad_partner<0xb1>(m1);
+    sw += quad_partner<0x4e>(sw);
+    m0 += quad_partner<0x4e>(m0);
+    m1 += quad_partner<0x4e>(m1);
+    m0 = m0 / sw;
+    m1 = m1 / sw;
+    e0 = coef * (x0 - a * m0);
+    e1 = coef * (x1 - a * m1);
+}
+
 __device__ __forceinline__ void gmm_eps_row(const GmmParams& g, int n, float x0, float x1,
                                             float& e0, float& e1) {
     gmm_eps_core(MeansMem{g.means}, g.K, g.a[n], g.inv2s2[n], g.coef[n], x0, x1, e0, e1);
@@ -167,6 +209,9 @@ __global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noi
     // most two columns (the block is whole waves), else a thread per column
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), nwaves = nth / 64;
     const bool wave_scan = BD <= 2 * nwaves;
+    // the components of a row over four lanes when the block has four
+    // threads for every row of a full window (gmm_loop_threads)
+    const bool quad = 4 * a.p * B <= nth;
     M mu;
     if constexpr (M::kBound > 0) mu.load(a.g.means, K);
     else mu.p = tb.means;
@@ -204,13 +249,27 @@ __global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noi
         if (!noise_in_lds)
             for (int i = tid; i < pe * BD; i += nth)
                 zw[i] = a.noise ? a.noise[(int64_t)t * BD + i] : 0.f;
-        for (int r = tid; r < pe * B; r += nth) {
-            const int j = r / B, b = r % B, m = t + j;
-            const float* x = ring + ((m <= f ? m : f) % P1) * BD + 2 * b;
-            float e0, e1;
-            gmm_eps_core(mu, K, tb.a[m], tb.inv2s2[m], tb.coef[m], x[0], x[1], e0, e1);
-            y[r * 2] = drift(tb.A[m], x[0], tb.B[m], e0);
-            y[r * 2 + 1] = drift(tb.A[m], x[1], tb.B[m], e1);
+        if (quad) {
+            // four lanes per window row (the launcher gives four threads a row)
+            for (int r = tid >> 2; r < pe * B; r += nth >> 2) {
+                const int j = r / B, b = r % B, m = t + j;
+                const float* x = ring + ((m <= f ? m : f) % P1) * BD + 2 * b;
+                float e0, e1;
+                gmm_eps_quad(tb.means, K, tid & 3, tb.a[m], tb.inv2s2[m], tb.coef[m], x[0], x[1], e0, e1);
+                if ((tid & 3) == 0) {
+                    y[r * 2] = drift(tb.A[m], x[0], tb.B[m], e0);
+                    y[r * 2 + 1] = drift(tb.A[m], x[1], tb.B[m], e1);
+                }
+            }
+        } else {
+            for (int r = tid; r < pe * B; r += nth) {
+                const int j = r / B, b = r % B, m = t + j;
+                const float* x = ring + ((m <= f ? m : f) % P1) * BD + 2 * b;
+                float e0, e1;
+                gmm_eps_core(mu, K, tb.a[m], tb.inv2s2[m], tb.coef[m], x[0], x[1], e0, e1);
+                y[r * 2] = drift(tb.A[m], x[0], tb.B[m], e0);
+                y[r * 2 + 1] = drift(tb.A[m], x[1], tb.B[m], e1);
+            }
         }
         if (tid == 0) s_stride = pe;
         __syncthreads();
@@ -299,8 +358,9 @@ __global__ __launch_bounds__(1024) void k_gmm_picard_loop(GmmLoopArgs a, int noi
     }
 }
 
-// The sequential chain for the 2-D mixture in one workgroup, one thread per
-// sample (its two coordinates never interact with other samples).  The noise
+// The sequential chain for the 2-D mixture in one workgroup, one thread, or
+// one quad of four lanes, per sample (its two coordinates never interact with
+// other samples).  The noise
 // of `chunk` steps at a time is staged in LDS by all threads together.
 template <class M>
 __global__ __launch_bounds__(1024) void k_gmm_sequential_loop(GmmLoopArgs a, int chunk) {
@@ -312,9 +372,13 @@ __global__ __launch_bounds__(1024) void k_gmm_sequential_loop(GmmLoopArgs a, int
     M mu;
     if constexpr (M::kBound > 0) mu.load(a.g.means, K);
     else mu.p = tb.means;
-    for (int b0 = 0; b0 < B; b0 += nth) {
-        const int nb = B - b0 < nth ? B - b0 : nth, b = b0 + tid;
-        const bool active = tid < nb;
+    // the components of a sample over four lanes when the block has four
+    // threads for every sample (gmm_loop_threads)
+    const bool quad = 4 * B <= nth;
+    const int per = quad ? nth >> 2 : nth, me = quad ? tid >> 2 : tid;   // samples per pass
+    for (int b0 = 0; b0 < B; b0 += per) {
+        const int nb = B - b0 < per ? B - b0 : per, b = b0 + me;
+        const bool active = me < nb;
         float x0 = 0.f, x1 = 0.f;
         if (active) {
             x0 = a.x0[2 * b];
@@ -332,19 +396,29 @@ __global__ __launch_bounds__(1024) void k_gmm_sequential_loop(GmmLoopArgs a, int
             for (int ii = 0; ii < n; ++ii) {
                 const int i = i0 + ii;
                 float e0, e1;
-                gmm_eps_core(mu, K, tb.a[i], tb.inv2s2[i], tb.coef[i], x0, x1, e0, e1);
-                const float* z = zs + (ii * nb + tid) * 2;
+                if (quad)
+                    gmm_eps_quad(tb.means, K, tid & 3, tb.a[i], tb.inv2s2[i], tb.coef[i], x0, x1, e0, e1);
+                else
+                    gmm_eps_core(mu, K, tb.a[i], tb.inv2s2[i], tb.coef[i], x0, x1, e0, e1);
+                const float* z = zs + (ii * nb + me) * 2;
                 const float v0 = __fadd_rn(__fadd_rn(x0, drift(tb.A[i], x0, tb.B[i], e0)), z[0]);
                 const float v1 = __fadd_rn(__fadd_rn(x1, drift(tb.A[i], x1, tb.B[i], e1)), z[1]);
                 x0 = v0;
                 x1 = v1;
             }
         }
-        if (active) {
+        if (active && (!quad || (tid & 3) == 0)) {
             a.out[2 * b] = x0;
             a.out[2 * b + 1] = x1;
         }
     }
+}
+
+// Threads of the two loops: four per row of a full window (Picard) or per
+// sample (sequential) when that fits one workgroup, else one.
+static int gmm_loop_threads(int64_t rows) {
+    const int64_t t = 4 * rows <= 1024 ? 4 * rows : rows;
+    return t < 1024 ? (int)((t + 63) / 64) * 64 : 1024;
 }
 
 }  // namespace
@@ -377,9 +451,9 @@ void launch_gmm_picard_loop(const GmmLoopArgs& a, const GmmDraw& draw, size_t ma
     if (draw.on && !noise_in_lds)
         fail(PD_ERR_INVALID_ARG, "gmm2d loop: drawing the noise in the loop needs it all in LDS");
     const size_t lds = noise_in_lds ? full : gmm_loop_lds_bytes(a.T, a.g.K, a.p, a.batch);
-    // enough waves for one drift per thread: fewer waves meet at the barriers
-    const int64_t work = (int64_t)a.p * a.batch;
-    const int threads = work < 1024 ? (int)((work + 63) / 64) * 64 : 1024;
+    // enough waves for one drift per four threads (or per thread): fewer
+    // waves meet at the barriers
+    const int threads = gmm_loop_threads((int64_t)a.p * a.batch);
     if (a.g.K <= 8)
         hipLaunchKernelGGL(k_gmm_picard_loop<MeansReg<8>>, dim3(1), dim3(threads), lds, s, a,
                            (int)noise_in_lds, draw);
@@ -394,7 +468,7 @@ void launch_gmm_picard_loop(const GmmLoopArgs& a, const GmmDraw& draw, size_t ma
 
 void launch_gmm_sequential_loop(const GmmLoopArgs& a, hipStream_t s) {
     if (a.g.K > kMaxK) fail(PD_ERR_UNSUPPORTED, "gmm2d supports at most 64 components");
-    const int threads = a.batch < 1024 ? ((a.batch + 63) / 64) * 64 : 1024;
+    const int threads = gmm_loop_threads(a.batch);
     const int per_step = 2 * (a.batch < threads ? a.batch : threads);
     const size_t tables = sizeof(float) * (6 * (size_t)a.T + 2 * (size_t)a.g.K);
     if (tables + sizeof(float) * per_step > kLoopLdsMax)
